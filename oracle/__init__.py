@@ -1,0 +1,145 @@
+"""ctypes wrapper of the fp64 CPU oracle.
+
+TEST INFRASTRUCTURE ONLY.  The oracle checks the GPU library; only the tests,
+the smoke check and the benchmark's CPU-baseline leg may import it.  It does
+not import the GPU package and the GPU package does not import it.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+from .build import LIB, build
+
+_lib = None
+
+
+def lib():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB):
+            build()
+        L = ctypes.CDLL(LIB)
+        dp = ctypes.POINTER(ctypes.c_double)
+        fp = ctypes.POINTER(ctypes.c_float)
+        ip = ctypes.POINTER(ctypes.c_int32)
+        L.orc_blob_size.restype = ctypes.c_size_t
+        L.orc_blob_size.argtypes = [ctypes.c_int, ctypes.c_int]
+        L.orc_sigmoid.restype = ctypes.c_double
+        L.orc_sigmoid.argtypes = [ctypes.c_double]
+        L.orc_silu.restype = ctypes.c_double
+        L.orc_silu.argtypes = [ctypes.c_double]
+        L.orc_linear.restype = None
+        L.orc_linear.argtypes = [dp, dp, dp, ctypes.c_int, ctypes.c_int, ctypes.c_int, dp]
+        L.orc_rmsnorm.restype = None
+        L.orc_rmsnorm.argtypes = [dp, dp, ctypes.c_int, ctypes.c_int, ctypes.c_double, dp]
+        for fn in (L.orc_scan_forward, L.orc_scan_backward):
+            fn.restype = None
+            fn.argtypes = [dp, dp, ctypes.c_int, ctypes.c_int, dp]
+        L.orc_track_forward.restype = ctypes.c_int
+        L.orc_track_forward.argtypes = [fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, dp, dp, dp]
+        L.orc_fit_tracks.restype = ctypes.c_long
+        L.orc_fit_tracks.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
+                                     ctypes.c_size_t, dp, ctypes.c_int]
+        L.orc_threads.restype = ctypes.c_int
+        L.orc_threads.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _d(a):
+    a = np.ascontiguousarray(a, dtype=np.float64)
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_double))
+
+
+def _f(a):
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    return a, a.ctypes.data_as(ctypes.POINTER(ctypes.c_float))
+
+
+def blob_size(n_layers: int, d: int) -> int:
+    return int(lib().orc_blob_size(n_layers, d))
+
+
+def sigmoid(v: float) -> float:
+    return lib().orc_sigmoid(float(v))
+
+
+def silu(v: float) -> float:
+    return lib().orc_silu(float(v))
+
+
+def linear(W, b, x):
+    """y[t] = b + W x[t] for rows x [n, n_in]; W [n_out, n_in]."""
+    W, pW = _d(W)
+    x, px = _d(np.atleast_2d(x))
+    n_out, n_in = W.shape
+    assert x.shape[1] == n_in
+    pb = None
+    if b is not None:
+        b, pb = _d(b)
+    y = np.empty((x.shape[0], n_out))
+    lib().orc_linear(pW, pb, px, x.shape[0], n_in, n_out, y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return y
+
+
+def rmsnorm(r, g, eps=1e-6):
+    r, pr = _d(np.atleast_2d(r))
+    g, pg = _d(g)
+    y = np.empty_like(r)
+    lib().orc_rmsnorm(pr, pg, r.shape[0], r.shape[1], eps, y.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return y
+
+
+def _scan(fn, x, a):
+    x, px = _d(x)
+    a, pa = _d(a)
+    assert x.shape == a.shape and x.ndim == 2
+    out = np.empty_like(x)
+    fn(px, pa, x.shape[0], x.shape[1], out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return out
+
+
+def scan_forward(x, a):
+    """Eq. (2) forward over rows of x, a [L, d]."""
+    return _scan(lib().orc_scan_forward, x, a)
+
+
+def scan_backward(x, a):
+    """Eq. (2) run from the last row to the first."""
+    return _scan(lib().orc_scan_backward, x, a)
+
+
+def track_forward(hits, blob, n_layers, d):
+    """One track: returns (out5, pooled [d], residual stream after the last layer [L, d])."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    blob, pb = _f(blob)
+    assert blob.size == blob_size(n_layers, d)
+    L = hits.shape[0]
+    out = np.empty(5)
+    pooled = np.empty(d)
+    resid = np.empty((max(L, 1), d))
+    dp = ctypes.POINTER(ctypes.c_double)
+    rc = lib().orc_track_forward(ph, L, n_layers, d, pb, out.ctypes.data_as(dp),
+                                 pooled.ctypes.data_as(dp), resid.ctypes.data_as(dp))
+    return out, pooled, (resid[:L] if rc == 0 else None)
+
+
+def fit_tracks(hits, offsets, blob, n_layers, d, n_threads=0):
+    """Packed batch: returns out [N, 5] float64 (NaN rows for tracks with no hits)."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    blob, pb = _f(blob)
+    n = offsets.size - 1
+    out = np.empty((max(n, 0), 5))
+    rc = lib().orc_fit_tracks(ph, offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n, n_layers, d,
+                              pb, blob.size, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(n_threads))
+    if rc < 0:
+        raise ValueError("oracle rejected its arguments")
+    return out
+
+
+def threads(n_threads=0) -> int:
+    return int(lib().orc_threads(int(n_threads)))

@@ -1,0 +1,292 @@
+"""Seeded synthetic inputs: helix tracks in a solenoid and random encoder weights.
+
+This module is shared by the tests, the benchmark and the CPU oracle's callers.
+It holds none of the encoder's arithmetic: it only draws track parameters,
+intersects helices with detector cylinders, and draws weight tensors.
+
+Tracks (stand-in for the paper's simulated muon samples, Sec. Data): a charged
+particle in a uniform field B along z follows a helix whose transverse radius is
+R = pT / (0.299792458 * B) metres (pT in GeV, B in tesla).  Each track is
+parameterised at its perigee by (d0, z0, phi, theta, q/p), the five quantities
+the method regresses (Sec. Method).  Hits are the intersections of the helix
+with barrel cylinders of fixed radius, ordered by increasing radius, which for
+these outgoing non-looping tracks is the time order the paper feeds the encoder
+(Sec. Data).  Each hit is smeared by 10 um along r*phi and along z.
+
+Packed layout (Sec. Kernel adaptation: packed, unpadded batches): hits of all
+tracks are concatenated into one float32 array [H, 3] of (x, y, z) in mm and
+track i owns rows offsets[i] .. offsets[i+1]-1 of it.
+
+Weights: one float32 blob in the canonical order documented in
+``blob_layout``; for bf16 workloads every value is rounded (round to nearest
+even) to a bf16-representable float32 before it is returned, so that the CPU
+oracle and the GPU library see identical weights.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+__all__ = [
+    "Workload", "WORKLOADS", "workload", "make_tracks", "make_track_chunk",
+    "make_weights", "blob_layout", "blob_size", "round_to_bf16", "TRACK_CHUNK",
+    "KAPPA_GEV_PER_T_M",
+]
+
+# pT [GeV] = KAPPA * B [T] * R [m] for a unit-charge particle.
+KAPPA_GEV_PER_T_M = 0.299792458
+# Tracks are generated in fixed chunks, each from its own seeded stream, so any
+# chunk (and therefore any subset of a large workload) can be regenerated alone.
+TRACK_CHUNK = 65536
+
+
+@dataclasses.dataclass(frozen=True)
+class Workload:
+    """One synthetic workload: model shape, number type and track sample."""
+    name: str
+    index: int            # 1-based; data seed 1000+index, weight seed 2000+index
+    n_layers: int
+    d_model: int
+    dtype: str            # "fp32" or "bf16"
+    n_tracks: int
+    len_min: int          # hits per track ~ U{len_min..len_max}
+    len_max: int
+    n_det_layers: int     # barrel cylinders, radii linearly spaced r_min..r_max
+    r_min: float = 30.0
+    r_max: float = 1000.0
+    z_max: float = 3000.0
+    b_field: float = 2.0  # tesla, along +z
+    pt_mode: str = "uniform_pt"   # "uniform_pt": pT~U(1,10); "uniform_invpt": 1/pT~U(0.1,1)
+    eta_max: float = 1.5
+    batch: int = 0        # tracks per fit_tracks call when the workload is streamed
+
+    @property
+    def data_seed(self) -> int:
+        return 1000 + self.index
+
+    @property
+    def weight_seed(self) -> int:
+        return 2000 + self.index
+
+
+WORKLOADS = {
+    w.name: w for w in [
+        Workload("tiny_d32_fp32", 1, n_layers=1, d_model=32, dtype="fp32", n_tracks=256,
+                 len_min=10, len_max=10, n_det_layers=10),
+        Workload("d128x4_fp32_65k", 2, n_layers=4, d_model=128, dtype="fp32", n_tracks=65536,
+                 len_min=8, len_max=20, n_det_layers=20),
+        Workload("d256x6_bf16_1m", 3, n_layers=6, d_model=256, dtype="bf16", n_tracks=1048576,
+                 len_min=8, len_max=30, n_det_layers=30),
+        Workload("long64_d128x4_bf16_200k", 4, n_layers=4, d_model=128, dtype="bf16",
+                 n_tracks=200000, len_min=64, len_max=64, n_det_layers=64),
+        Workload("deploy_d128x4_bf16_8m", 5, n_layers=4, d_model=128, dtype="bf16",
+                 n_tracks=8388608, len_min=8, len_max=20, n_det_layers=20,
+                 pt_mode="uniform_invpt", batch=262144),
+    ]
+}
+
+
+def workload(name_or_index) -> Workload:
+    if isinstance(name_or_index, Workload):
+        return name_or_index
+    if isinstance(name_or_index, int):
+        for w in WORKLOADS.values():
+            if w.index == name_or_index:
+                return w
+        raise KeyError(name_or_index)
+    return WORKLOADS[name_or_index]
+
+
+# ----------------------------------------------------------------------------
+# Helix tracks
+# ----------------------------------------------------------------------------
+
+def _streams(seed: int, chunk: int):
+    """One independent stream per drawn quantity, so that the first n draws of
+    every quantity do not depend on how many tracks are drawn."""
+    names = ("pt", "eta", "phi", "d0", "z0", "q", "length", "smear_rphi", "smear_z")
+    return {k: np.random.default_rng([seed, chunk, i]) for i, k in enumerate(names)}
+
+
+def _draw_params(w: Workload, rng, n: int):
+    if not isinstance(rng, dict):
+        rng = _streams(int(rng.integers(2 ** 31)), 0)
+    if w.pt_mode == "uniform_pt":
+        pt = rng["pt"].uniform(1.0, 10.0, n)
+    elif w.pt_mode == "uniform_invpt":
+        pt = 1.0 / rng["pt"].uniform(0.1, 1.0, n)
+    else:
+        raise ValueError(w.pt_mode)
+    eta = rng["eta"].uniform(-w.eta_max, w.eta_max, n)
+    phi = rng["phi"].uniform(-math.pi, math.pi, n)
+    d0 = rng["d0"].normal(0.0, 0.1, n)
+    z0 = rng["z0"].normal(0.0, 1.0, n)
+    q = np.where(rng["q"].random(n) < 0.5, -1.0, 1.0)
+    length = rng["length"].integers(w.len_min, w.len_max + 1, n)
+    return pt, eta, phi, d0, z0, q, length
+
+
+def helix_hits(pt, eta, phi, d0, z0, q, radii, b_field):
+    """Noise-free intersections of helices with cylinders.
+
+    Arrays of shape [n] for the track parameters and [m] for the radii; returns
+    x, y, z of shape [n, m] (mm) and the transverse arc length s [n, m].
+    The circle has radius R and centre C = (d0 + R/k) * n_hat with
+    n_hat = (-sin phi, cos phi) and k = -q (sense of rotation), so that the
+    perigee is P0 = d0 * n_hat with direction (cos phi, sin phi).  The turning
+    angle a at radius r follows from |C + Rot(k a)(P0 - C)| = r.
+    """
+    R = 1000.0 * pt / (KAPPA_GEV_PER_T_M * b_field)          # mm
+    k = -q
+    nx, ny = -np.sin(phi), np.cos(phi)
+    cs = d0 + R / k                                           # signed centre distance
+    cx, cy = cs * nx, cs * ny
+    D = np.abs(cs)
+    ux, uy = -(R / k) * nx, -(R / k) * ny                     # P0 - C
+    r = np.asarray(radii, dtype=np.float64)[None, :]
+    cos_a = (D[:, None] ** 2 + R[:, None] ** 2 - r ** 2) / (2.0 * R[:, None] * D[:, None])
+    if np.any(np.abs(cos_a) > 1.0):
+        raise ValueError("a helix does not reach a detector cylinder")
+    a = np.arccos(cos_a)
+    th = k[:, None] * a
+    c, s = np.cos(th), np.sin(th)
+    x = cx[:, None] + ux[:, None] * c - uy[:, None] * s
+    y = cy[:, None] + ux[:, None] * s + uy[:, None] * c
+    arc = R[:, None] * a
+    z = z0[:, None] + arc * np.sinh(eta)[:, None]
+    return x, y, z, arc
+
+
+def make_track_chunk(w: Workload, chunk: int, n: int, seed: int | None = None, smear: bool = True):
+    """Generate tracks chunk*TRACK_CHUNK .. +n-1 of a workload.
+
+    Returns (hits float32 [H,3], lengths int32 [n], truth float64 [n,5]) where
+    truth holds (d0, z0, phi, theta, q/p) at the perigee.
+    """
+    seed = w.data_seed if seed is None else seed
+    rng = _streams(seed, chunk)
+    pt, eta, phi, d0, z0, q, length = _draw_params(w, rng, n)
+    radii = np.linspace(w.r_min, w.r_max, w.n_det_layers)
+    x, y, z, _ = helix_hits(pt, eta, phi, d0, z0, q, radii, w.b_field)
+    if smear:
+        rphi = rng["smear_rphi"].normal(0.0, 0.010, x.shape)
+        dz = rng["smear_z"].normal(0.0, 0.010, x.shape)
+        ang = np.arctan2(y, x) + rphi / radii[None, :]
+        x = radii[None, :] * np.cos(ang)
+        y = radii[None, :] * np.sin(ang)
+        z = z + dz
+    if np.any(np.abs(z) > w.z_max):
+        raise ValueError("hit outside the detector length")
+    keep = np.arange(w.n_det_layers)[None, :] < length[:, None]
+    hits = np.stack([x[keep], y[keep], z[keep]], axis=1).astype(np.float32)
+    theta = 2.0 * np.arctan(np.exp(-eta))
+    p = pt * np.cosh(eta)
+    truth = np.stack([d0, z0, phi, theta, q / p], axis=1)
+    return hits, length.astype(np.int32), truth
+
+
+def make_tracks(w, n_tracks: int | None = None, seed: int | None = None, smear: bool = True,
+                with_truth: bool = False):
+    """Generate the first ``n_tracks`` tracks of a workload (default: all).
+
+    Returns (hits float32 [H,3], offsets int32 [N+1]) and, if requested, the
+    truth perigee parameters float64 [N,5].
+    """
+    w = workload(w)
+    n_tracks = w.n_tracks if n_tracks is None else int(n_tracks)
+    hits_parts, len_parts, truth_parts = [], [], []
+    done, chunk = 0, 0
+    while done < n_tracks:
+        n = min(TRACK_CHUNK, n_tracks - done)
+        h, l, t = make_track_chunk(w, chunk, n, seed, smear)
+        hits_parts.append(h)
+        len_parts.append(l)
+        truth_parts.append(t)
+        done += n
+        chunk += 1
+    lengths = np.concatenate(len_parts) if len_parts else np.zeros(0, np.int32)
+    offsets = np.zeros(n_tracks + 1, dtype=np.int64)
+    np.cumsum(lengths, out=offsets[1:])
+    if offsets[-1] >= 2 ** 31:
+        raise ValueError("too many hits for int32 offsets")
+    hits = np.concatenate(hits_parts) if hits_parts else np.zeros((0, 3), np.float32)
+    out = (np.ascontiguousarray(hits), offsets.astype(np.int32))
+    if with_truth:
+        out = out + (np.concatenate(truth_parts) if truth_parts else np.zeros((0, 5)),)
+    return out
+
+
+# ----------------------------------------------------------------------------
+# Weights
+# ----------------------------------------------------------------------------
+
+def blob_layout(n_layers: int, d: int):
+    """Canonical fp32 weight blob: list of (name, shape, fan_in, kind).
+
+    Matrices are row-major [out][in].  kind is "w" (normal, variance 1/fan_in),
+    "b" (uniform in +-fan_in^-1/2) or "g" (RMSNorm gain, uniform in [0.5, 1.5]).
+    Rows 0..d-1 of in.W/in.b give the candidate x, rows d..2d-1 the gate
+    pre-activation, rows 2d..3d-1 are present but unused.  Columns 0..d-1 of
+    out.W read the forward-scan state, columns d..2d-1 the backward-scan state.
+    Head outputs are ordered (d0, z0, phi, theta, q/p).
+    """
+    lay = [("embed.W", (d, 3), 3, "w"), ("embed.b", (d,), 3, "b")]
+    for l in range(n_layers):
+        p = f"layer{l}."
+        lay += [(p + "norm.g", (d,), d, "g"),
+                (p + "in.W", (3 * d, d), d, "w"), (p + "in.b", (3 * d,), d, "b"),
+                (p + "out.W", (d, 2 * d), 2 * d, "w"), (p + "out.b", (d,), 2 * d, "b")]
+    lay += [("head.W1", (d, d), d, "w"), ("head.b1", (d,), d, "b"),
+            ("head.W2", (5, d), d, "w"), ("head.b2", (5,), d, "b")]
+    return lay
+
+
+def blob_size(n_layers: int, d: int) -> int:
+    return int(sum(int(np.prod(s)) for _, s, _, _ in blob_layout(n_layers, d)))
+
+
+def round_to_bf16(a: np.ndarray) -> np.ndarray:
+    """Round float32 values to the nearest bf16 (ties to even), kept as float32."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32)
+
+
+def make_weights(w=None, *, n_layers: int | None = None, d: int | None = None,
+                 dtype: str | None = None, seed: int | None = None) -> np.ndarray:
+    """Draw the canonical weight blob from one PCG64 stream, in blob order."""
+    if w is not None:
+        w = workload(w)
+        n_layers = w.n_layers if n_layers is None else n_layers
+        d = w.d_model if d is None else d
+        dtype = w.dtype if dtype is None else dtype
+        seed = w.weight_seed if seed is None else seed
+    rng = np.random.Generator(np.random.PCG64(seed))
+    parts = []
+    for _, shape, fan_in, kind in blob_layout(n_layers, d):
+        n = int(np.prod(shape))
+        if kind == "w":
+            v = rng.normal(0.0, fan_in ** -0.5, n)
+        elif kind == "b":
+            v = rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n)
+        else:
+            v = rng.uniform(0.5, 1.5, n)
+        parts.append(v)
+    blob = np.concatenate(parts).astype(np.float32)
+    if dtype == "bf16":
+        blob = round_to_bf16(blob)
+    return blob
+
+
+def split_blob(blob: np.ndarray, n_layers: int, d: int) -> dict:
+    """View the blob as named arrays (float64 copies)."""
+    out, o = {}, 0
+    for name, shape, _, _ in blob_layout(n_layers, d):
+        n = int(np.prod(shape))
+        out[name] = np.asarray(blob[o:o + n], dtype=np.float64).reshape(shape)
+        o += n
+    assert o == blob.size
+    return out
