@@ -1,0 +1,223 @@
+#!/usr/bin/env python3
+"""Throughput of the fused track-fit encoder on one MI355X.
+
+One step = one pass of the whole forward path (embedding, all encoder layers,
+mean pool, head) over the workload's batch stream: for the deployment workload
+8,388,608 synthetic helix tracks in 32 fit_tracks calls of 262,144 tracks,
+captured once in a HIP graph and replayed.  Inputs are resident in HBM before
+the timed region.  Prints one JSON line.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ProcessPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import tracksynth as ts  # noqa: E402
+
+METRIC = "tracks/sec (encoder+head forward) on 1 MI355X; MFMA util / HBM GB/s vs peak"
+PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6, "bf16_f16act": 2516.6}  # dense MFMA, MI355X datasheet
+PEAK_HBM_GBS = 8000.0
+
+
+def algorithmic_flops(n_layers, d, n_hits, n_tracks):
+    """8 d^2 per hit and layer (candidate + gate projections: 2 * d * 2d, merge:
+    2 * 2d * d), 6 d per hit for the 3->d embedding, 2 d^2 + 10 d per track for
+    the head.  The unused third of the input projection is not counted."""
+    return 8.0 * d * d * n_layers * n_hits + 6.0 * d * n_hits + (2.0 * d * d + 10.0 * d) * n_tracks
+
+
+def algorithmic_bytes(n_hits, n_tracks):
+    """12 B per hit read, 4 B per track of offsets, 20 B per track written."""
+    return 12.0 * n_hits + 4.0 * (n_tracks + 1) + 20.0 * n_tracks
+
+
+def _chunk(args):
+    name, c, n = args
+    h, l, _ = ts.make_track_chunk(ts.workload(name), c, n)
+    return h, l
+
+
+def generate(w, n_tracks, workers):
+    chunks = []
+    done, c = 0, 0
+    while done < n_tracks:
+        n = min(ts.TRACK_CHUNK, n_tracks - done)
+        chunks.append((w.name, c, n))
+        done += n
+        c += 1
+    if workers > 1 and len(chunks) > 1:
+        with ProcessPoolExecutor(workers) as ex:
+            parts = list(ex.map(_chunk, chunks))
+    else:
+        parts = [_chunk(a) for a in chunks]
+    hits = np.concatenate([p[0] for p in parts])
+    lengths = np.concatenate([p[1] for p in parts])
+    offs = np.zeros(n_tracks + 1, np.int64)
+    np.cumsum(lengths, out=offs[1:])
+    return hits, offs.astype(np.int32)
+
+
+def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
+    """Time the fp64 oracle on a bounded, seeded sample of the same tracks."""
+    import oracle
+    n_all = offs.size - 1
+    rng = np.random.default_rng(7)
+    # calibrate on 256 tracks, then size the sample for about `seconds`
+    idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
+
+    def run(sel):
+        L = offs[sel + 1] - offs[sel]
+        h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+        o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+        t0 = time.perf_counter()
+        out = oracle.fit_tracks(h, o, blob, w.n_layers, w.d_model, n_threads=threads)
+        return out, time.perf_counter() - t0
+
+    _, dt = run(idx)
+    n = int(min(n_all, max(256, 256 * seconds / max(dt, 1e-3))))
+    sel = np.sort(rng.choice(n_all, size=n, replace=False))
+    ref, dt = run(sel)
+    g = gpu_out[sel].astype(np.float64)
+    rms = np.sqrt(np.mean(ref ** 2, axis=0))
+    err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), rms)))
+    return {"value": n / dt, "unit": "tracks/s", "cores": oracle.threads(threads), "kind": "oracle",
+            "sample": f"{n} tracks drawn without replacement (seed 7) from the {n_all}-track workload, "
+                      f"fp64 C oracle, {dt:.1f} s wall",
+            "parity_max_col_err_on_sample": err}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="deploy_d128x4_bf16_8m", choices=list(ts.WORKLOADS))
+    ap.add_argument("--mode", default=None, help="library mode: fp32, bf16 or bf16_f16act")
+    ap.add_argument("--n-tracks", type=int, default=None, help="override the workload's track count")
+    ap.add_argument("--batch", type=int, default=None, help="tracks per fit_tracks call")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the forward pass has no cross-track exchange, and "
+              "multi-GPU runs are not part of this build (shard the batch by offsets ranges "
+              "across processes instead).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2609_32479_amd as tf
+
+    w = ts.workload(args.workload)
+    mode = args.mode or tf.MODE_FOR_WEIGHTS[w.dtype]
+    n_tracks = args.n_tracks or w.n_tracks
+    batch = args.batch or (w.batch if w.batch else n_tracks)
+    workers = min(16, os.cpu_count() or 1)
+
+    t0 = time.perf_counter()
+    hits, offs = generate(w, n_tracks, workers)
+    blob = ts.make_weights(w)
+    print(f"[bench] generated {n_tracks} tracks / {hits.shape[0]} hits in {time.perf_counter() - t0:.1f} s",
+          file=sys.stderr, flush=True)
+
+    dev = torch.device("cuda:0")
+    h = torch.from_numpy(hits).to(dev)
+    o = torch.from_numpy(offs).to(dev)
+    out = torch.empty((n_tracks, 5), dtype=torch.float32, device=dev)
+    W = tf.Weights(blob, w.n_layers, w.d_model, mode)
+    starts = list(range(0, n_tracks, batch))
+
+    def step(stream=None):
+        for s0 in starts:
+            n = min(batch, n_tracks - s0)
+            tf.fit_tracks(h, o[s0:], W, out=out[s0:], n_tracks=n, stream=stream)
+
+    # per-launch kernel time, eager, with events on the launch stream
+    torch.cuda.synchronize()
+    step()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in starts]
+    for (a, b), s0 in zip(ev, starts):
+        a.record()
+        tf.fit_tracks(h, o[s0:], W, out=out[s0:], n_tracks=min(batch, n_tracks - s0))
+        b.record()
+    torch.cuda.synchronize()
+    launch_ms = np.array([a.elapsed_time(b) for a, b in ev])
+
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            step(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                step(side)
+        torch.cuda.synchronize()
+
+    def run_step():
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        run_step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_total = e0.elapsed_time(e1)
+    ms_per_step = ms_total / args.steps
+    value = n_tracks / (ms_per_step / 1e3)
+
+    flags = tf.device_error(W)
+    gpu_out = out.cpu().numpy()
+    n_hits = int(offs[-1] - offs[0])
+    flops_step = algorithmic_flops(w.n_layers, w.d_model, n_hits, n_tracks)
+    # dominant (only) kernel: algorithmic flops of one launch / its mean duration
+    per_launch_flops = flops_step / len(starts)
+    kernel_ms = float(launch_ms.mean())
+    achieved_tflops = per_launch_flops / (kernel_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[mode]
+    bytes_step = algorithmic_bytes(n_hits, n_tracks)
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "tracks/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"fp32": "f32", "bf16": "bf16", "bf16_f16act": "bf16 weights, f16 activations, f32 accumulate"}[mode],
+        "data": "synthetic helix tracks (2 T solenoid, seeded), random-init weights",
+        "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
+                   "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model, "mode": mode,
+                   "hip_graph": graph is not None},
+        "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
+                     "frac": achieved_tflops / peak, "traffic": None,
+                     "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
+                     "flops_per_launch": per_launch_flops},
+        "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
+                "frac": bytes_step / (ms_per_step / 1e3) / 1e9 / PEAK_HBM_GBS},
+        "host_wall_s": wall,
+        "device_error_flags": flags,
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(w, blob, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

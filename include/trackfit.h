@@ -1,0 +1,149 @@
+/*
+ * trackfit: batched inference of a bidirectional gated linear recurrent
+ * encoder that regresses the five perigee parameters (d0, z0, phi, theta, q/p)
+ * of a charged-particle track from its time-ordered hit sequence, on AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The method (paper "Fast and Precise Learned Charged-Particle Trajectory
+ * Regression at the Large Hadron Collider", Sec. Method and Sec. Encoder):
+ * each hit (x, y, z) is min-max normalised and embedded to width d; each of
+ * n_layers pre-norm layers applies RMSNorm, one linear projection to a
+ * candidate n_t and a gate pre-activation, z_t = sigmoid(gate), the update of
+ * Eq. (2) h_t = h_{t-1} + z_t (.) (n_t - h_{t-1}) run forward and in reverse
+ * from a zero state, and a linear merge of the two directions added to the
+ * residual stream; the stream is averaged over the track's hits and a
+ * two-layer head (SiLU between) gives five outputs.
+ *
+ * C ABI: plain pointers and sizes only.  Device pointers are HIP device
+ * memory of the current device; the library never synchronises the stream,
+ * never allocates inside fit_tracks, and may therefore be captured in a HIP
+ * graph.
+ */
+#ifndef TRACKFIT_H
+#define TRACKFIT_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    TF_OK = 0,
+    TF_EINVAL = -1,       /* a host-checkable argument is invalid; nothing was launched */
+    TF_ENOMEM = -2,       /* device or host allocation failed (tf_weights_create only) */
+    TF_EHIP = -3,         /* a HIP runtime call failed */
+    TF_EUNSUPPORTED = -4  /* valid request the library does not implement (e.g. d_model) */
+} tf_status;
+
+typedef enum { TF_FP32 = 0, TF_BF16 = 1, TF_BF16_F16ACT = 2 } tf_dtype;
+
+/* Model shape and number type.
+ * d_model: 32, 64, 128 or 256.  n_layers: 0..64.
+ * Projections run on matrix cores with fp32 accumulation in every mode; the
+ * gate, both scan states, the residual stream, the mean pool and the outputs
+ * are fp32 in every mode (Sec. Kernel adaptation: reduced-precision
+ * projections, fp32 recurrence).  The modes differ in the GEMM operands:
+ * TF_FP32         fp32 weights and activations.
+ * TF_BF16         bf16 weights; the normalised activations and the scan
+ *                 outputs are rounded to bf16 as GEMM operands.
+ * TF_BF16_F16ACT  bf16-valued weights (held exactly in fp16), activations
+ *                 rounded to fp16 (the paper's fp16 projections): same speed as
+ *                 TF_BF16 with 3 more mantissa bits on the activations.
+ * In both 16-bit modes the RMSNorm gain is folded into the input-projection
+ * weights (rounded once to the operand type) and the two head layers multiply
+ * their fp32 input as a high and a low 16-bit part. */
+typedef struct {
+    int32_t n_layers;
+    int32_t d_model;
+    int32_t dtype;    /* tf_dtype */
+    int32_t reserved; /* must be 0 */
+} tf_config;
+
+/* Opaque: device-resident weights in kernel order plus a sticky device error
+ * word.  Owned by the library. */
+typedef struct tf_weights tf_weights;
+
+/*
+ * Copy a canonical float32 weight blob to the current device.
+ *
+ * Blob order (matrices row-major [out][in]):
+ *   embed.W[d][3], embed.b[d],
+ *   per layer: norm.g[d], in.W[3d][d], in.b[3d], out.W[d][2d], out.b[d],
+ *   head.W1[d][d], head.b1[d], head.W2[5][d], head.b2[5].
+ * Rows 0..d-1 of in.W give the candidate, rows d..2d-1 the gate
+ * pre-activation, rows 2d..3d-1 are unused.  Columns 0..d-1 of out.W read the
+ * forward state, d..2d-1 the reverse state.  n_floats must equal
+ * tf_blob_size(n_layers, d_model).  In the 16-bit modes the matrix values
+ * should already be bf16-representable; others are rounded to nearest even.
+ *
+ * Ownership: host_blob is only read during the call.  *out receives a handle
+ * the caller frees with tf_weights_destroy.  Synchronous.
+ * Errors: TF_EINVAL (null pointers, bad sizes, reserved != 0),
+ * TF_EUNSUPPORTED (d_model or n_layers outside the supported set),
+ * TF_ENOMEM, TF_EHIP.  On error *out is set to NULL.
+ */
+tf_status tf_weights_create(const tf_config *cfg, const float *host_blob, size_t n_floats,
+                            tf_weights **out);
+
+/* Free a handle (NULL is a no-op).  Synchronises the device first. */
+void tf_weights_destroy(tf_weights *w);
+
+/* Number of floats of the canonical blob for a model shape (0 if invalid). */
+size_t tf_blob_size(int32_t n_layers, int32_t d_model);
+
+/* Longest track (in hits) the kernels accept for this handle: 64 for
+ * d_model <= 128 in the 16-bit modes and d_model <= 64 in TF_FP32, else 32.
+ * Longer tracks get NaN outputs and set TF_DEVERR_TOO_LONG. */
+int32_t tf_max_hits(const tf_weights *w);
+
+/*
+ * Fit a packed batch of tracks (Sec. Kernel adaptation: packed, unpadded
+ * layout; the problem statement of Sec. Method: one ordered hit sequence in,
+ * five perigee parameters out).
+ *
+ * hits     device, float32 [n_hits][3] = (x, y, z) in mm, time-ordered within
+ *          each track.  Read only.
+ * n_hits   rows of hits (bounds every read: a track whose rows leave
+ *          [0, n_hits) gets NaN outputs and sets TF_DEVERR_BAD_OFFSETS).
+ * offsets  device, int32 [n_tracks + 1]: track i owns rows
+ *          offsets[i] .. offsets[i+1]-1.  Non-decreasing; offsets[0] may be > 0
+ *          (absolute offsets into a larger array).  Read only.
+ * n_tracks host scalar >= 0.  0 is a no-op returning TF_OK.
+ * w        weights from tf_weights_create (same device).
+ * out      device, float32 [n_tracks][5]: d0, z0, phi, theta, q/p order.
+ *          Every row is written.  Must not overlap the inputs.
+ * stream   HIP stream (0 = null stream).
+ *
+ * Asynchronous: returns after enqueueing; no allocation, no host sync, so the
+ * call can be captured into a HIP graph.  Tracks with zero hits, more than
+ * tf_max_hits hits, a decreasing offset or rows outside [0, n_hits) get NaN
+ * outputs and set the sticky device error word (tf_get_device_error).
+ * A handle may be used from several streams at once.
+ * Errors: TF_EINVAL (null pointers with n_tracks > 0, n_tracks < 0,
+ * n_hits < 0), TF_EHIP (launch failure).
+ */
+tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                     const tf_weights *w, float *out, hipStream_t stream);
+
+/* Bits of the sticky device error word. */
+#define TF_DEVERR_EMPTY_TRACK 1   /* a track with zero hits */
+#define TF_DEVERR_TOO_LONG 2      /* a track longer than tf_max_hits */
+#define TF_DEVERR_BAD_OFFSETS 4   /* decreasing offsets or rows outside [0, n_hits) */
+
+/* Read (and if clear != 0, reset) the sticky device error word after the work
+ * already enqueued on stream.  Synchronises stream.  *flags receives the OR of
+ * TF_DEVERR_* bits seen since the last clear. */
+tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear);
+
+/* Static description of a status code. */
+const char *tf_status_string(tf_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* TRACKFIT_H */

@@ -1,0 +1,160 @@
+"""Python binding of libtrackfit (the gfx950 track-fit encoder).
+
+Argument marshalling only: every step of the forward pass runs in the HIP
+kernels behind the C ABI declared in include/trackfit.h.  PyTorch supplies
+device memory and streams.  There is no fallback: if the library is missing
+or the GPU is absent, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch  # noqa: F401  -- load torch's HIP runtime before the library (one runtime per process)
+
+__all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_size",
+           "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS",
+           "TrackfitError", "lib"]
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtrackfit.so")
+
+TF_OK, TF_EINVAL, TF_ENOMEM, TF_EHIP, TF_EUNSUPPORTED = 0, -1, -2, -3, -4
+TF_FP32, TF_BF16, TF_BF16_F16ACT = 0, 1, 2
+DTYPES = {"fp32": TF_FP32, "bf16": TF_BF16, "bf16_f16act": TF_BF16_F16ACT}
+# Library mode used for a model whose weights are given in the named type:
+# bf16 weights run with fp16 activation operands (see include/trackfit.h).
+MODE_FOR_WEIGHTS = {"fp32": "fp32", "bf16": "bf16_f16act"}
+DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS = 1, 2, 4
+
+EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_max_hits",
+            "fit_tracks", "tf_get_device_error", "tf_status_string")
+
+
+class TrackfitError(RuntimeError):
+    def __init__(self, status: int, what: str):
+        super().__init__(f"{what}: {_status_string(status)} ({status})")
+        self.status = status
+
+
+class Config(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libtrackfit.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: run __graft_entry__.build() first")
+        L = ctypes.CDLL(LIB_PATH)
+        vp = ctypes.c_void_p
+        L.tf_weights_create.restype = ctypes.c_int
+        L.tf_weights_create.argtypes = [ctypes.POINTER(Config), vp, ctypes.c_size_t, ctypes.POINTER(vp)]
+        L.tf_weights_destroy.restype = None
+        L.tf_weights_destroy.argtypes = [vp]
+        L.tf_blob_size.restype = ctypes.c_size_t
+        L.tf_blob_size.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        L.tf_max_hits.restype = ctypes.c_int32
+        L.tf_max_hits.argtypes = [vp]
+        L.fit_tracks.restype = ctypes.c_int
+        L.fit_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, vp]
+        L.tf_get_device_error.restype = ctypes.c_int
+        L.tf_get_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
+        L.tf_status_string.restype = ctypes.c_char_p
+        L.tf_status_string.argtypes = [ctypes.c_int]
+        _lib = L
+    return _lib
+
+
+def _status_string(status: int) -> str:
+    try:
+        return lib().tf_status_string(int(status)).decode()
+    except Exception:  # library itself unavailable
+        return "unknown"
+
+
+def _check(status: int, what: str):
+    if status != TF_OK:
+        raise TrackfitError(status, what)
+
+
+def blob_size(n_layers: int, d_model: int) -> int:
+    return int(lib().tf_blob_size(int(n_layers), int(d_model)))
+
+
+def _stream_handle(stream) -> int:
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return int(stream.cuda_stream) if hasattr(stream, "cuda_stream") else int(stream)
+
+
+class Weights:
+    """Device-resident weights (tf_weights handle) on the current device."""
+
+    def __init__(self, blob, n_layers: int, d_model: int, dtype: str = "fp32"):
+        """dtype: "fp32", "bf16" or "bf16_f16act" (library modes, include/trackfit.h)."""
+        import numpy as np
+        arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
+        cfg = Config(int(n_layers), int(d_model), DTYPES[dtype], 0)
+        h = ctypes.c_void_p()
+        _check(lib().tf_weights_create(ctypes.byref(cfg), arr.ctypes.data, arr.size, ctypes.byref(h)),
+               "tf_weights_create")
+        self._h = h
+        self.n_layers, self.d_model, self.dtype = int(n_layers), int(d_model), dtype
+        self.max_hits = int(lib().tf_max_hits(h))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().tf_weights_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def fit_tracks(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights, out: torch.Tensor | None = None,
+               n_tracks: int | None = None, stream=None) -> torch.Tensor:
+    """Enqueue one fit of a packed batch on ``stream`` (default: current stream).
+
+    hits    float32 [H, 3] on the GPU; offsets int32 [N+1] on the GPU (absolute
+    row offsets, may start above 0); returns out float32 [N, 5].  ``n_tracks``
+    defaults to offsets.numel() - 1 (a prefix of a longer offsets array may be
+    given instead).
+    """
+    if not (hits.is_cuda and offsets.is_cuda):
+        raise ValueError("hits and offsets must be GPU tensors")
+    if hits.dtype != torch.float32 or offsets.dtype != torch.int32:
+        raise TypeError("hits must be float32 and offsets int32")
+    if not (hits.is_contiguous() and offsets.is_contiguous()):
+        raise ValueError("hits and offsets must be contiguous")
+    if hits.dim() != 2 or hits.shape[1] != 3:
+        raise ValueError("hits must have shape [H, 3]")
+    n = offsets.numel() - 1 if n_tracks is None else int(n_tracks)
+    if n < 0 or n + 1 > offsets.numel():
+        raise ValueError("n_tracks does not fit the offsets array")
+    if out is None:
+        out = torch.empty((n, 5), dtype=torch.float32, device=hits.device)
+    elif not (out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and out.numel() >= 5 * n):
+        raise ValueError("out must be a contiguous float32 GPU tensor with room for [N, 5]")
+    _check(lib().fit_tracks(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, weights.handle,
+                            out.data_ptr(), _stream_handle(stream)), "fit_tracks")
+    return out
+
+
+def device_error(weights: Weights, stream=None, clear: bool = True) -> int:
+    """Sticky device error bits (DEVERR_*) seen since the last clear; syncs the stream."""
+    v = ctypes.c_int32(0)
+    _check(lib().tf_get_device_error(weights.handle, _stream_handle(stream), ctypes.byref(v), int(clear)),
+           "tf_get_device_error")
+    return int(v.value)

@@ -1,0 +1,860 @@
+// trackfit: fused gfx950 (CDNA4) kernel for batched inference of the
+// bidirectional gated linear recurrent track-fit encoder, and its C ABI.
+//
+// What is computed (paper: Sec. Method, Sec. Encoder, Eq. (2)): per track,
+// min-max normalised hits -> 3->d embedding -> n_layers x [RMSNorm -> one
+// projection to candidate x_t and gate pre-activation -> z_t = sigmoid ->
+// forward and reverse scans of h_t = h_{t-1} + z_t (x_t - h_{t-1}) ->
+// linear merge of both directions added to the residual stream] -> mean over
+// the track's hits -> W2 SiLU(W1 p + b1) + b2.
+//
+// How (Sec. Kernel adaptation is prior art for another GPU; this is a design
+// for CDNA4):
+//  * One wave64 owns a tile of whole tracks: up to CAP = 64 hits (32 at
+//    d = 256), packed greedily from the unpadded batch, at most 32 tracks.
+//    The residual stream of the tile (CAP x d fp32) stays in registers for all
+//    layers; nothing but hits, offsets and the five outputs touches HBM.
+//  * Projections run on 32x32 matrix cores: v_mfma_f32_32x32x16_bf16 for the
+//    bf16 model, v_mfma_f32_32x32x2_f32 for the fp32 model.  The residual
+//    stream is held transposed (channels on MFMA rows, hits on columns), which
+//    is exactly the A-operand layout of the input projection, so the norm
+//    output feeds the matrix core without any data movement.
+//  * The input projection puts hits on MFMA rows.  Hit slots are assigned to
+//    rows so that each lane's 16 accumulator rows per hit tile are consecutive
+//    hits of one of two streams (lanes 0-31: first half of the tile, lanes
+//    32-63: second half).  The scan along the track therefore runs serially in
+//    registers, one channel per lane; the single track that may straddle the
+//    two streams is finished with one cross-half exchange of the boundary
+//    state and a rerun of its steps in the second stream, so every track sees
+//    the same sequence of operations wherever it sits in a tile.
+//  * Scan outputs go through a wave-private LDS buffer once per 32-channel
+//    chunk (the only transpose), and the output projection for that chunk is
+//    accumulated straight into the residual registers (K split over chunks).
+//  * Mean pooling and the head run per tile on the same wave.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <vector>
+
+#include "trackfit.h"
+
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(8))) float f32x8;
+
+// Matrix-core operand types.  OP_F32: fp32 weights and operands
+// (v_mfma_f32_32x32x2_f32).  OP_BF16: bf16 weights and bf16 activation
+// operands (v_mfma_f32_32x32x16_bf16).  OP_F16: bf16-valued weights held
+// exactly in fp16 and fp16 activation operands (v_mfma_f32_32x32x16_f16).
+// Accumulation is fp32 in all three.
+enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRmsEps = 1e-6f;
+// |gate pre-activation| is clamped to 80 (scaled by log2 e) so that exp stays
+// finite; the change in the gate is below exp(-80).
+constexpr float kGateClamp = 80.0f * kLog2e;
+constexpr int kMaxTracksPerTile = 32;
+constexpr int kLdsBytesMax = 160 * 1024;
+
+constexpr int cmin(int a, int b) { return a < b ? a : b; }
+constexpr size_t round16(size_t v) { return (v + 15) & ~size_t(15); }
+
+// ---------------------------------------------------------------------------
+// Compile-time shape of one kernel instance.
+// ---------------------------------------------------------------------------
+template <int D, int OP>
+struct KCfg {
+    static constexpr bool HALF = OP != OP_F32;
+    // 32-hit tiles per wave tile: as many as the register file holds next to
+    // the residual stream (fp32 operands take twice the registers of bf16)
+    static constexpr int HT = (HALF ? D <= 128 : D <= 64) ? 2 : 1;
+    static constexpr int CAP = 32 * HT;          // hits per wave tile
+    static constexpr int SP = 16 * HT;           // positions per stream (2 streams)
+    static constexpr int MT = D / 32;            // 32-channel blocks
+    static constexpr int K = HALF ? 16 : 2;      // MFMA reduction depth
+    static constexpr int KL = K / 2;             // operand values per lane per k-step
+    static constexpr int KS1 = D / K;            // k-steps over d
+    static constexpr int KS2 = 64 / K;           // k-steps over one chunk of [f; b]
+    static constexpr int RPK = 16 / KL;          // k-steps per 16 accumulator rows
+    static constexpr int FBS = HALF ? 72 : 65;   // LDS row stride of [f; b] (elements)
+    static constexpr int STS = 33;               // LDS row stride of pooling stage (floats)
+    static constexpr int PLS = D + 4;            // LDS row stride of pooled / hidden (floats)
+    static constexpr size_t FB_BYTES = size_t(CAP) * FBS * (HALF ? 2 : 4);
+    static constexpr size_t ST_BYTES = size_t(CAP) * STS * 4;
+    static constexpr size_t POOL_OFF = round16(FB_BYTES > ST_BYTES ? FB_BYTES : ST_BYTES);
+    static constexpr size_t META_OFF = round16(POOL_OFF + size_t(kMaxTracksPerTile) * PLS * 4);
+    static constexpr size_t WAVE_BYTES = round16(META_OFF + 2 * kMaxTracksPerTile * 4);
+    static constexpr int WAVES = cmin(4, int(kLdsBytesMax / WAVE_BYTES));
+    static_assert(WAVES >= 1, "LDS budget");
+    static_assert(D % 32 == 0, "d must be a multiple of 32");
+};
+
+template <int OP> struct Frag;
+template <> struct Frag<OP_BF16> {
+    typedef bf16x8 T;
+    typedef __bf16 E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) {
+        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+        return __builtin_convertvector(f, bf16x8);
+    }
+};
+template <> struct Frag<OP_F16> {
+    typedef f16x8 T;
+    typedef _Float16 E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) {
+        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+        return __builtin_convertvector(f, f16x8);
+    }
+};
+template <> struct Frag<OP_F32> {
+    typedef float T;
+    typedef float E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) { return v[0]; }
+};
+
+// Device-side weights, already in the order the kernel reads them.
+struct DevParams {
+    const float4 *emb;   // [D] (w_x, w_y, w_z, b) with the min-max map folded in
+    const void *win;     // [L][NCH][2][KS1][64][KL]  candidate / gate B fragments
+    const float *bin;    // [L][2][D] candidate bias, gate bias (gate scaled by -log2 e)
+    const void *wout;    // [L][NCH][MT][KS2][64][KL]  output-projection A fragments
+    const float *bout;   // [L][D]
+    const void *w1;      // [MT][KS1][64][KL]  head layer 1 B fragments
+    const float *b1;     // [D]
+    const void *w2;      // [KS1][64][KL]      head layer 2 B fragments (cols >= 5 zero)
+    const float *b2;     // [5]
+    int n_layers;
+};
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Tile hit index held in hit slot s (0 <= s < CAP).  Slot s = 32 n + 8 i + 4 g + j
+// is row 8 i + 4 g + j of hit tile n in the input projection; that row lands
+// in lanes of half g at accumulator register 4 i + j, which is position
+// 16 n + 4 i + j of stream g, i.e. tile hit SP * g + 16 n + 4 i + j.
+template <int SP>
+__device__ __forceinline__ int slot_to_hit(int s) {
+    int n = s >> 5, i = (s >> 3) & 3, g = (s >> 2) & 1, j = s & 3;
+    return SP * g + 16 * n + 4 * i + j;
+}
+
+// The head multiplies fp32 vectors (pooled stream, hidden layer) by the
+// weights: with 16-bit operands each vector is split into a rounded high part
+// and the rounded remainder, and both are multiplied (the weights are exact in
+// the operand type), so the head keeps about 16 significant bits.
+template <class F>
+__device__ __forceinline__ void split_operand(const float *v, typename F::T &hi, typename F::T &lo) {
+    hi = F::pack(v);
+    if constexpr (sizeof(typename F::E) == 2) {
+        float r[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) r[u] = v[u] - (float)hi[u];
+        lo = F::pack(r);
+    } else {
+        lo = hi;
+    }
+}
+
+// Scan outputs of one lane (stream hh, channel cc of the chunk) to the [f; b]
+// buffer: row = hit slot of position p, column = col0 + cc.
+template <class C, class E>
+__device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int hh, int cc) {
+#pragma unroll
+    for (int p = 0; p < C::SP; ++p) {
+        const int s = 32 * (p >> 4) + 8 * ((p >> 2) & 3) + 4 * hh + (p & 3);
+        reinterpret_cast<E *>(ws)[s * C::FBS + col0 + cc] = (E)v[p];
+    }
+}
+
+template <int D, int OP>
+__global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kernel(
+    const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
+    int n_tracks, DevParams P, float *__restrict__ out, int *__restrict__ err) {
+    using C = KCfg<D, OP>;
+    using F = Frag<OP>;
+    using FT = typename F::T;
+    using FE = typename F::E;
+    constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
+    constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK;
+    constexpr int NCH = D / 32;
+
+    __shared__ __attribute__((aligned(16))) char smem[C::WAVES * C::WAVE_BYTES];
+    const int lane = threadIdx.x & 63;
+    const int wid = threadIdx.x >> 6;
+    char *ws = smem + size_t(wid) * C::WAVE_BYTES;
+    float *stage = reinterpret_cast<float *>(ws);                  // [CAP][STS]
+    float *pooled = reinterpret_cast<float *>(ws + C::POOL_OFF);   // [32][PLS]
+    int *t_start = reinterpret_cast<int *>(ws + C::META_OFF);      // [32]
+    int *t_len = t_start + kMaxTracksPerTile;                      // [32]
+
+    const int hh = lane >> 5;  // lane half
+    const int cc = lane & 31;  // lane column
+
+    // Contiguous group of tracks for this wave, balanced by track count.
+    const long long gw = (long long)blockIdx.x * C::WAVES + wid;
+    const long long nw = (long long)gridDim.x * C::WAVES;
+    const int g_begin = int((long long)n_tracks * gw / nw);
+    const int g_end = int((long long)n_tracks * (gw + 1) / nw);
+
+    int errbits = 0;
+    const float qnan = __builtin_nanf("");
+
+    int t = g_begin;
+    while (t < g_end) {
+        // ---- pick the tile: the longest run of whole tracks t.. with <= CAP hits
+        const int idx = t + lane;
+        int off = 0;
+        if (lane <= kMaxTracksPerTile && idx <= g_end) off = offsets[idx];
+        const int base = uniform(off);
+        const int prev = __shfl_up(off, 1);
+        const bool ok = lane >= 1 && lane <= kMaxTracksPerTile && idx <= g_end && off >= prev &&
+                        (long long)off - base <= CAP && (long long)off <= n_hits_total && base >= 0;
+        const unsigned long long okm = __ballot(ok);
+        const int k = __builtin_ctzll(~(okm >> 1));
+        if (k == 0) {
+            // track t alone cannot be fitted: rows outside [0, n_hits), an end
+            // offset before its start, or more hits than a tile holds
+            const int off1 = __builtin_amdgcn_readlane(off, 1);
+            const bool bad = base < 0 || off1 < base || (long long)off1 > n_hits_total;
+            errbits |= bad ? TF_DEVERR_BAD_OFFSETS : TF_DEVERR_TOO_LONG;
+            if (lane < 5) out[(size_t)t * 5 + lane] = qnan;
+            t += 1;
+            continue;
+        }
+        const int n = __builtin_amdgcn_readlane(off, k) - base;  // hits in the tile, 0..CAP
+        if (n == 0) {
+            errbits |= TF_DEVERR_EMPTY_TRACK;
+            for (int e = lane; e < 5 * k; e += 64) out[(size_t)t * 5 + e] = qnan;
+            t += k;
+            continue;
+        }
+        // track metadata and start mask
+        const int nxt = __shfl_down(off, 1);
+        if (lane < k) {
+            t_start[lane] = off - base;
+            t_len[lane] = nxt - off;
+        }
+        unsigned long long smask = 0;
+        bool empty = false;
+        for (int j = 0; j < k; ++j) {
+            const int sj = __builtin_amdgcn_readlane(off, j) - base;
+            const int lj = __builtin_amdgcn_readlane(off, j + 1) - base - sj;
+            if (lj > 0)
+                smask |= 1ull << sj;
+            else
+                empty = true;
+        }
+        if (empty) errbits |= TF_DEVERR_EMPTY_TRACK;
+        const unsigned long long valid = n >= 64 ? ~0ull : ((1ull << n) - 1);
+        const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
+        const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
+        const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
+        const unsigned int sb0 = unsigned(vstart) & spm, sb1 = unsigned(vstart >> SP) & spm;
+        const unsigned int eb0 = unsigned(emask) & spm, eb1 = unsigned(emask >> SP) & spm;
+        const unsigned int sbl = hh ? sb1 : sb0;  // this lane's stream
+        const unsigned int ebl = hh ? eb1 : eb0;
+        const unsigned int sany = sb0 | sb1, eany = eb0 | eb1;
+        // One track may straddle the two streams (tile hit SP is not a start).
+        const bool cross = n > SP && !((smask >> SP) & 1ull);
+        const int fs1 = sb1 ? __builtin_ctz(sb1) : SP;           // fwd fix-up: stream 1, p < fs1
+        const int le0 = eb0 ? 31 - __builtin_clz(eb0) : -1;      // bwd fix-up: stream 0, p > le0
+
+        // ---- embedding (normalisation folded into the weights), residual stream
+        // r[m][nt][q]: channel 32 m + 8 (q/4) + 4 hh + (q%4), hit slot 32 nt + cc
+        f32x16 r[MT][HT];
+#pragma unroll
+        for (int nt = 0; nt < HT; ++nt) {
+            const int th = slot_to_hit<SP>(32 * nt + cc);
+            float hx = 0.f, hy = 0.f, hz = 0.f;
+            if (th < n) {
+                const float *hp = hits + ((size_t)base + th) * 3;
+                hx = hp[0];
+                hy = hp[1];
+                hz = hp[2];
+            }
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const float4 e = P.emb[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                    r[m][nt][q] = fmaf(e.x, hx, fmaf(e.y, hy, fmaf(e.z, hz, e.w)));
+                }
+        }
+
+        // ---- layers
+        for (int l = 0; l < P.n_layers; ++l) {
+            // RMSNorm: each lane holds half the channels of hit slot 32 nt + cc
+            FT yf[HT][KS1];
+#pragma unroll
+            for (int nt = 0; nt < HT; ++nt) {
+                float ss = 0.f;
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) ss = fmaf(r[m][nt][q], r[m][nt][q], ss);
+                ss += __shfl_xor(ss, 32);
+                float rs;
+                if constexpr (C::HALF)
+                    rs = rsqrtf(ss * (1.0f / D) + kRmsEps);
+                else
+                    rs = 1.0f / sqrtf(ss * (1.0f / D) + kRmsEps);
+#pragma unroll
+                for (int ks = 0; ks < KS1; ++ks) {
+                    float v[8];
+#pragma unroll
+                    for (int u = 0; u < KL; ++u) v[u] = r[ks / RPK][nt][(ks % RPK) * KL + u] * rs;
+                    yf[nt][ks] = F::pack(v);
+                }
+            }
+            const char *winl = static_cast<const char *>(P.win) +
+                               (size_t)l * NCH * 2 * KS1 * 64 * sizeof(FT);
+            const char *woutl = static_cast<const char *>(P.wout) +
+                                (size_t)l * NCH * MT * KS2 * 64 * sizeof(FT);
+            const float *binl = P.bin + (size_t)l * 2 * D;
+
+            for (int ch = 0; ch < NCH; ++ch) {
+                // input projection for channels 32 ch .. +31: hits on rows
+                f32x16 ax[HT], gx[HT];
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        ax[nt][q] = 0.f;
+                        gx[nt][q] = 0.f;
+                    }
+                const FT *wx = reinterpret_cast<const FT *>(winl) + (size_t)(ch * 2 + 0) * KS1 * 64;
+                const FT *wg = reinterpret_cast<const FT *>(winl) + (size_t)(ch * 2 + 1) * KS1 * 64;
+#pragma unroll
+                for (int ks = 0; ks < KS1; ++ks) {
+                    const FT bx = wx[ks * 64 + lane];
+                    const FT bg = wg[ks * 64 + lane];
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) {
+                        ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
+                        gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
+                    }
+                }
+                // gate and the two scan coefficients: a x and (1 - a)
+                const float bxv = binl[32 * ch + cc];
+                const float bgv = binl[D + 32 * ch + cc];
+                float AX[HT * 16], CF[HT * 16];
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        const float x = ax[nt][q] + bxv;
+                        float e, a;  // e = exp(-gate), a = sigmoid(gate) = 1 / (1 + e)
+                        if constexpr (C::HALF) {
+                            // hardware exp2 / reciprocal; the bias holds -log2(e) * b
+                            e = __builtin_amdgcn_exp2f(
+                                __builtin_amdgcn_fmed3f(fmaf(gx[nt][q], -kLog2e, bgv), -kGateClamp, kGateClamp));
+                            a = __builtin_amdgcn_rcpf(1.0f + e);
+                        } else {
+                            // correctly rounded division and library exp for the fp32 model
+                            e = expf(-__builtin_amdgcn_fmed3f(gx[nt][q] + bgv, -80.0f, 80.0f));
+                            a = 1.0f / (1.0f + e);
+                        }
+                        AX[nt * 16 + q] = a * x;
+                        CF[nt * 16 + q] = e * a;
+                    }
+                // forward scan along this lane's stream
+                wave_lds_sync();  // previous chunk's reads of the [f; b] buffer are done
+                {
+                    float Fs[HT * 16];
+                    float f = 0.f;
+#pragma unroll
+                    for (int p = 0; p < SP; ++p) {
+                        const float nf = fmaf(CF[p], f, AX[p]);
+                        if ((sany >> p) & 1u)
+                            f = ((sbl >> p) & 1u) ? AX[p] : nf;
+                        else
+                            f = nf;
+                        Fs[p] = f;
+                    }
+                    if (cross) {
+                        // the track straddling the two streams: redo the head of stream 1
+                        // up to its first track start from the true state at the end of
+                        // stream 0, with the same operations as an unsplit scan
+                        float fr = __shfl_xor(Fs[SP - 1], 32);
+#pragma unroll
+                        for (int p = 0; p < SP; ++p) {
+                            if (p < fs1) {
+                                fr = fmaf(CF[p], fr, AX[p]);
+                                if (hh) Fs[p] = fr;
+                            }
+                        }
+                    }
+                    store_fb<C, FE>(ws, Fs, 0, hh, cc);
+                }
+                // reverse scan
+                {
+                    float Bs[HT * 16];
+                    float b = 0.f;
+#pragma unroll
+                    for (int p = SP - 1; p >= 0; --p) {
+                        const float nb = fmaf(CF[p], b, AX[p]);
+                        if ((eany >> p) & 1u)
+                            b = ((ebl >> p) & 1u) ? AX[p] : nb;
+                        else
+                            b = nb;
+                        Bs[p] = b;
+                    }
+                    if (cross) {
+                        // and redo the tail of stream 0 back to its last track end from the
+                        // true reverse state at the start of stream 1
+                        float br = __shfl_xor(Bs[0], 32);
+#pragma unroll
+                        for (int p = SP - 1; p >= 0; --p) {
+                            if (p > le0) {
+                                br = fmaf(CF[p], br, AX[p]);
+                                if (!hh) Bs[p] = br;
+                            }
+                        }
+                    }
+                    store_fb<C, FE>(ws, Bs, 32, hh, cc);
+                }
+                wave_lds_sync();
+                // output projection, K split over chunks.  The 16-bit modes
+                // accumulate straight into the residual registers; the fp32 model
+                // sums each chunk in fresh accumulators and adds the chunk once, so
+                // the residual is rounded once per chunk rather than per k-step.
+                const FT *wo = reinterpret_cast<const FT *>(woutl) + (size_t)ch * MT * KS2 * 64;
+                f32x16 part[C::HALF ? 1 : MT][HT];
+                if constexpr (!C::HALF) {
+#pragma unroll
+                    for (int m = 0; m < MT; ++m)
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                            for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
+                }
+#pragma unroll
+                for (int kk = 0; kk < KS2; ++kk) {
+                    FT bfr[HT];
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) {
+                        const int row = 32 * nt + cc;
+                        const FE *fb = reinterpret_cast<const FE *>(ws);
+                        bfr[nt] = *reinterpret_cast<const FT *>(fb + row * C::FBS + kk * K + hh * KL);
+                    }
+#pragma unroll
+                    for (int m = 0; m < MT; ++m) {
+                        const FT a = wo[((size_t)m * KS2 + kk) * 64 + lane];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) {
+                            if constexpr (C::HALF)
+                                r[m][nt] = F::mma(a, bfr[nt], r[m][nt]);
+                            else
+                                part[m][nt] = F::mma(a, bfr[nt], part[m][nt]);
+                        }
+                    }
+                }
+                if constexpr (!C::HALF) {
+#pragma unroll
+                    for (int m = 0; m < MT; ++m)
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) r[m][nt] += part[m][nt];
+                }
+            }
+            // output-projection bias
+            const float *bo = P.bout + (size_t)l * D;
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const float bv = bo[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) r[m][nt][q] += bv;
+                }
+        }
+
+        // ---- mean pool over each track's hits, 32 channels at a time
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            wave_lds_sync();
+#pragma unroll
+            for (int nt = 0; nt < HT; ++nt) {
+                const int th = slot_to_hit<SP>(32 * nt + cc);
+#pragma unroll
+                for (int q = 0; q < 16; ++q)
+                    stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
+            }
+            wave_lds_sync();
+            for (int j = hh; j < k; j += 2) {
+                const int s0 = t_start[j], len = t_len[j];
+                float sum = 0.f;
+                for (int u = 0; u < len; ++u) sum += stage[(s0 + u) * C::STS + cc];
+                pooled[j * C::PLS + 32 * m + cc] = sum / (float)len;
+            }
+        }
+        wave_lds_sync();
+
+        // ---- head layer 1: hidden = SiLU(W1 p + b1), tracks on rows
+        f32x16 hid[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS1; ++ks) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < KL; ++u) v[u] = pooled[cc * C::PLS + ks * K + hh * KL + u];
+            FT a_hi, a_lo;
+            split_operand<F>(v, a_hi, a_lo);
+            const FT *w1 = reinterpret_cast<const FT *>(P.w1);
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                const FT b = w1[((size_t)m * KS1 + ks) * 64 + lane];
+                hid[m] = F::mma(a_hi, b, hid[m]);
+                if constexpr (C::HALF) hid[m] = F::mma(a_lo, b, hid[m]);
+            }
+        }
+        wave_lds_sync();
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            const float bv = P.b1[32 * m + cc];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const float v = hid[m][q] + bv;
+                const int row = 8 * (q >> 2) + 4 * hh + (q & 3);
+                float sv;  // SiLU(v) = v / (1 + exp(-v))
+                if constexpr (C::HALF)
+                    sv = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(__builtin_amdgcn_fmed3f(
+                                                          -v * kLog2e, -kGateClamp, kGateClamp)));
+                else
+                    sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
+                pooled[row * C::PLS + 32 * m + cc] = sv;
+            }
+        }
+        wave_lds_sync();
+        // ---- head layer 2: five outputs per track (columns >= 5 of W2 are zero)
+        f32x16 o;
+#pragma unroll
+        for (int q = 0; q < 16; ++q) o[q] = 0.f;
+#pragma unroll
+        for (int ks = 0; ks < KS1; ++ks) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < KL; ++u) v[u] = pooled[cc * C::PLS + ks * K + hh * KL + u];
+            FT a_hi, a_lo;
+            split_operand<F>(v, a_hi, a_lo);
+            const FT b = reinterpret_cast<const FT *>(P.w2)[ks * 64 + lane];
+            o = F::mma(a_hi, b, o);
+            if constexpr (C::HALF) o = F::mma(a_lo, b, o);
+        }
+        if (cc < 5) {
+            const float bv = P.b2[cc];
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                const int row = 8 * (q >> 2) + 4 * hh + (q & 3);
+                if (row < k) out[(size_t)(t + row) * 5 + cc] = o[q] + bv;
+            }
+        }
+        t += k;
+    }
+    if (errbits && lane == 0) atomicOr(err, errbits);
+}
+
+// ---------------------------------------------------------------------------
+// Host side
+// ---------------------------------------------------------------------------
+
+uint16_t to_bf16(double v) {
+    float f = (float)v;
+    uint32_t u;
+    std::memcpy(&u, &f, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return uint16_t((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return uint16_t(u >> 16);
+}
+
+// Host-side packer of weight arrays in the kernel's operand type.
+struct Packer {
+    int op;
+    std::vector<unsigned char> bytes;
+    size_t begin() {  // 256-byte aligned start of a new array
+        size_t o = (bytes.size() + 255) & ~size_t(255);
+        bytes.resize(o);
+        return o;
+    }
+    void push(double v) {  // one matrix-core operand element
+        size_t o = bytes.size();
+        if (op == OP_BF16) {
+            uint16_t b = to_bf16(v);
+            bytes.resize(o + 2);
+            std::memcpy(&bytes[o], &b, 2);
+        } else if (op == OP_F16) {
+            _Float16 h = (_Float16)(float)v;
+            bytes.resize(o + 2);
+            std::memcpy(&bytes[o], &h, 2);
+        } else {
+            push_f32(v);
+        }
+    }
+    void push_f32(double v) {
+        size_t o = bytes.size();
+        bytes.resize(o + 4);
+        float f = (float)v;
+        std::memcpy(&bytes[o], &f, 4);
+    }
+};
+
+}  // namespace
+
+struct tf_weights {
+    int n_layers = 0, d = 0, dtype = 0, max_hits = 0, device = 0, cu_count = 0;
+    void *dmem = nullptr;
+    int *err = nullptr;
+    DevParams params{};
+};
+
+extern "C" size_t tf_blob_size(int32_t n_layers, int32_t d) {
+    if (n_layers < 0 || d <= 0) return 0;
+    size_t dd = (size_t)d;
+    size_t per_layer = dd + 3 * dd * dd + 3 * dd + dd * 2 * dd + dd;
+    return 4 * dd + (size_t)n_layers * per_layer + dd * dd + dd + 5 * dd + 5;
+}
+
+extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, size_t n_floats,
+                                       tf_weights **out) {
+    if (!out) return TF_EINVAL;
+    *out = nullptr;
+    if (!cfg || !blob || cfg->reserved != 0) return TF_EINVAL;
+    const int L = cfg->n_layers, D = cfg->d_model;
+    if (cfg->dtype != TF_FP32 && cfg->dtype != TF_BF16 && cfg->dtype != TF_BF16_F16ACT) return TF_EINVAL;
+    if (L < 0 || D <= 0) return TF_EINVAL;
+    if (!(D == 32 || D == 64 || D == 128 || D == 256) || L > 64) return TF_EUNSUPPORTED;
+    if (n_floats != tf_blob_size(L, D)) return TF_EINVAL;
+    const int op = cfg->dtype == TF_BF16 ? OP_BF16 : cfg->dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32;
+    const bool half = op != OP_F32;
+    const int K = half ? 16 : 2, KL = K / 2, KS1 = D / K, KS2 = 64 / K, RPK = 16 / KL;
+    const int MT = D / 32, NCH = D / 32;
+
+    // blob views
+    const size_t dd = (size_t)D;
+    const float *eW = blob, *eb = blob + 3 * dd;
+    const size_t lstride = dd + 3 * dd * dd + 3 * dd + dd * 2 * dd + dd;
+    auto g_of = [&](int l) { return blob + 4 * dd + (size_t)l * lstride; };
+    auto inW_of = [&](int l) { return g_of(l) + dd; };
+    auto inb_of = [&](int l) { return inW_of(l) + 3 * dd * dd; };
+    auto outW_of = [&](int l) { return inb_of(l) + 3 * dd; };
+    auto outb_of = [&](int l) { return outW_of(l) + dd * 2 * dd; };
+    const float *W1 = blob + 4 * dd + (size_t)L * lstride;
+    const float *b1 = W1 + dd * dd, *W2 = b1 + dd, *b2 = W2 + 5 * dd;
+
+    Packer pk{op, {}};
+    // embedding with u = (x - lo) / span folded in: r = (W/span) x + (b - W lo / span)
+    const size_t o_emb = pk.begin();
+    const double lo[3] = {-1000.0, -1000.0, -3000.0}, span[3] = {2000.0, 2000.0, 6000.0};
+    for (int c = 0; c < D; ++c) {
+        double b = eb[c];
+        for (int k = 0; k < 3; ++k) {
+            pk.push_f32(eW[c * 3 + k] / span[k]);
+            b -= eW[c * 3 + k] * lo[k] / span[k];
+        }
+        pk.push_f32(b);
+    }
+    // input projection B fragments: lane (g, c) value u of k-step ks holds
+    // W[out 32 ch + c][in 32 m + 8 i + 4 g + j] * gain[in], with
+    // (m, 4 i + j) = (ks / RPK, (ks % RPK) * KL + u).
+    const size_t o_win = pk.begin();
+    for (int l = 0; l < L; ++l) {
+        const float *W = inW_of(l), *g = g_of(l);
+        for (int ch = 0; ch < NCH; ++ch)
+            for (int part = 0; part < 2; ++part)
+                for (int ks = 0; ks < KS1; ++ks)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int u = 0; u < KL; ++u) {
+                            const int gg = lane / 32, c = lane % 32;
+                            const int reg = (ks % RPK) * KL + u, m = ks / RPK;
+                            const int in = 32 * m + 8 * (reg / 4) + 4 * gg + (reg % 4);
+                            const int row = part * D + 32 * ch + c;
+                            pk.push((double)W[(size_t)row * D + in] * g[in]);
+                        }
+    }
+    const size_t o_bin = pk.begin();
+    for (int l = 0; l < L; ++l) {
+        const float *b = inb_of(l);
+        for (int o = 0; o < D; ++o) pk.push_f32(b[o]);
+        const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
+        for (int o = 0; o < D; ++o) pk.push_f32(gs * b[D + o]);
+    }
+    // output projection A fragments: lane (g, c) value u of k-step kk holds
+    // W[out 32 m + c][column of [f; b] channel q = kk K + g KL + u of chunk ch]
+    const size_t o_wout = pk.begin();
+    for (int l = 0; l < L; ++l) {
+        const float *W = outW_of(l);
+        for (int ch = 0; ch < NCH; ++ch)
+            for (int m = 0; m < MT; ++m)
+                for (int kk = 0; kk < KS2; ++kk)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int u = 0; u < KL; ++u) {
+                            const int gg = lane / 32, c = lane % 32;
+                            const int q = kk * K + gg * KL + u;
+                            const int col = q < 32 ? 32 * ch + q : D + 32 * ch + (q - 32);
+                            pk.push(W[(size_t)(32 * m + c) * 2 * D + col]);
+                        }
+    }
+    const size_t o_bout = pk.begin();
+    for (int l = 0; l < L; ++l)
+        for (int o = 0; o < D; ++o) pk.push_f32(outb_of(l)[o]);
+    // head
+    const size_t o_w1 = pk.begin();
+    for (int m = 0; m < MT; ++m)
+        for (int ks = 0; ks < KS1; ++ks)
+            for (int lane = 0; lane < 64; ++lane)
+                for (int u = 0; u < KL; ++u)
+                    pk.push(W1[(size_t)(32 * m + lane % 32) * D + ks * K + (lane / 32) * KL + u]);
+    const size_t o_b1 = pk.begin();
+    for (int o = 0; o < D; ++o) pk.push_f32(b1[o]);
+    const size_t o_w2 = pk.begin();
+    for (int ks = 0; ks < KS1; ++ks)
+        for (int lane = 0; lane < 64; ++lane)
+            for (int u = 0; u < KL; ++u) {
+                const int c = lane % 32;
+                pk.push(c < 5 ? (double)W2[(size_t)c * D + ks * K + (lane / 32) * KL + u] : 0.0);
+            }
+    const size_t o_b2 = pk.begin();
+    for (int o = 0; o < 5; ++o) pk.push_f32(b2[o]);
+    const size_t o_err = pk.begin();
+    pk.push_f32(0.0);
+    const size_t total = pk.begin();
+    (void)RPK;
+
+    tf_weights *w = new (std::nothrow) tf_weights();
+    if (!w) return TF_ENOMEM;
+    if (hipGetDevice(&w->device) != hipSuccess ||
+        hipDeviceGetAttribute(&w->cu_count, hipDeviceAttributeMultiprocessorCount, w->device) != hipSuccess) {
+        delete w;
+        return TF_EHIP;
+    }
+    if (hipMalloc(&w->dmem, total) != hipSuccess) {
+        delete w;
+        return TF_ENOMEM;
+    }
+    std::vector<unsigned char> &hb = pk.bytes;
+    std::memset(&hb[o_err], 0, 4);
+    if (hipMemcpy(w->dmem, hb.data(), total, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(w->dmem);
+        delete w;
+        return TF_EHIP;
+    }
+    char *b = static_cast<char *>(w->dmem);
+    w->n_layers = L;
+    w->d = D;
+    w->dtype = cfg->dtype;
+    w->max_hits = (half ? D <= 128 : D <= 64) ? 64 : 32;
+    w->err = reinterpret_cast<int *>(b + o_err);
+    DevParams &P = w->params;
+    P.emb = reinterpret_cast<const float4 *>(b + o_emb);
+    P.win = b + o_win;
+    P.bin = reinterpret_cast<const float *>(b + o_bin);
+    P.wout = b + o_wout;
+    P.bout = reinterpret_cast<const float *>(b + o_bout);
+    P.w1 = b + o_w1;
+    P.b1 = reinterpret_cast<const float *>(b + o_b1);
+    P.w2 = b + o_w2;
+    P.b2 = reinterpret_cast<const float *>(b + o_b2);
+    P.n_layers = L;
+    *out = w;
+    return TF_OK;
+}
+
+extern "C" void tf_weights_destroy(tf_weights *w) {
+    if (!w) return;
+    (void)hipDeviceSynchronize();
+    (void)hipFree(w->dmem);
+    delete w;
+}
+
+extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
+
+namespace {
+template <int D, int OP>
+hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                  const tf_weights *w, float *out, hipStream_t stream) {
+    using C = KCfg<D, OP>;
+    // at least 16 tracks per wave; at most two workgroups per compute unit
+    long long waves = (n_tracks + 15) / 16;
+    long long blocks = (waves + C::WAVES - 1) / C::WAVES;
+    const long long cap = (long long)w->cu_count * 2;
+    if (blocks > cap) blocks = cap;
+    if (blocks < 1) blocks = 1;
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+                       hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, w->err);
+    return hipGetLastError();
+}
+
+template <int D>
+hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                    const tf_weights *w, float *out, hipStream_t stream) {
+    switch (w->dtype) {
+        case TF_BF16: return launch<D, OP_BF16>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16_F16ACT: return launch<D, OP_F16>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        default: return launch<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    }
+}
+}  // namespace
+
+extern "C" tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                                const tf_weights *w, float *out, hipStream_t stream) {
+    if (!w || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
+    if (n_tracks == 0) return TF_OK;
+    if (!offsets || !out || (!hits && n_hits > 0)) return TF_EINVAL;
+    hipError_t e;
+    switch (w->d) {
+        case 32: e = launch_d<32>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 64: e = launch_d<64>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 128: e = launch_d<128>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 256: e = launch_d<256>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        default: return TF_EUNSUPPORTED;
+    }
+    return e == hipSuccess ? TF_OK : TF_EHIP;
+}
+
+extern "C" tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear) {
+    if (!w || !flags) return TF_EINVAL;
+    int v = 0;
+    if (hipMemcpyAsync(&v, w->err, 4, hipMemcpyDeviceToHost, stream) != hipSuccess) return TF_EHIP;
+    if (hipStreamSynchronize(stream) != hipSuccess) return TF_EHIP;
+    *flags = v;
+    if (clear) {
+        if (hipMemsetAsync(w->err, 0, 4, stream) != hipSuccess) return TF_EHIP;
+        if (hipStreamSynchronize(stream) != hipSuccess) return TF_EHIP;
+    }
+    return TF_OK;
+}
+
+extern "C" const char *tf_status_string(tf_status s) {
+    switch (s) {
+        case TF_OK: return "ok";
+        case TF_EINVAL: return "invalid argument";
+        case TF_ENOMEM: return "out of memory";
+        case TF_EHIP: return "HIP runtime error";
+        case TF_EUNSUPPORTED: return "unsupported configuration";
+    }
+    return "unknown status";
+}

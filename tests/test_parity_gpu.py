@@ -1,0 +1,212 @@
+"""GPU parity: the HIP library through its C ABI against the fp64 oracle.
+
+Inputs are the seeded synthetic helix workloads (stand-ins for the paper's
+simulated muon samples).  Tolerances: 1e-5 relative for the fp32 model and
+2e-2 for the bf16 model, per output column (tests/parity.py).
+"""
+import dataclasses
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import tracksynth as ts
+from tests.parity import TOL, assert_parity, column_rms
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+N_PARITY = {"tiny_d32_fp32": 256, "d128x4_fp32_65k": 2048, "d256x6_bf16_1m": 512,
+            "long64_d128x4_bf16_200k": 512, "deploy_d128x4_bf16_8m": 2048}
+THREADS = int(os.environ.get("ORACLE_THREADS", "0"))
+
+
+@pytest.fixture(scope="module")
+def tf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32479_amd as tf
+    return tf
+
+
+def _weights(tf, w, blob=None, mode=None):
+    blob = ts.make_weights(w) if blob is None else blob
+    mode = tf.MODE_FOR_WEIGHTS[w.dtype] if mode is None else mode
+    return tf.Weights(blob, w.n_layers, w.d_model, mode), blob
+
+
+def _gpu(tf, W, hits, offs, n_tracks=None):
+    h = torch.from_numpy(np.ascontiguousarray(hits)).cuda()
+    o = torch.from_numpy(np.ascontiguousarray(offs, dtype=np.int32)).cuda()
+    out = tf.fit_tracks(h, o, W, n_tracks=n_tracks)
+    torch.cuda.synchronize()
+    return out.cpu().numpy()
+
+
+def _ref(w, hits, offs, blob):
+    return oracle.fit_tracks(hits, offs, blob, w.n_layers, w.d_model, n_threads=THREADS)
+
+
+@pytest.mark.parametrize("name", list(ts.WORKLOADS))
+def test_parity_workload(tf, name):
+    w = ts.WORKLOADS[name]
+    print(f"[parity] {name} n={N_PARITY[name]}", flush=True)
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=N_PARITY[name])
+    g = _gpu(tf, W, hits, offs)
+    r = _ref(w, hits, offs, blob)
+    emax, l2 = assert_parity(g, r, TOL[w.dtype], name)
+    print(f"[parity] {name} max col err {emax} l2 {l2}", flush=True)
+    assert tf.device_error(W) == 0
+
+
+@pytest.mark.parametrize("name,d,L", [("d128x4_fp32_65k", 128, 1), ("deploy_d128x4_bf16_8m", 128, 1),
+                                      ("deploy_d128x4_bf16_8m", 128, 64), ("d128x4_fp32_65k", 128, 32),
+                                      ("d256x6_bf16_1m", 256, 32), ("tiny_d32_fp32", 32, 64)])
+def test_fixed_lengths(tf, name, d, L):
+    """All tracks of one length: length 1 (scan of one step) and the maximum."""
+    w = dataclasses.replace(ts.WORKLOADS[name], len_min=L, len_max=L, n_det_layers=max(L, 8))
+    print(f"[fixed] {name} L={L}", flush=True)
+    W, blob = _weights(tf, w)
+    assert W.max_hits >= L
+    hits, offs = ts.make_tracks(w, n_tracks=300)
+    g = _gpu(tf, W, hits, offs)
+    r = _ref(w, hits, offs, blob)
+    assert_parity(g, r, TOL[w.dtype], f"{name} L={L}")
+    assert tf.device_error(W) == 0
+
+
+@pytest.mark.parametrize("name", ["d128x4_fp32_65k", "deploy_d128x4_bf16_8m", "d256x6_bf16_1m"])
+def test_ragged_mix_and_small_batches(tf, name):
+    """Lengths 1..max mixed at random, batches of 1, 2, 33 and 1000 tracks."""
+    w0 = ts.WORKLOADS[name]
+    print(f"[ragged] {name}", flush=True)
+    W, blob = _weights(tf, w0)
+    maxL = W.max_hits
+    w = dataclasses.replace(w0, len_min=1, len_max=maxL, n_det_layers=maxL)
+    hits, offs = ts.make_tracks(w, n_tracks=1000)
+    r_all = _ref(w, hits, offs, blob)
+    for n in (1, 2, 33, 1000):
+        g = _gpu(tf, W, hits, offs[: n + 1])
+        assert_parity(g, r_all[:n], TOL[w.dtype], f"{name} n={n}", rms=column_rms(r_all))
+    assert tf.device_error(W) == 0
+
+
+# Pure bf16 activation operands: the rounding of the candidate and scan-output
+# operands to 8 significant bits alone gives up to about 3e-2 on the 6-layer
+# d=256 model's worst track (column-relative), so the bf16 mode is held to a
+# documented bound per workload rather than the 2e-2 of the fp16-activation mode.
+BF16_PURE_BOUND = {"d256x6_bf16_1m": 6e-2, "long64_d128x4_bf16_200k": 3e-2, "deploy_d128x4_bf16_8m": 3e-2}
+
+
+@pytest.mark.parametrize("name", list(BF16_PURE_BOUND))
+def test_parity_pure_bf16_mode(tf, name):
+    w = ts.WORKLOADS[name]
+    print(f"[parity-bf16] {name}", flush=True)
+    W, blob = _weights(tf, w, mode="bf16")
+    hits, offs = ts.make_tracks(w, n_tracks=N_PARITY[name])
+    g = _gpu(tf, W, hits, offs)
+    r = _ref(w, hits, offs, blob)
+    emax, l2 = assert_parity(g, r, BF16_PURE_BOUND[name], name + " (bf16 operands)")
+    assert l2.max() <= 2e-2
+    print(f"[parity-bf16] {name} max col err {emax} l2 {l2}", flush=True)
+
+
+def test_absolute_offsets_and_prefix(tf):
+    """offsets[0] > 0 into a larger hit array, and n_tracks below offsets.numel()-1."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=700)
+    ref = _ref(w, hits, offs, blob)
+    # tracks 300..599 through an absolute slice of the full offsets array
+    g = _gpu(tf, W, hits, offs[300:], n_tracks=300)
+    assert_parity(g, ref[300:600], TOL[w.dtype], "absolute offsets")
+    assert tf.device_error(W) == 0
+
+
+def test_bad_tracks_give_nan_and_flags(tf):
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=50)
+    L = np.diff(offs)
+    # track 10 emptied, track 20 made longer than the maximum
+    L[10] = 0
+    L[20] = W.max_hits + 5
+    long_hits = np.zeros((L.sum(), 3), np.float32)
+    o2 = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+    for i in range(50):
+        src = hits[offs[i]:offs[i + 1]]
+        n = min(L[i], src.shape[0])
+        long_hits[o2[i]:o2[i] + n] = src[:n]
+        if L[i] > n:
+            long_hits[o2[i] + n:o2[i + 1]] = src[-1]
+    g = _gpu(tf, W, long_hits, o2)
+    assert np.all(np.isnan(g[10])) and np.all(np.isnan(g[20]))
+    good = np.ones(50, bool)
+    good[[10, 20]] = False
+    r = _ref(w, long_hits, o2, blob)
+    assert_parity(g[good], r[good], TOL[w.dtype], "neighbours of bad tracks")
+    flags = tf.device_error(W)
+    assert flags == (tf.DEVERR_EMPTY_TRACK | tf.DEVERR_TOO_LONG)
+    assert tf.device_error(W) == 0   # cleared
+
+
+def test_offsets_outside_hits_flagged(tf):
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=20)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    out = torch.empty((20, 5), device="cuda")
+    # claim fewer rows than the offsets reach: the tail tracks must be refused
+    tf.lib().fit_tracks(h.data_ptr(), int(offs[15]), o.data_ptr(), 20, W.handle, out.data_ptr(), None)
+    torch.cuda.synchronize()
+    g = out.cpu().numpy()
+    assert np.all(np.isfinite(g[:15]))
+    assert np.all(np.isnan(g[15:]))
+    assert tf.device_error(W) & tf.DEVERR_BAD_OFFSETS
+
+
+@pytest.mark.parametrize("name,mode", [("deploy_d128x4_bf16_8m", None), ("deploy_d128x4_bf16_8m", "bf16"),
+                                       ("d128x4_fp32_65k", None), ("d256x6_bf16_1m", None)])
+def test_determinism_and_neighbour_independence(tf, name, mode):
+    w = ts.WORKLOADS[name]
+    W, blob = _weights(tf, w, mode=mode)
+    hits, offs = ts.make_tracks(w, n_tracks=5000)
+    a = _gpu(tf, W, hits, offs)
+    b = _gpu(tf, W, hits, offs)
+    assert np.array_equal(a, b)                      # bitwise run to run
+    perm = np.random.default_rng(0).permutation(5000)
+    L = np.diff(offs)
+    hp = np.concatenate([hits[offs[i]:offs[i + 1]] for i in perm])
+    op = np.concatenate([[0], np.cumsum(L[perm])]).astype(np.int32)
+    c = _gpu(tf, W, hp, op)
+    # a track's result does not depend on which tracks share its tile (bitwise)
+    assert np.array_equal(c, a[perm])
+
+
+def test_graph_replay_matches_direct(tf):
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=20000)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    direct = tf.fit_tracks(h, o, W)
+    torch.cuda.synchronize()
+    out = torch.zeros_like(direct)
+    s = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(s):
+        tf.fit_tracks(h, o, W, out=out, n_tracks=10000, stream=s)  # warm up on the capture stream
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=s):
+            tf.fit_tracks(h, o[:10001], W, out=out[:10000], stream=s)
+            tf.fit_tracks(h, o[10000:], W, out=out[10000:], n_tracks=10000, stream=s)
+    ref = direct.cpu().numpy()
+    for rep in range(3):
+        out.zero_()
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(out.cpu().numpy(), ref), f"replay {rep}"
