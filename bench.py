@@ -133,7 +133,7 @@ def main():
     h = torch.from_numpy(hits).to(dev)
     o = torch.from_numpy(offs).to(dev)
     out = torch.empty((n_tracks, 5), dtype=torch.float32, device=dev)
-    W = tf.Weights(blob, w.n_layers, w.d_model, mode)
+    W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=w.len_max)
     starts = list(range(0, n_tracks, batch))
 
     def step(stream=None):
@@ -204,6 +204,7 @@ def main():
         "data": "synthetic helix tracks (2 T solenoid, seeded), random-init weights",
         "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
                    "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model, "mode": mode,
+                   "max_hits": W.max_hits,
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved_tflops / peak, "traffic": None,

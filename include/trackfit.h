@@ -60,7 +60,10 @@ typedef struct {
     int32_t n_layers;
     int32_t d_model;
     int32_t dtype;    /* tf_dtype */
-    int32_t reserved; /* must be 0 */
+    int32_t max_hits; /* longest track the caller will pass; 0 = the largest
+                         supported (64 for d_model <= 128, 32 for 256).  Up to
+                         32 selects the one-tile-per-wave kernel, which is
+                         faster; longer tracks then get NaN and an error flag. */
 } tf_config;
 
 /* Opaque: device-resident weights in kernel order plus a sticky device error
@@ -82,8 +85,8 @@ typedef struct tf_weights tf_weights;
  *
  * Ownership: host_blob is only read during the call.  *out receives a handle
  * the caller frees with tf_weights_destroy.  Synchronous.
- * Errors: TF_EINVAL (null pointers, bad sizes, reserved != 0),
- * TF_EUNSUPPORTED (d_model or n_layers outside the supported set),
+ * Errors: TF_EINVAL (null pointers, bad sizes, max_hits < 0),
+ * TF_EUNSUPPORTED (d_model, n_layers or max_hits outside the supported set),
  * TF_ENOMEM, TF_EHIP.  On error *out is set to NULL.
  */
 tf_status tf_weights_create(const tf_config *cfg, const float *host_blob, size_t n_floats,
@@ -95,9 +98,9 @@ void tf_weights_destroy(tf_weights *w);
 /* Number of floats of the canonical blob for a model shape (0 if invalid). */
 size_t tf_blob_size(int32_t n_layers, int32_t d_model);
 
-/* Longest track (in hits) the kernels accept for this handle: 64 for
- * d_model <= 128 in the 16-bit modes and d_model <= 64 in TF_FP32, else 32.
- * Longer tracks get NaN outputs and set TF_DEVERR_TOO_LONG. */
+/* Longest track (in hits) the kernels accept for this handle: 32 or 64, from
+ * tf_config.max_hits.  Longer tracks get NaN outputs and set
+ * TF_DEVERR_TOO_LONG. */
 int32_t tf_max_hits(const tf_weights *w);
 
 /*

@@ -38,7 +38,7 @@ class TrackfitError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("reserved", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("max_hits", ctypes.c_int32)]
 
 
 _lib = None
@@ -95,11 +95,12 @@ def _stream_handle(stream) -> int:
 class Weights:
     """Device-resident weights (tf_weights handle) on the current device."""
 
-    def __init__(self, blob, n_layers: int, d_model: int, dtype: str = "fp32"):
-        """dtype: "fp32", "bf16" or "bf16_f16act" (library modes, include/trackfit.h)."""
+    def __init__(self, blob, n_layers: int, d_model: int, dtype: str = "fp32", max_hits: int = 0):
+        """dtype: "fp32", "bf16" or "bf16_f16act" (library modes, include/trackfit.h);
+        max_hits: longest track that will be passed (0: the largest supported)."""
         import numpy as np
         arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
-        cfg = Config(int(n_layers), int(d_model), DTYPES[dtype], 0)
+        cfg = Config(int(n_layers), int(d_model), DTYPES[dtype], int(max_hits))
         h = ctypes.c_void_p()
         _check(lib().tf_weights_create(ctypes.byref(cfg), arr.ctypes.data, arr.size, ctypes.byref(h)),
                "tf_weights_create")

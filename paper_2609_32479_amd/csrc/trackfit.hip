@@ -60,7 +60,6 @@ constexpr float kRmsEps = 1e-6f;
 // |gate pre-activation| is clamped to 80 (scaled by log2 e) so that exp stays
 // finite; the change in the gate is below exp(-80).
 constexpr float kGateClamp = 80.0f * kLog2e;
-constexpr int kMaxTracksPerTile = 32;
 constexpr int kLdsBytesMax = 160 * 1024;
 
 constexpr int cmin(int a, int b) { return a < b ? a : b; }
@@ -69,12 +68,11 @@ constexpr size_t round16(size_t v) { return (v + 15) & ~size_t(15); }
 // ---------------------------------------------------------------------------
 // Compile-time shape of one kernel instance.
 // ---------------------------------------------------------------------------
-template <int D, int OP>
+template <int D, int OP, int HT_>
 struct KCfg {
     static constexpr bool HALF = OP != OP_F32;
-    // 32-hit tiles per wave tile: as many as the register file holds next to
-    // the residual stream (fp32 operands take twice the registers of bf16)
-    static constexpr int HT = (HALF ? D <= 128 : D <= 64) ? 2 : 1;
+    static constexpr int HT = HT_;               // 32-hit tiles per wave tile
+    static constexpr int MAXTR = 16 * HT;        // tracks per wave tile
     static constexpr int CAP = 32 * HT;          // hits per wave tile
     static constexpr int SP = 16 * HT;           // positions per stream (2 streams)
     static constexpr int MT = D / 32;            // 32-channel blocks
@@ -89,9 +87,11 @@ struct KCfg {
     static constexpr size_t FB_BYTES = size_t(CAP) * FBS * (HALF ? 2 : 4);
     static constexpr size_t ST_BYTES = size_t(CAP) * STS * 4;
     static constexpr size_t POOL_OFF = round16(FB_BYTES > ST_BYTES ? FB_BYTES : ST_BYTES);
-    static constexpr size_t META_OFF = round16(POOL_OFF + size_t(kMaxTracksPerTile) * PLS * 4);
-    static constexpr size_t WAVE_BYTES = round16(META_OFF + 2 * kMaxTracksPerTile * 4);
-    static constexpr int WAVES = cmin(4, int(kLdsBytesMax / WAVE_BYTES));
+    static constexpr size_t META_OFF = round16(POOL_OFF + size_t(MAXTR) * PLS * 4);
+    static constexpr size_t WAVE_BYTES = round16(META_OFF + 2 * MAXTR * 4);
+    // waves per SIMD: two when a wave fits in half the register file
+    static constexpr int OCC = (HALF && HT == 1 && D <= 128) ? 2 : 1;
+    static constexpr int WAVES = cmin(4, int(kLdsBytesMax / OCC / WAVE_BYTES));
     static_assert(WAVES >= 1, "LDS budget");
     static_assert(D % 32 == 0, "d must be a multiple of 32");
 };
@@ -150,6 +150,21 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
+// Lane mask (wave-uniform, 64 bits) of the lanes whose stream has bit p set:
+// lanes 0-31 follow b0, lanes 32-63 follow b1.
+__device__ __forceinline__ unsigned long long half_mask(unsigned b0, unsigned b1, int p) {
+    const unsigned long long lo = ((b0 >> p) & 1u) ? 0x00000000ffffffffull : 0ull;
+    const unsigned long long hi = ((b1 >> p) & 1u) ? 0xffffffff00000000ull : 0ull;
+    return lo | hi;
+}
+
+// v in lanes outside m, 0 in lanes of m: one v_cndmask with the mask in SGPRs.
+__device__ __forceinline__ float zero_lanes(float v, unsigned long long m) {
+    float r;
+    asm("v_cndmask_b32_e64 %0, %1, 0, %2" : "=v"(r) : "v"(v), "s"(m));
+    return r;
+}
+
 // Tile hit index held in hit slot s (0 <= s < CAP).  Slot s = 32 n + 8 i + 4 g + j
 // is row 8 i + 4 g + j of hit tile n in the input projection; that row lands
 // in lanes of half g at accumulator register 4 i + j, which is position
@@ -188,14 +203,16 @@ __device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int
     }
 }
 
-template <int D, int OP>
-__global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kernel(
+template <int D, int OP, int HT_>
+__global__ __attribute__((amdgpu_flat_work_group_size(64, 256), amdgpu_waves_per_eu(KCfg<D, OP, HT_>::OCC, KCfg<D, OP, HT_>::OCC)))
+void tf_encoder_kernel(
     const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
     int n_tracks, DevParams P, float *__restrict__ out, int *__restrict__ err) {
-    using C = KCfg<D, OP>;
+    using C = KCfg<D, OP, HT_>;
     using F = Frag<OP>;
     using FT = typename F::T;
     using FE = typename F::E;
+    constexpr int kMaxTracksPerTile = C::MAXTR;
     constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
     constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK;
     constexpr int NCH = D / 32;
@@ -205,9 +222,9 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
     const int wid = threadIdx.x >> 6;
     char *ws = smem + size_t(wid) * C::WAVE_BYTES;
     float *stage = reinterpret_cast<float *>(ws);                  // [CAP][STS]
-    float *pooled = reinterpret_cast<float *>(ws + C::POOL_OFF);   // [32][PLS]
-    int *t_start = reinterpret_cast<int *>(ws + C::META_OFF);      // [32]
-    int *t_len = t_start + kMaxTracksPerTile;                      // [32]
+    float *pooled = reinterpret_cast<float *>(ws + C::POOL_OFF);   // [MAXTR][PLS]
+    int *t_start = reinterpret_cast<int *>(ws + C::META_OFF);      // [MAXTR]
+    int *t_len = t_start + kMaxTracksPerTile;                      // [MAXTR]
 
     const int hh = lane >> 5;  // lane half
     const int cc = lane & 31;  // lane column
@@ -273,9 +290,6 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
         const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
         const unsigned int sb0 = unsigned(vstart) & spm, sb1 = unsigned(vstart >> SP) & spm;
         const unsigned int eb0 = unsigned(emask) & spm, eb1 = unsigned(emask >> SP) & spm;
-        const unsigned int sbl = hh ? sb1 : sb0;  // this lane's stream
-        const unsigned int ebl = hh ? eb1 : eb0;
-        const unsigned int sany = sb0 | sb1, eany = eb0 | eb1;
         // One track may straddle the two streams (tile hit SP is not a start).
         const bool cross = n > SP && !((smask >> SP) & 1ull);
         const int fs1 = sb1 ? __builtin_ctz(sb1) : SP;           // fwd fix-up: stream 1, p < fs1
@@ -386,11 +400,8 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
                     float f = 0.f;
 #pragma unroll
                     for (int p = 0; p < SP; ++p) {
-                        const float nf = fmaf(CF[p], f, AX[p]);
-                        if ((sany >> p) & 1u)
-                            f = ((sbl >> p) & 1u) ? AX[p] : nf;
-                        else
-                            f = nf;
+                        // a track start drops the carried state: f = 0 * f + a x
+                        f = fmaf(zero_lanes(CF[p], half_mask(sb0, sb1, p)), f, AX[p]);
                         Fs[p] = f;
                     }
                     if (cross) {
@@ -414,11 +425,8 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
                     float b = 0.f;
 #pragma unroll
                     for (int p = SP - 1; p >= 0; --p) {
-                        const float nb = fmaf(CF[p], b, AX[p]);
-                        if ((eany >> p) & 1u)
-                            b = ((ebl >> p) & 1u) ? AX[p] : nb;
-                        else
-                            b = nb;
+                        // a track end drops the state carried from the next track
+                        b = fmaf(zero_lanes(CF[p], half_mask(eb0, eb1, p)), b, AX[p]);
                         Bs[p] = b;
                     }
                     if (cross) {
@@ -511,7 +519,9 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
         }
         wave_lds_sync();
 
-        // ---- head layer 1: hidden = SiLU(W1 p + b1), tracks on rows
+        // ---- head layer 1: hidden = SiLU(W1 p + b1), tracks on rows (rows past
+        // the tile's tracks are never stored; their loads repeat the last row)
+        const int prow = cc < kMaxTracksPerTile ? cc : kMaxTracksPerTile - 1;
         f32x16 hid[MT];
 #pragma unroll
         for (int m = 0; m < MT; ++m)
@@ -521,7 +531,7 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
         for (int ks = 0; ks < KS1; ++ks) {
             float v[8];
 #pragma unroll
-            for (int u = 0; u < KL; ++u) v[u] = pooled[cc * C::PLS + ks * K + hh * KL + u];
+            for (int u = 0; u < KL; ++u) v[u] = pooled[prow * C::PLS + ks * K + hh * KL + u];
             FT a_hi, a_lo;
             split_operand<F>(v, a_hi, a_lo);
             const FT *w1 = reinterpret_cast<const FT *>(P.w1);
@@ -546,7 +556,7 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
                                                           -v * kLog2e, -kGateClamp, kGateClamp)));
                 else
                     sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
-                pooled[row * C::PLS + 32 * m + cc] = sv;
+                if (row < kMaxTracksPerTile) pooled[row * C::PLS + 32 * m + cc] = sv;
             }
         }
         wave_lds_sync();
@@ -558,7 +568,7 @@ __global__ __launch_bounds__((64 * KCfg<D, OP>::WAVES), 1) void tf_encoder_kerne
         for (int ks = 0; ks < KS1; ++ks) {
             float v[8];
 #pragma unroll
-            for (int u = 0; u < KL; ++u) v[u] = pooled[cc * C::PLS + ks * K + hh * KL + u];
+            for (int u = 0; u < KL; ++u) v[u] = pooled[prow * C::PLS + ks * K + hh * KL + u];
             FT a_hi, a_lo;
             split_operand<F>(v, a_hi, a_lo);
             const FT b = reinterpret_cast<const FT *>(P.w2)[ks * 64 + lane];
@@ -642,12 +652,15 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
                                        tf_weights **out) {
     if (!out) return TF_EINVAL;
     *out = nullptr;
-    if (!cfg || !blob || cfg->reserved != 0) return TF_EINVAL;
+    if (!cfg || !blob || cfg->max_hits < 0) return TF_EINVAL;
     const int L = cfg->n_layers, D = cfg->d_model;
     if (cfg->dtype != TF_FP32 && cfg->dtype != TF_BF16 && cfg->dtype != TF_BF16_F16ACT) return TF_EINVAL;
     if (L < 0 || D <= 0) return TF_EINVAL;
     if (!(D == 32 || D == 64 || D == 128 || D == 256) || L > 64) return TF_EUNSUPPORTED;
     if (n_floats != tf_blob_size(L, D)) return TF_EINVAL;
+    const int supported = D <= 128 ? 64 : 32;
+    const int limit = cfg->max_hits == 0 ? supported : cfg->max_hits;
+    if (limit > supported) return TF_EUNSUPPORTED;
     const int op = cfg->dtype == TF_BF16 ? OP_BF16 : cfg->dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32;
     const bool half = op != OP_F32;
     const int K = half ? 16 : 2, KL = K / 2, KS1 = D / K, KS2 = 64 / K, RPK = 16 / KL;
@@ -766,7 +779,9 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     w->n_layers = L;
     w->d = D;
     w->dtype = cfg->dtype;
-    w->max_hits = (half ? D <= 128 : D <= 64) ? 64 : 32;
+    // tile shape: one 32-hit tile per wave (two waves per SIMD in the 16-bit
+    // modes) when tracks have at most 32 hits, two 32-hit tiles otherwise
+    w->max_hits = limit <= 32 ? 32 : 64;
     w->err = reinterpret_cast<int *>(b + o_err);
     DevParams &P = w->params;
     P.emb = reinterpret_cast<const float4 *>(b + o_emb);
@@ -793,28 +808,38 @@ extern "C" void tf_weights_destroy(tf_weights *w) {
 extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
 
 namespace {
-template <int D, int OP>
+template <int D, int OP, int HT>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                   const tf_weights *w, float *out, hipStream_t stream) {
-    using C = KCfg<D, OP>;
-    // at least 16 tracks per wave; at most two workgroups per compute unit
-    long long waves = (n_tracks + 15) / 16;
+    using C = KCfg<D, OP, HT>;
+    // at least 8 tracks per wave; at most OCC workgroups of resident waves per
+    // compute unit, so that every wave's track group is scheduled at once
+    long long waves = (n_tracks + 7) / 8;
     long long blocks = (waves + C::WAVES - 1) / C::WAVES;
-    const long long cap = (long long)w->cu_count * 2;
+    const long long cap = (long long)w->cu_count * C::OCC * (4 / C::WAVES > 0 ? 4 / C::WAVES : 1);
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((tf_encoder_kernel<D, OP>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
                        hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, w->err);
     return hipGetLastError();
+}
+
+template <int D, int OP>
+hipError_t launch_ht(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                     const tf_weights *w, float *out, hipStream_t stream) {
+    if constexpr (D <= 128) {
+        if (w->max_hits == 64) return launch<D, OP, 2>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    }
+    return launch<D, OP, 1>(hits, n_hits, offsets, n_tracks, w, out, stream);
 }
 
 template <int D>
 hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                     const tf_weights *w, float *out, hipStream_t stream) {
     switch (w->dtype) {
-        case TF_BF16: return launch<D, OP_BF16>(hits, n_hits, offsets, n_tracks, w, out, stream);
-        case TF_BF16_F16ACT: return launch<D, OP_F16>(hits, n_hits, offsets, n_tracks, w, out, stream);
-        default: return launch<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16: return launch_ht<D, OP_BF16>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16_F16ACT: return launch_ht<D, OP_F16>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        default: return launch_ht<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
     }
 }
 }  // namespace

@@ -61,7 +61,7 @@ def test_argument_checks_without_gpu(tf):
     assert L.tf_weights_create(ctypes.byref(cfg), blob, 347909, None) == tf.TF_EINVAL
     bad = tf.Config(4, 128, 7, 0)
     assert L.tf_weights_create(ctypes.byref(bad), blob, 347909, ctypes.byref(h)) == tf.TF_EINVAL
-    bad = tf.Config(4, 128, tf.TF_FP32, 1)
+    bad = tf.Config(4, 128, tf.TF_FP32, -1)
     assert L.tf_weights_create(ctypes.byref(bad), blob, 347909, ctypes.byref(h)) == tf.TF_EINVAL
     bad = tf.Config(4, 96, tf.TF_FP32, 0)
     assert L.tf_weights_create(ctypes.byref(bad), blob, L.tf_blob_size(4, 96), ctypes.byref(h)) \

@@ -30,10 +30,11 @@ def tf():
     return tf
 
 
-def _weights(tf, w, blob=None, mode=None):
+def _weights(tf, w, blob=None, mode=None, max_hits=None):
     blob = ts.make_weights(w) if blob is None else blob
     mode = tf.MODE_FOR_WEIGHTS[w.dtype] if mode is None else mode
-    return tf.Weights(blob, w.n_layers, w.d_model, mode), blob
+    max_hits = w.len_max if max_hits is None else max_hits
+    return tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits), blob
 
 
 def _gpu(tf, W, hits, offs, n_tracks=None):
@@ -68,7 +69,7 @@ def test_fixed_lengths(tf, name, d, L):
     """All tracks of one length: length 1 (scan of one step) and the maximum."""
     w = dataclasses.replace(ts.WORKLOADS[name], len_min=L, len_max=L, n_det_layers=max(L, 8))
     print(f"[fixed] {name} L={L}", flush=True)
-    W, blob = _weights(tf, w)
+    W, blob = _weights(tf, w, max_hits=L)
     assert W.max_hits >= L
     hits, offs = ts.make_tracks(w, n_tracks=300)
     g = _gpu(tf, W, hits, offs)
@@ -77,12 +78,15 @@ def test_fixed_lengths(tf, name, d, L):
     assert tf.device_error(W) == 0
 
 
-@pytest.mark.parametrize("name", ["d128x4_fp32_65k", "deploy_d128x4_bf16_8m", "d256x6_bf16_1m"])
-def test_ragged_mix_and_small_batches(tf, name):
-    """Lengths 1..max mixed at random, batches of 1, 2, 33 and 1000 tracks."""
+@pytest.mark.parametrize("name,max_hits", [("d128x4_fp32_65k", 0), ("d128x4_fp32_65k", 32),
+                                           ("deploy_d128x4_bf16_8m", 0), ("deploy_d128x4_bf16_8m", 32),
+                                           ("d256x6_bf16_1m", 0)])
+def test_ragged_mix_and_small_batches(tf, name, max_hits):
+    """Lengths 1..max mixed at random, batches of 1, 2, 33 and 1000 tracks, for
+    both tile shapes (one or two 32-hit tiles per wave)."""
     w0 = ts.WORKLOADS[name]
-    print(f"[ragged] {name}", flush=True)
-    W, blob = _weights(tf, w0)
+    print(f"[ragged] {name} max_hits={max_hits}", flush=True)
+    W, blob = _weights(tf, w0, max_hits=max_hits)
     maxL = W.max_hits
     w = dataclasses.replace(w0, len_min=1, len_max=maxL, n_det_layers=maxL)
     hits, offs = ts.make_tracks(w, n_tracks=1000)
