@@ -10,27 +10,37 @@
 //
 // How (Sec. Kernel adaptation is prior art for another GPU; this is a design
 // for CDNA4):
-//  * One wave64 owns a tile of whole tracks: up to CAP = 64 hits (32 at
-//    d = 256), packed greedily from the unpadded batch, at most 32 tracks.
-//    The residual stream of the tile (CAP x d fp32) stays in registers for all
+//  * One wave64 owns a tile of whole tracks: 32 hit slots (64 when tracks may
+//    be longer than 32 hits), packed greedily from the unpadded batch.  The
+//    residual stream of the tile (slots x d, fp32) stays in registers for all
 //    layers; nothing but hits, offsets and the five outputs touches HBM.
-//  * Projections run on 32x32 matrix cores: v_mfma_f32_32x32x16_bf16 for the
-//    bf16 model, v_mfma_f32_32x32x2_f32 for the fp32 model.  The residual
-//    stream is held transposed (channels on MFMA rows, hits on columns), which
-//    is exactly the A-operand layout of the input projection, so the norm
-//    output feeds the matrix core without any data movement.
+//  * All waves of a workgroup walk the same sequence of weight "stages" (the
+//    input projection of a 32-channel chunk, the output projection of that
+//    chunk, the head) in lockstep.  Each stage is copied once per workgroup
+//    from L2 into a double-buffered LDS ring, prefetched into registers one
+//    stage ahead, so matrix-core operands come from LDS and the copy of stage
+//    s+1 overlaps the compute of stage s.  Weights are stored in the device
+//    already in per-lane fragment order, so every copy and every operand read
+//    is a contiguous 1 KiB per wave.
+//  * Projections run on 32x32 matrix cores: v_mfma_f32_32x32x16_{bf16,f16}
+//    for the 16-bit modes, v_mfma_f32_32x32x2_f32 for the fp32 model.  The
+//    residual stream is held transposed (channels on MFMA rows, hits on
+//    columns), which is exactly the A-operand layout of the input projection,
+//    so the norm output feeds the matrix core without any data movement.
 //  * The input projection puts hits on MFMA rows.  Hit slots are assigned to
-//    rows so that each lane's 16 accumulator rows per hit tile are consecutive
-//    hits of one of two streams (lanes 0-31: first half of the tile, lanes
-//    32-63: second half).  The scan along the track therefore runs serially in
-//    registers, one channel per lane; the single track that may straddle the
-//    two streams is finished with one cross-half exchange of the boundary
-//    state and a rerun of its steps in the second stream, so every track sees
-//    the same sequence of operations wherever it sits in a tile.
+//    rows so that each lane's 16 accumulator rows per 32-hit tile are
+//    consecutive hits of one of two streams (lanes 0-31: first half of the
+//    tile, lanes 32-63: second half).  The scan along the track therefore runs
+//    serially in registers, one channel per lane; the single track that may
+//    straddle the two streams is finished with one cross-half exchange of the
+//    boundary state and a rerun of its steps in the second stream, so every
+//    track sees the same sequence of operations wherever it sits in a tile.
 //  * Scan outputs go through a wave-private LDS buffer once per 32-channel
 //    chunk (the only transpose), and the output projection for that chunk is
-//    accumulated straight into the residual registers (K split over chunks).
-//  * Mean pooling and the head run per tile on the same wave.
+//    accumulated into the residual registers (K split over chunks).
+//  * Mean pooling runs per 32-channel block through wave-private LDS; the head
+//    is computed transposed (hidden units on rows), so its hidden layer feeds
+//    the second head GEMM straight from the accumulators.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -46,6 +56,8 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(8))) float f32x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 // Matrix-core operand types.  OP_F32: fp32 weights and operands
 // (v_mfma_f32_32x32x2_f32).  OP_BF16: bf16 weights and bf16 activation
@@ -53,17 +65,17 @@ typedef __attribute__((ext_vector_type(8))) float f32x8;
 // exactly in fp16 and fp16 activation operands (v_mfma_f32_32x32x16_f16).
 // Accumulation is fp32 in all three.
 enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
-typedef __attribute__((ext_vector_type(16))) float f32x16;
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRmsEps = 1e-6f;
-// |gate pre-activation| is clamped to 80 (scaled by log2 e) so that exp stays
-// finite; the change in the gate is below exp(-80).
+// |gate pre-activation| is clamped to 80 (scaled by log2 e in the 16-bit
+// modes) so that exp stays finite; the change in the gate is below exp(-80).
 constexpr float kGateClamp = 80.0f * kLog2e;
 constexpr int kLdsBytesMax = 160 * 1024;
+constexpr int kCopyBytes = 1024;  // one wave-wide 16-byte-per-lane copy
 
-constexpr int cmin(int a, int b) { return a < b ? a : b; }
-constexpr size_t round16(size_t v) { return (v + 15) & ~size_t(15); }
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int round_up(int v, int m) { return (v + m - 1) / m * m; }
 
 // ---------------------------------------------------------------------------
 // Compile-time shape of one kernel instance.
@@ -72,28 +84,46 @@ template <int D, int OP, int HT_>
 struct KCfg {
     static constexpr bool HALF = OP != OP_F32;
     static constexpr int HT = HT_;               // 32-hit tiles per wave tile
-    static constexpr int MAXTR = 16 * HT;        // tracks per wave tile
-    static constexpr int CAP = 32 * HT;          // hits per wave tile
+    static constexpr int CAP = 32 * HT;          // hit slots per wave tile
     static constexpr int SP = 16 * HT;           // positions per stream (2 streams)
+    static constexpr int MAXTR = 16 * HT;        // tracks per wave tile
     static constexpr int MT = D / 32;            // 32-channel blocks
+    static constexpr int NCH = D / 32;           // chunks of the scan / output projection
     static constexpr int K = HALF ? 16 : 2;      // MFMA reduction depth
     static constexpr int KL = K / 2;             // operand values per lane per k-step
     static constexpr int KS1 = D / K;            // k-steps over d
     static constexpr int KS2 = 64 / K;           // k-steps over one chunk of [f; b]
     static constexpr int RPK = 16 / KL;          // k-steps per 16 accumulator rows
-    static constexpr int FBS = HALF ? 72 : 65;   // LDS row stride of [f; b] (elements)
-    static constexpr int STS = 33;               // LDS row stride of pooling stage (floats)
-    static constexpr int PLS = D + 4;            // LDS row stride of pooled / hidden (floats)
-    static constexpr size_t FB_BYTES = size_t(CAP) * FBS * (HALF ? 2 : 4);
-    static constexpr size_t ST_BYTES = size_t(CAP) * STS * 4;
-    static constexpr size_t POOL_OFF = round16(FB_BYTES > ST_BYTES ? FB_BYTES : ST_BYTES);
-    static constexpr size_t META_OFF = round16(POOL_OFF + size_t(MAXTR) * PLS * 4);
-    static constexpr size_t WAVE_BYTES = round16(META_OFF + 2 * MAXTR * 4);
-    // waves per SIMD: two when a wave fits in half the register file
-    static constexpr int OCC = (HALF && HT == 1 && D <= 128) ? 2 : 1;
-    static constexpr int WAVES = cmin(4, int(kLdsBytesMax / OCC / WAVE_BYTES));
-    static_assert(WAVES >= 1, "LDS budget");
+    static constexpr int KPB = 32 / K;           // k-steps per 32-channel block
+    static constexpr int EB = HALF ? 2 : 4;      // operand element bytes
+    static constexpr int FRAG = 64 * KL * EB;    // one wave-wide operand fragment
+    // weight stages (all padded to STAGE bytes)
+    static constexpr int G1_FR = 2 * KS1;        // candidate + gate fragments of a chunk
+    static constexpr int G2_FR = MT * KS2;       // output-projection fragments of a chunk
+    static constexpr int G1_BYTES = G1_FR * FRAG + 64 * 4;  // + bx[32], bg[32]
+    static constexpr int G2_BYTES = G2_FR * FRAG + D * 4;   // + bout[D]
+    static constexpr int STAGE = round_up(cmax(G1_BYTES, G2_BYTES), kCopyBytes);
+    static constexpr int KSPS_RAW = (STAGE - D * 4) / (MT * FRAG);   // head-1 k-steps per stage
+    static constexpr int KSPS = (KSPS_RAW >= KS1 ? KS1 : KSPS_RAW / KPB * KPB);
+    static constexpr int NH1 = KS1 / KSPS;       // head-1 stages
+    static constexpr int COPIES = STAGE / kCopyBytes;
+    // waves per workgroup and per SIMD
+    static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 8 : 4;
+    static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;  // copies per wave per stage
+    // wave-private LDS: [f; b] buffer, aliased by the pooling scratch
+    static constexpr int FBS = HALF ? 72 : 65;   // row stride of [f; b] (elements)
+    static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
+    static constexpr int FB_BYTES = CAP * FBS * EB;
+    static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
+    static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 2 * MAXTR * 4;
+    // workgroup LDS: embedding table, two stage slots, wave regions
+    static constexpr int EMB_BYTES = D * 16;
+    static constexpr int SLOT0 = EMB_BYTES;
+    static constexpr int WAVE0 = SLOT0 + 2 * STAGE;
+    static constexpr int LDS_BYTES = WAVE0 + WAVES * WAVE_BYTES;
+    static_assert(LDS_BYTES <= kLdsBytesMax, "LDS budget");
     static_assert(D % 32 == 0, "d must be a multiple of 32");
+    static_assert(KSPS >= KPB && KS1 % KSPS == 0, "head stage split");
 };
 
 template <int OP> struct Frag;
@@ -128,18 +158,12 @@ template <> struct Frag<OP_F32> {
     static __device__ __forceinline__ T pack(const float *v) { return v[0]; }
 };
 
-// Device-side weights, already in the order the kernel reads them.
+// Device-side weights.
 struct DevParams {
-    const float4 *emb;   // [D] (w_x, w_y, w_z, b) with the min-max map folded in
-    const void *win;     // [L][NCH][2][KS1][64][KL]  candidate / gate B fragments
-    const float *bin;    // [L][2][D] candidate bias, gate bias (gate scaled by -log2 e)
-    const void *wout;    // [L][NCH][MT][KS2][64][KL]  output-projection A fragments
-    const float *bout;   // [L][D]
-    const void *w1;      // [MT][KS1][64][KL]  head layer 1 B fragments
-    const float *b1;     // [D]
-    const void *w2;      // [KS1][64][KL]      head layer 2 B fragments (cols >= 5 zero)
-    const float *b2;     // [5]
+    const float4 *emb;           // [D] (w_x, w_y, w_z, b) with the min-max map folded in
+    const unsigned char *stages; // n_stages x STAGE bytes, in the order the kernel walks them
     int n_layers;
+    int n_stages;                // 2 * n_layers * NCH + NH1 + 1
 };
 
 __device__ __forceinline__ void wave_lds_sync() {
@@ -203,31 +227,73 @@ __device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int
     }
 }
 
+// Double-buffered copy of the weight stages into LDS.  Each wave copies its
+// share (1 KiB pieces w, w + WAVES, ...) of the next stage into registers,
+// stores them to the free slot after the current stage's compute, and the
+// workgroup barrier publishes the slot.
+template <class C>
+struct StageCopier {
+    u32x4 buf[C::LPW];
+    __device__ __forceinline__ void load(const unsigned char *stages, int n_stages, int s, int wid, int lane) {
+        const unsigned char *src = stages + (size_t)(s % n_stages) * C::STAGE;
+#pragma unroll
+        for (int i = 0; i < C::LPW; ++i) {
+            const int piece = wid + i * C::WAVES;
+            if (piece < C::COPIES)
+                buf[i] = *reinterpret_cast<const u32x4 *>(src + piece * kCopyBytes + lane * 16);
+        }
+    }
+    __device__ __forceinline__ void store(char *slot, int wid, int lane) {
+#pragma unroll
+        for (int i = 0; i < C::LPW; ++i) {
+            const int piece = wid + i * C::WAVES;
+            if (piece < C::COPIES) *reinterpret_cast<u32x4 *>(slot + piece * kCopyBytes + lane * 16) = buf[i];
+        }
+    }
+};
+
 template <int D, int OP, int HT_>
-__global__ __attribute__((amdgpu_flat_work_group_size(64, 256), amdgpu_waves_per_eu(KCfg<D, OP, HT_>::OCC, KCfg<D, OP, HT_>::OCC)))
-void tf_encoder_kernel(
-    const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
-    int n_tracks, DevParams P, float *__restrict__ out, int *__restrict__ err) {
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
+                          amdgpu_waves_per_eu(KCfg<D, OP, HT_>::WAVES / 4, KCfg<D, OP, HT_>::WAVES / 4)))
+void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
+                       int n_tracks, DevParams P, float *__restrict__ out, int *__restrict__ err) {
     using C = KCfg<D, OP, HT_>;
     using F = Frag<OP>;
     using FT = typename F::T;
     using FE = typename F::E;
-    constexpr int kMaxTracksPerTile = C::MAXTR;
     constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
-    constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK;
-    constexpr int NCH = D / 32;
+    constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK, KPB = C::KPB, NCH = C::NCH;
+    constexpr int MAXTR = C::MAXTR;
 
-    __shared__ __attribute__((aligned(16))) char smem[C::WAVES * C::WAVE_BYTES];
+    __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
     const int lane = threadIdx.x & 63;
-    const int wid = threadIdx.x >> 6;
-    char *ws = smem + size_t(wid) * C::WAVE_BYTES;
-    float *stage = reinterpret_cast<float *>(ws);                  // [CAP][STS]
-    float *pooled = reinterpret_cast<float *>(ws + C::POOL_OFF);   // [MAXTR][PLS]
-    int *t_start = reinterpret_cast<int *>(ws + C::META_OFF);      // [MAXTR]
-    int *t_len = t_start + kMaxTracksPerTile;                      // [MAXTR]
+    const int wid = uniform(threadIdx.x >> 6);
+    const float4 *emb = reinterpret_cast<const float4 *>(smem);
+    char *ws = smem + C::WAVE0 + wid * C::WAVE_BYTES;
+    float *stage = reinterpret_cast<float *>(ws);                           // [CAP][STS]
+    float *pblk = stage + CAP * C::STS;                                     // [MAXTR][STS]
+    int *t_start = reinterpret_cast<int *>(ws + C::WAVE_BYTES - 2 * MAXTR * 4);
+    int *t_len = t_start + MAXTR;
 
     const int hh = lane >> 5;  // lane half
     const int cc = lane & 31;  // lane column
+
+    // embedding table to LDS, first two weight stages in flight
+    for (int i = threadIdx.x; i < D; i += 64 * C::WAVES) reinterpret_cast<float4 *>(smem)[i] = P.emb[i];
+    StageCopier<C> cp;
+    cp.load(P.stages, P.n_stages, 0, wid, lane);
+    cp.store(smem + C::SLOT0, wid, lane);
+    cp.load(P.stages, P.n_stages, 1, wid, lane);
+    __syncthreads();
+    int sidx = 0;  // index of the stage being consumed (counts across tiles)
+    // after the compute of stage sidx: publish stage sidx+1, start loading sidx+2
+    auto advance = [&]() {
+        cp.store(smem + C::SLOT0 + ((sidx + 1) & 1) * C::STAGE, wid, lane);
+        __syncthreads();
+        cp.load(P.stages, P.n_stages, sidx + 2, wid, lane);
+        ++sidx;
+    };
+    auto slot = [&]() -> const char * { return smem + C::SLOT0 + (sidx & 1) * C::STAGE; };
 
     // Contiguous group of tracks for this wave, balanced by track count.
     const long long gw = (long long)blockIdx.x * C::WAVES + wid;
@@ -239,351 +305,380 @@ void tf_encoder_kernel(
     const float qnan = __builtin_nanf("");
 
     int t = g_begin;
-    while (t < g_end) {
-        // ---- pick the tile: the longest run of whole tracks t.. with <= CAP hits
-        const int idx = t + lane;
-        int off = 0;
-        if (lane <= kMaxTracksPerTile && idx <= g_end) off = offsets[idx];
-        const int base = uniform(off);
-        const int prev = __shfl_up(off, 1);
-        const bool ok = lane >= 1 && lane <= kMaxTracksPerTile && idx <= g_end && off >= prev &&
-                        (long long)off - base <= CAP && (long long)off <= n_hits_total && base >= 0;
-        const unsigned long long okm = __ballot(ok);
-        const int k = __builtin_ctzll(~(okm >> 1));
-        if (k == 0) {
-            // track t alone cannot be fitted: rows outside [0, n_hits), an end
-            // offset before its start, or more hits than a tile holds
-            const int off1 = __builtin_amdgcn_readlane(off, 1);
-            const bool bad = base < 0 || off1 < base || (long long)off1 > n_hits_total;
-            errbits |= bad ? TF_DEVERR_BAD_OFFSETS : TF_DEVERR_TOO_LONG;
-            if (lane < 5) out[(size_t)t * 5 + lane] = qnan;
-            t += 1;
-            continue;
-        }
-        const int n = __builtin_amdgcn_readlane(off, k) - base;  // hits in the tile, 0..CAP
-        if (n == 0) {
-            errbits |= TF_DEVERR_EMPTY_TRACK;
-            for (int e = lane; e < 5 * k; e += 64) out[(size_t)t * 5 + e] = qnan;
-            t += k;
-            continue;
-        }
-        // track metadata and start mask
-        const int nxt = __shfl_down(off, 1);
-        if (lane < k) {
-            t_start[lane] = off - base;
-            t_len[lane] = nxt - off;
-        }
-        unsigned long long smask = 0;
-        bool empty = false;
-        for (int j = 0; j < k; ++j) {
-            const int sj = __builtin_amdgcn_readlane(off, j) - base;
-            const int lj = __builtin_amdgcn_readlane(off, j + 1) - base - sj;
-            if (lj > 0)
-                smask |= 1ull << sj;
-            else
-                empty = true;
-        }
-        if (empty) errbits |= TF_DEVERR_EMPTY_TRACK;
-        const unsigned long long valid = n >= 64 ? ~0ull : ((1ull << n) - 1);
-        const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
-        const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
-        const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
-        const unsigned int sb0 = unsigned(vstart) & spm, sb1 = unsigned(vstart >> SP) & spm;
-        const unsigned int eb0 = unsigned(emask) & spm, eb1 = unsigned(emask >> SP) & spm;
-        // One track may straddle the two streams (tile hit SP is not a start).
-        const bool cross = n > SP && !((smask >> SP) & 1ull);
-        const int fs1 = sb1 ? __builtin_ctz(sb1) : SP;           // fwd fix-up: stream 1, p < fs1
-        const int le0 = eb0 ? 31 - __builtin_clz(eb0) : -1;      // bwd fix-up: stream 0, p > le0
-
-        // ---- embedding (normalisation folded into the weights), residual stream
-        // r[m][nt][q]: channel 32 m + 8 (q/4) + 4 hh + (q%4), hit slot 32 nt + cc
-        f32x16 r[MT][HT];
-#pragma unroll
-        for (int nt = 0; nt < HT; ++nt) {
-            const int th = slot_to_hit<SP>(32 * nt + cc);
-            float hx = 0.f, hy = 0.f, hz = 0.f;
-            if (th < n) {
-                const float *hp = hits + ((size_t)base + th) * 3;
-                hx = hp[0];
-                hy = hp[1];
-                hz = hp[2];
+    for (;;) {
+        // ---- pick the tile: the longest run of whole tracks t.. with <= CAP hits.
+        // Tracks that cannot be fitted are flagged and skipped here.
+        int k = 0, n = 0, base = 0, off = 0;
+        while (t < g_end) {
+            const int idx = t + lane;
+            off = 0;
+            if (lane <= MAXTR && idx <= g_end) off = offsets[idx];
+            base = uniform(off);
+            const int prev = __shfl_up(off, 1);
+            const bool ok = lane >= 1 && lane <= MAXTR && idx <= g_end && off >= prev &&
+                            (long long)off - base <= CAP && (long long)off <= n_hits_total && base >= 0;
+            const unsigned long long okm = __ballot(ok);
+            k = __builtin_ctzll(~(okm >> 1));
+            if (k == 0) {
+                // rows outside [0, n_hits), an end offset before its start, or
+                // more hits than a tile holds
+                const int off1 = __builtin_amdgcn_readlane(off, 1);
+                const bool bad = base < 0 || off1 < base || (long long)off1 > n_hits_total;
+                errbits |= bad ? TF_DEVERR_BAD_OFFSETS : TF_DEVERR_TOO_LONG;
+                if (lane < 5) out[(size_t)t * 5 + lane] = qnan;
+                t += 1;
+                continue;
             }
+            n = __builtin_amdgcn_readlane(off, k) - base;
+            if (n == 0) {  // all k tracks are empty
+                errbits |= TF_DEVERR_EMPTY_TRACK;
+                for (int e = lane; e < 5 * k; e += 64) out[(size_t)t * 5 + e] = qnan;
+                t += k;
+                continue;
+            }
+            break;
+        }
+        const bool work = t < g_end;
+        if (!__syncthreads_or(work)) break;  // every wave of the workgroup is done
+
+        // ---- tile metadata: track starts and lengths, start/end masks per stream
+        unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
+        bool cross = false;
+        int fs1 = SP, le0 = -1;
+        f32x16 r[MT][HT];
+        if (work) {
+            const int nxt = __shfl_down(off, 1);
+            if (lane < k) {
+                t_start[lane] = off - base;
+                t_len[lane] = nxt - off;
+            }
+            unsigned long long smask = 0;
+            bool empty = false;
+            for (int j = 0; j < k; ++j) {
+                const int sj = __builtin_amdgcn_readlane(off, j) - base;
+                const int lj = __builtin_amdgcn_readlane(off, j + 1) - base - sj;
+                if (lj > 0)
+                    smask |= 1ull << sj;
+                else
+                    empty = true;
+            }
+            if (empty) errbits |= TF_DEVERR_EMPTY_TRACK;
+            const unsigned long long valid = n >= 64 ? ~0ull : ((1ull << n) - 1);
+            const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
+            const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
+            const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
+            sb0 = unsigned(vstart) & spm;
+            sb1 = unsigned(vstart >> SP) & spm;
+            eb0 = unsigned(emask) & spm;
+            eb1 = unsigned(emask >> SP) & spm;
+            // one track may straddle the two streams (tile hit SP is not a start)
+            cross = n > SP && !((smask >> SP) & 1ull);
+            fs1 = sb1 ? __builtin_ctz(sb1) : SP;       // fwd rerun: stream 1, p < fs1
+            le0 = eb0 ? 31 - __builtin_clz(eb0) : -1;  // bwd rerun: stream 0, p > le0
+
+            // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
-            for (int m = 0; m < MT; ++m)
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const float4 e = P.emb[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
-                    r[m][nt][q] = fmaf(e.x, hx, fmaf(e.y, hy, fmaf(e.z, hz, e.w)));
+            for (int nt = 0; nt < HT; ++nt) {
+                const int th = slot_to_hit<SP>(32 * nt + cc);
+                float hx = 0.f, hy = 0.f, hz = 0.f;
+                if (th < n) {
+                    const float *hp = hits + ((size_t)base + th) * 3;
+                    hx = hp[0];
+                    hy = hp[1];
+                    hz = hp[2];
                 }
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        const float4 e = emb[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                        r[m][nt][q] = fmaf(e.x, hx, fmaf(e.y, hy, fmaf(e.z, hz, e.w)));
+                    }
+            }
         }
 
         // ---- layers
         for (int l = 0; l < P.n_layers; ++l) {
-            // RMSNorm: each lane holds half the channels of hit slot 32 nt + cc
             FT yf[HT][KS1];
+            if (work) {
+                // RMSNorm: each lane holds half the channels of hit slot 32 nt + cc
 #pragma unroll
-            for (int nt = 0; nt < HT; ++nt) {
-                float ss = 0.f;
-#pragma unroll
-                for (int m = 0; m < MT; ++m)
-#pragma unroll
-                    for (int q = 0; q < 16; ++q) ss = fmaf(r[m][nt][q], r[m][nt][q], ss);
-                ss += __shfl_xor(ss, 32);
-                float rs;
-                if constexpr (C::HALF)
-                    rs = rsqrtf(ss * (1.0f / D) + kRmsEps);
-                else
-                    rs = 1.0f / sqrtf(ss * (1.0f / D) + kRmsEps);
-#pragma unroll
-                for (int ks = 0; ks < KS1; ++ks) {
-                    float v[8];
-#pragma unroll
-                    for (int u = 0; u < KL; ++u) v[u] = r[ks / RPK][nt][(ks % RPK) * KL + u] * rs;
-                    yf[nt][ks] = F::pack(v);
-                }
-            }
-            const char *winl = static_cast<const char *>(P.win) +
-                               (size_t)l * NCH * 2 * KS1 * 64 * sizeof(FT);
-            const char *woutl = static_cast<const char *>(P.wout) +
-                                (size_t)l * NCH * MT * KS2 * 64 * sizeof(FT);
-            const float *binl = P.bin + (size_t)l * 2 * D;
-
-            for (int ch = 0; ch < NCH; ++ch) {
-                // input projection for channels 32 ch .. +31: hits on rows
-                f32x16 ax[HT], gx[HT];
-#pragma unroll
-                for (int nt = 0; nt < HT; ++nt)
-#pragma unroll
-                    for (int q = 0; q < 16; ++q) {
-                        ax[nt][q] = 0.f;
-                        gx[nt][q] = 0.f;
-                    }
-                const FT *wx = reinterpret_cast<const FT *>(winl) + (size_t)(ch * 2 + 0) * KS1 * 64;
-                const FT *wg = reinterpret_cast<const FT *>(winl) + (size_t)(ch * 2 + 1) * KS1 * 64;
-#pragma unroll
-                for (int ks = 0; ks < KS1; ++ks) {
-                    const FT bx = wx[ks * 64 + lane];
-                    const FT bg = wg[ks * 64 + lane];
-#pragma unroll
-                    for (int nt = 0; nt < HT; ++nt) {
-                        ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
-                        gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
-                    }
-                }
-                // gate and the two scan coefficients: a x and (1 - a)
-                const float bxv = binl[32 * ch + cc];
-                const float bgv = binl[D + 32 * ch + cc];
-                float AX[HT * 16], CF[HT * 16];
-#pragma unroll
-                for (int nt = 0; nt < HT; ++nt)
-#pragma unroll
-                    for (int q = 0; q < 16; ++q) {
-                        const float x = ax[nt][q] + bxv;
-                        float e, a;  // e = exp(-gate), a = sigmoid(gate) = 1 / (1 + e)
-                        if constexpr (C::HALF) {
-                            // hardware exp2 / reciprocal; the bias holds -log2(e) * b
-                            e = __builtin_amdgcn_exp2f(
-                                __builtin_amdgcn_fmed3f(fmaf(gx[nt][q], -kLog2e, bgv), -kGateClamp, kGateClamp));
-                            a = __builtin_amdgcn_rcpf(1.0f + e);
-                        } else {
-                            // correctly rounded division and library exp for the fp32 model
-                            e = expf(-__builtin_amdgcn_fmed3f(gx[nt][q] + bgv, -80.0f, 80.0f));
-                            a = 1.0f / (1.0f + e);
-                        }
-                        AX[nt * 16 + q] = a * x;
-                        CF[nt * 16 + q] = e * a;
-                    }
-                // forward scan along this lane's stream
-                wave_lds_sync();  // previous chunk's reads of the [f; b] buffer are done
-                {
-                    float Fs[HT * 16];
-                    float f = 0.f;
-#pragma unroll
-                    for (int p = 0; p < SP; ++p) {
-                        // a track start drops the carried state: f = 0 * f + a x
-                        f = fmaf(zero_lanes(CF[p], half_mask(sb0, sb1, p)), f, AX[p]);
-                        Fs[p] = f;
-                    }
-                    if (cross) {
-                        // the track straddling the two streams: redo the head of stream 1
-                        // up to its first track start from the true state at the end of
-                        // stream 0, with the same operations as an unsplit scan
-                        float fr = __shfl_xor(Fs[SP - 1], 32);
-#pragma unroll
-                        for (int p = 0; p < SP; ++p) {
-                            if (p < fs1) {
-                                fr = fmaf(CF[p], fr, AX[p]);
-                                if (hh) Fs[p] = fr;
-                            }
-                        }
-                    }
-                    store_fb<C, FE>(ws, Fs, 0, hh, cc);
-                }
-                // reverse scan
-                {
-                    float Bs[HT * 16];
-                    float b = 0.f;
-#pragma unroll
-                    for (int p = SP - 1; p >= 0; --p) {
-                        // a track end drops the state carried from the next track
-                        b = fmaf(zero_lanes(CF[p], half_mask(eb0, eb1, p)), b, AX[p]);
-                        Bs[p] = b;
-                    }
-                    if (cross) {
-                        // and redo the tail of stream 0 back to its last track end from the
-                        // true reverse state at the start of stream 1
-                        float br = __shfl_xor(Bs[0], 32);
-#pragma unroll
-                        for (int p = SP - 1; p >= 0; --p) {
-                            if (p > le0) {
-                                br = fmaf(CF[p], br, AX[p]);
-                                if (!hh) Bs[p] = br;
-                            }
-                        }
-                    }
-                    store_fb<C, FE>(ws, Bs, 32, hh, cc);
-                }
-                wave_lds_sync();
-                // output projection, K split over chunks.  The 16-bit modes
-                // accumulate straight into the residual registers; the fp32 model
-                // sums each chunk in fresh accumulators and adds the chunk once, so
-                // the residual is rounded once per chunk rather than per k-step.
-                const FT *wo = reinterpret_cast<const FT *>(woutl) + (size_t)ch * MT * KS2 * 64;
-                f32x16 part[C::HALF ? 1 : MT][HT];
-                if constexpr (!C::HALF) {
+                for (int nt = 0; nt < HT; ++nt) {
+                    float ss = 0.f;
 #pragma unroll
                     for (int m = 0; m < MT; ++m)
 #pragma unroll
-                        for (int nt = 0; nt < HT; ++nt)
+                        for (int q = 0; q < 16; ++q) ss = fmaf(r[m][nt][q], r[m][nt][q], ss);
+                    ss += __shfl_xor(ss, 32);
+                    float rs;
+                    if constexpr (C::HALF)
+                        rs = rsqrtf(ss * (1.0f / D) + kRmsEps);
+                    else
+                        rs = 1.0f / sqrtf(ss * (1.0f / D) + kRmsEps);
 #pragma unroll
-                            for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
-                }
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        float v[8];
 #pragma unroll
-                for (int kk = 0; kk < KS2; ++kk) {
-                    FT bfr[HT];
-#pragma unroll
-                    for (int nt = 0; nt < HT; ++nt) {
-                        const int row = 32 * nt + cc;
-                        const FE *fb = reinterpret_cast<const FE *>(ws);
-                        bfr[nt] = *reinterpret_cast<const FT *>(fb + row * C::FBS + kk * K + hh * KL);
+                        for (int u = 0; u < KL; ++u) v[u] = r[ks / RPK][nt][(ks % RPK) * KL + u] * rs;
+                        yf[nt][ks] = F::pack(v);
                     }
+                }
+            }
+            for (int ch = 0; ch < NCH; ++ch) {
+                // ---- stage: input projection of channels 32 ch .. +31 (hits on rows),
+                // gate, both scans, [f; b] to LDS
+                if (work) {
+                    const char *sl = slot();
+                    const FT *wf = reinterpret_cast<const FT *>(sl);
+                    const float *bias = reinterpret_cast<const float *>(sl + C::G1_FR * C::FRAG);
+                    f32x16 ax[HT], gx[HT];
 #pragma unroll
-                    for (int m = 0; m < MT; ++m) {
-                        const FT a = wo[((size_t)m * KS2 + kk) * 64 + lane];
+                    for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) {
+                            ax[nt][q] = 0.f;
+                            gx[nt][q] = 0.f;
+                        }
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        const FT bx = wf[ks * 64 + lane];
+                        const FT bg = wf[(KS1 + ks) * 64 + lane];
 #pragma unroll
                         for (int nt = 0; nt < HT; ++nt) {
-                            if constexpr (C::HALF)
-                                r[m][nt] = F::mma(a, bfr[nt], r[m][nt]);
-                            else
-                                part[m][nt] = F::mma(a, bfr[nt], part[m][nt]);
+                            ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
+                            gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
                         }
                     }
-                }
-                if constexpr (!C::HALF) {
+                    const float bxv = bias[cc];
+                    const float bgv = bias[32 + cc];
+                    float AX[HT * 16], CF[HT * 16];
 #pragma unroll
-                    for (int m = 0; m < MT; ++m)
+                    for (int nt = 0; nt < HT; ++nt)
 #pragma unroll
-                        for (int nt = 0; nt < HT; ++nt) r[m][nt] += part[m][nt];
+                        for (int q = 0; q < 16; ++q) {
+                            const float x = ax[nt][q] + bxv;
+                            float e, a;  // e = exp(-gate), a = sigmoid(gate) = 1 / (1 + e)
+                            if constexpr (C::HALF) {
+                                // hardware exp2 / reciprocal; the bias holds -log2(e) * b
+                                e = __builtin_amdgcn_exp2f(
+                                    __builtin_amdgcn_fmed3f(fmaf(gx[nt][q], -kLog2e, bgv), -kGateClamp, kGateClamp));
+                                a = __builtin_amdgcn_rcpf(1.0f + e);
+                            } else {
+                                // correctly rounded division and library exp for the fp32 model
+                                e = expf(-__builtin_amdgcn_fmed3f(gx[nt][q] + bgv, -80.0f, 80.0f));
+                                a = 1.0f / (1.0f + e);
+                            }
+                            AX[nt * 16 + q] = a * x;
+                            CF[nt * 16 + q] = e * a;
+                        }
+                    wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
+                    // forward scan along this lane's stream
+                    {
+                        float Fs[HT * 16];
+                        float f = 0.f;
+#pragma unroll
+                        for (int p = 0; p < SP; ++p) {
+                            // a track start drops the carried state: f = 0 * f + a x
+                            f = fmaf(zero_lanes(CF[p], half_mask(sb0, sb1, p)), f, AX[p]);
+                            Fs[p] = f;
+                        }
+                        if (cross) {
+                            // the track straddling the two streams: redo the head of stream 1
+                            // up to its first track start from the true state at the end of
+                            // stream 0, with the same operations as an unsplit scan
+                            float fr = __shfl_xor(Fs[SP - 1], 32);
+#pragma unroll
+                            for (int p = 0; p < SP; ++p) {
+                                if (p < fs1) {
+                                    fr = fmaf(CF[p], fr, AX[p]);
+                                    if (hh) Fs[p] = fr;
+                                }
+                            }
+                        }
+                        store_fb<C, FE>(ws, Fs, 0, hh, cc);
+                    }
+                    // reverse scan
+                    {
+                        float Bs[HT * 16];
+                        float b = 0.f;
+#pragma unroll
+                        for (int p = SP - 1; p >= 0; --p) {
+                            // a track end drops the state carried from the next track
+                            b = fmaf(zero_lanes(CF[p], half_mask(eb0, eb1, p)), b, AX[p]);
+                            Bs[p] = b;
+                        }
+                        if (cross) {
+                            // and redo the tail of stream 0 back to its last track end from
+                            // the true reverse state at the start of stream 1
+                            float br = __shfl_xor(Bs[0], 32);
+#pragma unroll
+                            for (int p = SP - 1; p >= 0; --p) {
+                                if (p > le0) {
+                                    br = fmaf(CF[p], br, AX[p]);
+                                    if (!hh) Bs[p] = br;
+                                }
+                            }
+                        }
+                        store_fb<C, FE>(ws, Bs, 32, hh, cc);
+                    }
                 }
+                advance();
+
+                // ---- stage: output projection of this chunk, K split over chunks.  The
+                // 16-bit modes accumulate straight into the residual registers; the
+                // fp32 model sums the chunk in fresh accumulators and adds it once.
+                if (work) {
+                    const char *sl = slot();
+                    const FT *wo = reinterpret_cast<const FT *>(sl);
+                    f32x16 part[C::HALF ? 1 : MT][HT];
+                    if constexpr (!C::HALF) {
+#pragma unroll
+                        for (int m = 0; m < MT; ++m)
+#pragma unroll
+                            for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                                for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
+                    }
+#pragma unroll
+                    for (int kk = 0; kk < KS2; ++kk) {
+                        FT bfr[HT];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) {
+                            const FE *fb = reinterpret_cast<const FE *>(ws);
+                            bfr[nt] = *reinterpret_cast<const FT *>(fb + (32 * nt + cc) * C::FBS + kk * K + hh * KL);
+                        }
+#pragma unroll
+                        for (int m = 0; m < MT; ++m) {
+                            const FT a = wo[(m * KS2 + kk) * 64 + lane];
+#pragma unroll
+                            for (int nt = 0; nt < HT; ++nt) {
+                                if constexpr (C::HALF)
+                                    r[m][nt] = F::mma(a, bfr[nt], r[m][nt]);
+                                else
+                                    part[m][nt] = F::mma(a, bfr[nt], part[m][nt]);
+                            }
+                        }
+                    }
+                    if constexpr (!C::HALF) {
+#pragma unroll
+                        for (int m = 0; m < MT; ++m)
+#pragma unroll
+                            for (int nt = 0; nt < HT; ++nt) r[m][nt] += part[m][nt];
+                    }
+                    if (ch == NCH - 1) {
+                        const float *bo = reinterpret_cast<const float *>(sl + C::G2_FR * C::FRAG);
+#pragma unroll
+                        for (int m = 0; m < MT; ++m)
+#pragma unroll
+                            for (int q = 0; q < 16; ++q) {
+                                const float bv = bo[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+#pragma unroll
+                                for (int nt = 0; nt < HT; ++nt) r[m][nt][q] += bv;
+                            }
+                    }
+                }
+                advance();
             }
-            // output-projection bias
-            const float *bo = P.bout + (size_t)l * D;
-#pragma unroll
-            for (int m = 0; m < MT; ++m)
-#pragma unroll
-                for (int q = 0; q < 16; ++q) {
-                    const float bv = bo[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
-#pragma unroll
-                    for (int nt = 0; nt < HT; ++nt) r[m][nt][q] += bv;
-                }
         }
 
-        // ---- mean pool over each track's hits, 32 channels at a time
-#pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            wave_lds_sync();
-#pragma unroll
-            for (int nt = 0; nt < HT; ++nt) {
-                const int th = slot_to_hit<SP>(32 * nt + cc);
-#pragma unroll
-                for (int q = 0; q < 16; ++q)
-                    stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
-            }
-            wave_lds_sync();
-            for (int j = hh; j < k; j += 2) {
-                const int s0 = t_start[j], len = t_len[j];
-                float sum = 0.f;
-                for (int u = 0; u < len; ++u) sum += stage[(s0 + u) * C::STS + cc];
-                pooled[j * C::PLS + 32 * m + cc] = sum / (float)len;
-            }
-        }
-        wave_lds_sync();
-
-        // ---- head layer 1: hidden = SiLU(W1 p + b1), tracks on rows (rows past
-        // the tile's tracks are never stored; their loads repeat the last row)
-        const int prow = cc < kMaxTracksPerTile ? cc : kMaxTracksPerTile - 1;
+        // ---- head, transposed: hid^T = W1 p^T (hidden units on rows, tracks on
+        // columns), pooled 32 channels at a time through wave-private LDS
         f32x16 hid[MT];
 #pragma unroll
         for (int m = 0; m < MT; ++m)
 #pragma unroll
             for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
+        const int prow = cc < MAXTR ? cc : MAXTR - 1;  // columns past the tile's tracks repeat the last
+        for (int j = 0; j < C::NH1; ++j) {
+            if (work) {
+                const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
-        for (int ks = 0; ks < KS1; ++ks) {
-            float v[8];
+                for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
+                    const int m = j * (C::KSPS / KPB) + bl;  // channel block being pooled
+                    wave_lds_sync();
 #pragma unroll
-            for (int u = 0; u < KL; ++u) v[u] = pooled[prow * C::PLS + ks * K + hh * KL + u];
-            FT a_hi, a_lo;
-            split_operand<F>(v, a_hi, a_lo);
-            const FT *w1 = reinterpret_cast<const FT *>(P.w1);
+                    for (int nt = 0; nt < HT; ++nt) {
+                        const int th = slot_to_hit<SP>(32 * nt + cc);
 #pragma unroll
-            for (int m = 0; m < MT; ++m) {
-                const FT b = w1[((size_t)m * KS1 + ks) * 64 + lane];
-                hid[m] = F::mma(a_hi, b, hid[m]);
-                if constexpr (C::HALF) hid[m] = F::mma(a_lo, b, hid[m]);
+                        for (int q = 0; q < 16; ++q)
+                            stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
+                    }
+                    wave_lds_sync();
+                    for (int tr = hh; tr < k; tr += 2) {
+                        const int s0 = t_start[tr], len = t_len[tr];
+                        float sum = 0.f;
+                        for (int u = 0; u < len; ++u) sum += stage[(s0 + u) * C::STS + cc];
+                        pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
+                    }
+                    wave_lds_sync();
+#pragma unroll
+                    for (int kb = 0; kb < KPB; ++kb) {
+                        float v[8];
+#pragma unroll
+                        for (int u = 0; u < KL; ++u) v[u] = pblk[prow * C::STS + kb * K + hh * KL + u];
+                        FT b_hi, b_lo;
+                        split_operand<F>(v, b_hi, b_lo);
+#pragma unroll
+                        for (int mu = 0; mu < MT; ++mu) {
+                            const FT a = w1[((bl * KPB + kb) * MT + mu) * 64 + lane];
+                            hid[mu] = F::mma(a, b_hi, hid[mu]);
+                            if constexpr (C::HALF) hid[mu] = F::mma(a, b_lo, hid[mu]);
+                        }
+                    }
+                }
+                if (j == C::NH1 - 1) {
+                    // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
+                    const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
+#pragma unroll
+                    for (int mu = 0; mu < MT; ++mu)
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) {
+                            const float v = hid[mu][q] + b1[32 * mu + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                            float sv;  // SiLU(v) = v / (1 + exp(-v))
+                            if constexpr (C::HALF)
+                                sv = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
+                                                                      __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
+                            else
+                                sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
+                            hid[mu][q] = sv;
+                        }
+                }
             }
+            advance();
         }
-        wave_lds_sync();
+        // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
+        // operand, output row q of column cc is output q of track cc
+        if (work) {
+            const FT *w2 = reinterpret_cast<const FT *>(slot());
+            const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
+            f32x16 o;
 #pragma unroll
-        for (int m = 0; m < MT; ++m) {
-            const float bv = P.b1[32 * m + cc];
+            for (int q = 0; q < 16; ++q) o[q] = 0.f;
 #pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                const float v = hid[m][q] + bv;
-                const int row = 8 * (q >> 2) + 4 * hh + (q & 3);
-                float sv;  // SiLU(v) = v / (1 + exp(-v))
-                if constexpr (C::HALF)
-                    sv = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(__builtin_amdgcn_fmed3f(
-                                                          -v * kLog2e, -kGateClamp, kGateClamp)));
-                else
-                    sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
-                if (row < kMaxTracksPerTile) pooled[row * C::PLS + 32 * m + cc] = sv;
+            for (int ks = 0; ks < KS1; ++ks) {
+                float v[8];
+#pragma unroll
+                for (int u = 0; u < KL; ++u) v[u] = hid[ks / RPK][(ks % RPK) * KL + u];
+                FT b_hi, b_lo;
+                split_operand<F>(v, b_hi, b_lo);
+                const FT a = w2[ks * 64 + lane];
+                o = F::mma(a, b_hi, o);
+                if constexpr (C::HALF) o = F::mma(a, b_lo, o);
             }
-        }
-        wave_lds_sync();
-        // ---- head layer 2: five outputs per track (columns >= 5 of W2 are zero)
-        f32x16 o;
-#pragma unroll
-        for (int q = 0; q < 16; ++q) o[q] = 0.f;
-#pragma unroll
-        for (int ks = 0; ks < KS1; ++ks) {
-            float v[8];
-#pragma unroll
-            for (int u = 0; u < KL; ++u) v[u] = pooled[prow * C::PLS + ks * K + hh * KL + u];
-            FT a_hi, a_lo;
-            split_operand<F>(v, a_hi, a_lo);
-            const FT b = reinterpret_cast<const FT *>(P.w2)[ks * 64 + lane];
-            o = F::mma(a_hi, b, o);
-            if constexpr (C::HALF) o = F::mma(a_lo, b, o);
-        }
-        if (cc < 5) {
-            const float bv = P.b2[cc];
-#pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                const int row = 8 * (q >> 2) + 4 * hh + (q & 3);
-                if (row < k) out[(size_t)(t + row) * 5 + cc] = o[q] + bv;
+            if (cc < k) {
+                float *op = out + (size_t)(t + cc) * 5;
+                if (hh == 0) {
+                    op[0] = o[0] + b2[0];
+                    op[1] = o[1] + b2[1];
+                    op[2] = o[2] + b2[2];
+                    op[3] = o[3] + b2[3];
+                } else {
+                    op[4] = o[0] + b2[4];
+                }
             }
+            t += k;
         }
-        t += k;
+        advance();
     }
     if (errbits && lane == 0) atomicOr(err, errbits);
 }
@@ -601,36 +696,59 @@ uint16_t to_bf16(double v) {
     return uint16_t(u >> 16);
 }
 
-// Host-side packer of weight arrays in the kernel's operand type.
-struct Packer {
+// Writer of one weight stage: operand elements in the kernel's operand type,
+// biases in fp32.
+struct StageWriter {
     int op;
-    std::vector<unsigned char> bytes;
-    size_t begin() {  // 256-byte aligned start of a new array
-        size_t o = (bytes.size() + 255) & ~size_t(255);
-        bytes.resize(o);
-        return o;
-    }
-    void push(double v) {  // one matrix-core operand element
-        size_t o = bytes.size();
+    unsigned char *p;
+    size_t o = 0;
+    void elem(double v) {
         if (op == OP_BF16) {
             uint16_t b = to_bf16(v);
-            bytes.resize(o + 2);
-            std::memcpy(&bytes[o], &b, 2);
+            std::memcpy(p + o, &b, 2);
+            o += 2;
         } else if (op == OP_F16) {
             _Float16 h = (_Float16)(float)v;
-            bytes.resize(o + 2);
-            std::memcpy(&bytes[o], &h, 2);
+            std::memcpy(p + o, &h, 2);
+            o += 2;
         } else {
-            push_f32(v);
+            f32(v);
         }
     }
-    void push_f32(double v) {
-        size_t o = bytes.size();
-        bytes.resize(o + 4);
+    void f32(double v) {
         float f = (float)v;
-        std::memcpy(&bytes[o], &f, 4);
+        std::memcpy(p + o, &f, 4);
+        o += 4;
     }
 };
+
+// Stage geometry of one instance, for the host.
+struct Geom {
+    int stage, ksps, nh1;
+};
+template <int D, int OP, int HT>
+Geom geom() {
+    using C = KCfg<D, OP, HT>;
+    return {C::STAGE, C::KSPS, C::NH1};
+}
+template <int D, int OP>
+Geom geom_ht(int ht) {
+    if constexpr (D <= 128) {
+        if (ht == 2) return geom<D, OP, 2>();
+    }
+    return geom<D, OP, 1>();
+}
+template <int OP>
+Geom geom_d(int D, int ht) {
+    switch (D) {
+        case 32: return geom_ht<32, OP>(ht);
+        case 64: return geom_ht<64, OP>(ht);
+        case 128: return geom_ht<128, OP>(ht);
+        default:
+            if constexpr (OP != OP_F32) return geom_ht<256, OP>(ht);
+            return geom_ht<128, OP>(ht);  // unreachable: fp32 d = 256 is refused
+    }
+}
 
 }  // namespace
 
@@ -658,13 +776,17 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     if (L < 0 || D <= 0) return TF_EINVAL;
     if (!(D == 32 || D == 64 || D == 128 || D == 256) || L > 64) return TF_EUNSUPPORTED;
     if (n_floats != tf_blob_size(L, D)) return TF_EINVAL;
+    const int op = cfg->dtype == TF_BF16 ? OP_BF16 : cfg->dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32;
+    const bool half = op != OP_F32;
+    if (!half && D > 128) return TF_EUNSUPPORTED;  // fp32 stages of d = 256 do not fit in LDS
     const int supported = D <= 128 ? 64 : 32;
     const int limit = cfg->max_hits == 0 ? supported : cfg->max_hits;
     if (limit > supported) return TF_EUNSUPPORTED;
-    const int op = cfg->dtype == TF_BF16 ? OP_BF16 : cfg->dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32;
-    const bool half = op != OP_F32;
+    const int ht = limit <= 32 ? 1 : 2;
+    const Geom G = op == OP_BF16 ? geom_d<OP_BF16>(D, ht) : op == OP_F16 ? geom_d<OP_F16>(D, ht) : geom_d<OP_F32>(D, ht);
     const int K = half ? 16 : 2, KL = K / 2, KS1 = D / K, KS2 = 64 / K, RPK = 16 / KL;
     const int MT = D / 32, NCH = D / 32;
+    const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
 
     // blob views
     const size_t dd = (size_t)D;
@@ -678,25 +800,34 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const float *W1 = blob + 4 * dd + (size_t)L * lstride;
     const float *b1 = W1 + dd * dd, *W2 = b1 + dd, *b2 = W2 + 5 * dd;
 
-    Packer pk{op, {}};
+    const int n_stages = 2 * L * NCH + G.nh1 + 1;
+    const size_t emb_bytes = (size_t)D * 16;
+    const size_t emb_off = 0, st_off = (emb_bytes + 255) & ~size_t(255);
+    const size_t err_off = st_off + (size_t)n_stages * G.stage;
+    const size_t total = err_off + 256;
+    std::vector<unsigned char> hb(total, 0);
+
     // embedding with u = (x - lo) / span folded in: r = (W/span) x + (b - W lo / span)
-    const size_t o_emb = pk.begin();
-    const double lo[3] = {-1000.0, -1000.0, -3000.0}, span[3] = {2000.0, 2000.0, 6000.0};
-    for (int c = 0; c < D; ++c) {
-        double b = eb[c];
-        for (int k = 0; k < 3; ++k) {
-            pk.push_f32(eW[c * 3 + k] / span[k]);
-            b -= eW[c * 3 + k] * lo[k] / span[k];
+    {
+        StageWriter w{OP_F32, hb.data() + emb_off};
+        const double lo[3] = {-1000.0, -1000.0, -3000.0}, span[3] = {2000.0, 2000.0, 6000.0};
+        for (int c = 0; c < D; ++c) {
+            double b = eb[c];
+            for (int k = 0; k < 3; ++k) {
+                w.f32(eW[c * 3 + k] / span[k]);
+                b -= eW[c * 3 + k] * lo[k] / span[k];
+            }
+            w.f32(b);
         }
-        pk.push_f32(b);
     }
-    // input projection B fragments: lane (g, c) value u of k-step ks holds
-    // W[out 32 ch + c][in 32 m + 8 i + 4 g + j] * gain[in], with
-    // (m, 4 i + j) = (ks / RPK, (ks % RPK) * KL + u).
-    const size_t o_win = pk.begin();
+    int s = 0;
     for (int l = 0; l < L; ++l) {
-        const float *W = inW_of(l), *g = g_of(l);
-        for (int ch = 0; ch < NCH; ++ch)
+        const float *Wi = inW_of(l), *g = g_of(l), *bi = inb_of(l), *Wo = outW_of(l), *bo = outb_of(l);
+        for (int ch = 0; ch < NCH; ++ch) {
+            // input projection B fragments: lane (g, c) value u of k-step ks holds
+            // W[out 32 ch + c][in 32 m + 8 i + 4 g + j] * gain[in], with
+            // (m, 4 i + j) = (ks / RPK, (ks % RPK) * KL + u); then bx[32], bg[32]
+            StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
             for (int part = 0; part < 2; ++part)
                 for (int ks = 0; ks < KS1; ++ks)
                     for (int lane = 0; lane < 64; ++lane)
@@ -705,22 +836,14 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
                             const int reg = (ks % RPK) * KL + u, m = ks / RPK;
                             const int in = 32 * m + 8 * (reg / 4) + 4 * gg + (reg % 4);
                             const int row = part * D + 32 * ch + c;
-                            pk.push((double)W[(size_t)row * D + in] * g[in]);
+                            w.elem((double)Wi[(size_t)row * D + in] * g[in]);
                         }
-    }
-    const size_t o_bin = pk.begin();
-    for (int l = 0; l < L; ++l) {
-        const float *b = inb_of(l);
-        for (int o = 0; o < D; ++o) pk.push_f32(b[o]);
-        const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
-        for (int o = 0; o < D; ++o) pk.push_f32(gs * b[D + o]);
-    }
-    // output projection A fragments: lane (g, c) value u of k-step kk holds
-    // W[out 32 m + c][column of [f; b] channel q = kk K + g KL + u of chunk ch]
-    const size_t o_wout = pk.begin();
-    for (int l = 0; l < L; ++l) {
-        const float *W = outW_of(l);
-        for (int ch = 0; ch < NCH; ++ch)
+            for (int c = 0; c < 32; ++c) w.f32(bi[32 * ch + c]);
+            for (int c = 0; c < 32; ++c) w.f32(gs * bi[D + 32 * ch + c]);
+            // output projection A fragments: lane (g, c) value u of k-step kk of
+            // block m holds W[out 32 m + c][column of [f; b] channel
+            // q = kk K + g KL + u of the chunk]; then bout[D]
+            StageWriter w2{op, hb.data() + st_off + (size_t)s++ * G.stage};
             for (int m = 0; m < MT; ++m)
                 for (int kk = 0; kk < KS2; ++kk)
                     for (int lane = 0; lane < 64; ++lane)
@@ -728,73 +851,69 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
                             const int gg = lane / 32, c = lane % 32;
                             const int q = kk * K + gg * KL + u;
                             const int col = q < 32 ? 32 * ch + q : D + 32 * ch + (q - 32);
-                            pk.push(W[(size_t)(32 * m + c) * 2 * D + col]);
+                            w2.elem(Wo[(size_t)(32 * m + c) * 2 * D + col]);
                         }
+            for (int c = 0; c < D; ++c) w2.f32(bo[c]);
+        }
     }
-    const size_t o_bout = pk.begin();
-    for (int l = 0; l < L; ++l)
-        for (int o = 0; o < D; ++o) pk.push_f32(outb_of(l)[o]);
-    // head
-    const size_t o_w1 = pk.begin();
-    for (int m = 0; m < MT; ++m)
+    // head layer 1 A fragments, KSPS k-steps per stage: lane (g, c) value u of
+    // k-step ks, unit tile mu holds W1[unit 32 mu + c][channel ks K + g KL + u];
+    // then b1[D]
+    for (int j = 0; j < G.nh1; ++j) {
+        StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
+        for (int kl = 0; kl < G.ksps; ++kl)
+            for (int mu = 0; mu < MT; ++mu)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int u = 0; u < KL; ++u) {
+                        const int ks = j * G.ksps + kl;
+                        w.elem(W1[(size_t)(32 * mu + lane % 32) * D + ks * K + (lane / 32) * KL + u]);
+                    }
+        for (int c = 0; c < D; ++c) w.f32(b1[c]);
+    }
+    // head layer 2 A fragments: lane (g, c) value u of k-step ks holds
+    // W2[output c][unit 32 m + 8 i + 4 g + j] (zero for c >= 5), the same unit
+    // order as the hidden accumulators; then b2[5]
+    {
+        StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
         for (int ks = 0; ks < KS1; ++ks)
             for (int lane = 0; lane < 64; ++lane)
-                for (int u = 0; u < KL; ++u)
-                    pk.push(W1[(size_t)(32 * m + lane % 32) * D + ks * K + (lane / 32) * KL + u]);
-    const size_t o_b1 = pk.begin();
-    for (int o = 0; o < D; ++o) pk.push_f32(b1[o]);
-    const size_t o_w2 = pk.begin();
-    for (int ks = 0; ks < KS1; ++ks)
-        for (int lane = 0; lane < 64; ++lane)
-            for (int u = 0; u < KL; ++u) {
-                const int c = lane % 32;
-                pk.push(c < 5 ? (double)W2[(size_t)c * D + ks * K + (lane / 32) * KL + u] : 0.0);
-            }
-    const size_t o_b2 = pk.begin();
-    for (int o = 0; o < 5; ++o) pk.push_f32(b2[o]);
-    const size_t o_err = pk.begin();
-    pk.push_f32(0.0);
-    const size_t total = pk.begin();
-    (void)RPK;
+                for (int u = 0; u < KL; ++u) {
+                    const int gg = lane / 32, c = lane % 32;
+                    const int reg = (ks % RPK) * KL + u, m = ks / RPK;
+                    const int unit = 32 * m + 8 * (reg / 4) + 4 * gg + (reg % 4);
+                    w.elem(c < 5 ? (double)W2[(size_t)c * D + unit] : 0.0);
+                }
+        for (int c = 0; c < 5; ++c) w.f32(b2[c]);
+    }
 
-    tf_weights *w = new (std::nothrow) tf_weights();
-    if (!w) return TF_ENOMEM;
-    if (hipGetDevice(&w->device) != hipSuccess ||
-        hipDeviceGetAttribute(&w->cu_count, hipDeviceAttributeMultiprocessorCount, w->device) != hipSuccess) {
-        delete w;
+    tf_weights *wt = new (std::nothrow) tf_weights();
+    if (!wt) return TF_ENOMEM;
+    if (hipGetDevice(&wt->device) != hipSuccess ||
+        hipDeviceGetAttribute(&wt->cu_count, hipDeviceAttributeMultiprocessorCount, wt->device) != hipSuccess) {
+        delete wt;
         return TF_EHIP;
     }
-    if (hipMalloc(&w->dmem, total) != hipSuccess) {
-        delete w;
+    if (hipMalloc(&wt->dmem, total) != hipSuccess) {
+        delete wt;
         return TF_ENOMEM;
     }
-    std::vector<unsigned char> &hb = pk.bytes;
-    std::memset(&hb[o_err], 0, 4);
-    if (hipMemcpy(w->dmem, hb.data(), total, hipMemcpyHostToDevice) != hipSuccess) {
-        (void)hipFree(w->dmem);
-        delete w;
+    if (hipMemcpy(wt->dmem, hb.data(), total, hipMemcpyHostToDevice) != hipSuccess) {
+        (void)hipFree(wt->dmem);
+        delete wt;
         return TF_EHIP;
     }
-    char *b = static_cast<char *>(w->dmem);
-    w->n_layers = L;
-    w->d = D;
-    w->dtype = cfg->dtype;
-    // tile shape: one 32-hit tile per wave (two waves per SIMD in the 16-bit
-    // modes) when tracks have at most 32 hits, two 32-hit tiles otherwise
-    w->max_hits = limit <= 32 ? 32 : 64;
-    w->err = reinterpret_cast<int *>(b + o_err);
-    DevParams &P = w->params;
-    P.emb = reinterpret_cast<const float4 *>(b + o_emb);
-    P.win = b + o_win;
-    P.bin = reinterpret_cast<const float *>(b + o_bin);
-    P.wout = b + o_wout;
-    P.bout = reinterpret_cast<const float *>(b + o_bout);
-    P.w1 = b + o_w1;
-    P.b1 = reinterpret_cast<const float *>(b + o_b1);
-    P.w2 = b + o_w2;
-    P.b2 = reinterpret_cast<const float *>(b + o_b2);
-    P.n_layers = L;
-    *out = w;
+    char *b = static_cast<char *>(wt->dmem);
+    wt->n_layers = L;
+    wt->d = D;
+    wt->dtype = cfg->dtype;
+    wt->max_hits = 32 * ht;
+    wt->err = reinterpret_cast<int *>(b + err_off);
+    wt->params.emb = reinterpret_cast<const float4 *>(b + emb_off);
+    wt->params.stages = reinterpret_cast<const unsigned char *>(b + st_off);
+    wt->params.n_layers = L;
+    wt->params.n_stages = n_stages;
+    (void)KS2;
+    *out = wt;
     return TF_OK;
 }
 
@@ -812,11 +931,11 @@ template <int D, int OP, int HT>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                   const tf_weights *w, float *out, hipStream_t stream) {
     using C = KCfg<D, OP, HT>;
-    // at least 8 tracks per wave; at most OCC workgroups of resident waves per
-    // compute unit, so that every wave's track group is scheduled at once
+    // one workgroup per compute unit (the LDS ring and the register file are
+    // sized for it), at least 8 tracks per wave
     long long waves = (n_tracks + 7) / 8;
     long long blocks = (waves + C::WAVES - 1) / C::WAVES;
-    const long long cap = (long long)w->cu_count * C::OCC * (4 / C::WAVES > 0 ? 4 / C::WAVES : 1);
+    const long long cap = (long long)w->cu_count;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
@@ -839,7 +958,9 @@ hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, i
     switch (w->dtype) {
         case TF_BF16: return launch_ht<D, OP_BF16>(hits, n_hits, offsets, n_tracks, w, out, stream);
         case TF_BF16_F16ACT: return launch_ht<D, OP_F16>(hits, n_hits, offsets, n_tracks, w, out, stream);
-        default: return launch_ht<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        default:
+            if constexpr (D <= 128) return launch_ht<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            return hipErrorNotSupported;
     }
 }
 }  // namespace
