@@ -116,10 +116,15 @@ struct KCfg {
     static constexpr int FB_BYTES = CAP * FBS * EB;
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
     static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 2 * MAXTR * 4;
-    // workgroup LDS: embedding table, two stage slots, wave regions
+    // workgroup LDS: embedding table, a ring of stage slots, wave regions.  The
+    // ring is as deep as LDS allows (at most 4 slots): stages s + 1 ..
+    // s + NSLOT - 1 are resident or in flight while stage s is computed.
     static constexpr int EMB_BYTES = D * 16;
     static constexpr int SLOT0 = EMB_BYTES;
-    static constexpr int WAVE0 = SLOT0 + 2 * STAGE;
+    static constexpr int NSLOT_FIT = (kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES) / STAGE;
+    static constexpr int NSLOT = NSLOT_FIT > 4 ? 4 : NSLOT_FIT;
+    static_assert(NSLOT >= 2, "stage ring");
+    static constexpr int WAVE0 = SLOT0 + NSLOT * STAGE;
     static constexpr int LDS_BYTES = WAVE0 + WAVES * WAVE_BYTES;
     static_assert(LDS_BYTES <= kLdsBytesMax, "LDS budget");
     static_assert(D % 32 == 0, "d must be a multiple of 32");
@@ -227,30 +232,49 @@ __device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int
     }
 }
 
-// Double-buffered copy of the weight stages into LDS.  Each wave copies its
-// share (1 KiB pieces w, w + WAVES, ...) of the next stage into registers,
-// stores them to the free slot after the current stage's compute, and the
-// workgroup barrier publishes the slot.
+// Copy of one weight stage from global memory straight into an LDS slot:
+// global_load_lds_dwordx4 moves 16 bytes per lane, 1 KiB per wave
+// instruction, into LDS at M0 + 16 * lane.  Each wave copies the pieces
+// w, w + WAVES, ...; waves with fewer pieces repeat the last one (same bytes to
+// the same place), so every wave issues exactly LPW loads per stage and can
+// wait for an older stage with a constant vmcnt.  The instruction is written
+// out because the compiler, which cannot tell the ring slots apart, would
+// otherwise wait for every such load before each LDS access; the kernel keeps
+// the count itself (wait_vmcnt).  The kernel has no other use of M0.
+__device__ __forceinline__ void lds_dma16(const void *gsrc, const char *ldst) {
+    const unsigned a = (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char *)ldst;
+    // one wait state between the M0 write and its use by the load
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(a)), "v"(gsrc)
+                 : "memory", "m0");
+}
+
 template <class C>
-struct StageCopier {
-    u32x4 buf[C::LPW];
-    __device__ __forceinline__ void load(const unsigned char *stages, int n_stages, int s, int wid, int lane) {
-        const unsigned char *src = stages + (size_t)(s % n_stages) * C::STAGE;
+__device__ __forceinline__ void copy_stage(const unsigned char *stages, int s, char *slot, int wid, int lane) {
+    const unsigned char *src = stages + (size_t)s * C::STAGE + lane * 16;
 #pragma unroll
-        for (int i = 0; i < C::LPW; ++i) {
-            const int piece = wid + i * C::WAVES;
-            if (piece < C::COPIES)
-                buf[i] = *reinterpret_cast<const u32x4 *>(src + piece * kCopyBytes + lane * 16);
-        }
+    for (int i = 0; i < C::LPW; ++i) {
+        int piece = wid + i * C::WAVES;
+        piece = piece < C::COPIES ? piece : C::COPIES - 1;
+        lds_dma16(src + piece * kCopyBytes, slot + piece * kCopyBytes);
     }
-    __device__ __forceinline__ void store(char *slot, int wid, int lane) {
-#pragma unroll
-        for (int i = 0; i < C::LPW; ++i) {
-            const int piece = wid + i * C::WAVES;
-            if (piece < C::COPIES) *reinterpret_cast<u32x4 *>(slot + piece * kCopyBytes + lane * 16) = buf[i];
-        }
-    }
-};
+}
+
+// Workgroup barrier that orders LDS only (the kernel shares nothing through
+// global memory within a workgroup).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
 
 template <int D, int OP, int HT_>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
@@ -278,22 +302,32 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     const int hh = lane >> 5;  // lane half
     const int cc = lane & 31;  // lane column
 
-    // embedding table to LDS, first two weight stages in flight
+    // embedding table to LDS; stages 0 .. NSLOT - 2 in flight
     for (int i = threadIdx.x; i < D; i += 64 * C::WAVES) reinterpret_cast<float4 *>(smem)[i] = P.emb[i];
-    StageCopier<C> cp;
-    cp.load(P.stages, P.n_stages, 0, wid, lane);
-    cp.store(smem + C::SLOT0, wid, lane);
-    cp.load(P.stages, P.n_stages, 1, wid, lane);
-    __syncthreads();
-    int sidx = 0;  // index of the stage being consumed (counts across tiles)
-    // after the compute of stage sidx: publish stage sidx+1, start loading sidx+2
-    auto advance = [&]() {
-        cp.store(smem + C::SLOT0 + ((sidx + 1) & 1) * C::STAGE, wid, lane);
-        __syncthreads();
-        cp.load(P.stages, P.n_stages, sidx + 2, wid, lane);
-        ++sidx;
+    const int S = P.n_stages;
+    auto slot_ptr = [&](int q) -> char * { return smem + C::SLOT0 + (q % C::NSLOT) * C::STAGE; };
+#pragma unroll
+    for (int q = 0; q < C::NSLOT - 1; ++q) copy_stage<C>(P.stages, q % S, slot_ptr(q), wid, lane);
+
+    // Stage q (counted across tiles; a tile iteration takes S stages) lives in
+    // slot q % NSLOT.  At the end of stage q every wave waits for its share of
+    // stage q + 1 (the loads of a wave complete in order, so this is a count of
+    // the younger stage loads still allowed in flight), the barrier publishes
+    // stage q + 1 and retires stage q, and stage q + NSLOT goes into the slot
+    // of stage q.  The last stage of a tile waits for everything (its output
+    // stores may complete out of order with the loads) and leaves the next
+    // load to the start of the next tile, after that tile's own loads.
+    int q = 0;
+    auto advance = [&](bool last) {
+        if (last)
+            wait_vmcnt<0>();
+        else
+            wait_vmcnt<(C::NSLOT - 2) * C::LPW>();
+        lds_barrier();
+        if (!last) copy_stage<C>(P.stages, (q + C::NSLOT) % S, slot_ptr(q + C::NSLOT), wid, lane);
+        ++q;
     };
-    auto slot = [&]() -> const char * { return smem + C::SLOT0 + (sidx & 1) * C::STAGE; };
+    auto slot = [&]() -> const char * { return slot_ptr(q); };
 
     // Contiguous group of tracks for this wave, balanced by track count.
     const long long gw = (long long)blockIdx.x * C::WAVES + wid;
@@ -339,7 +373,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             break;
         }
         const bool work = t < g_end;
+        wait_vmcnt<0>();                     // stages q .. q + NSLOT - 2 are in LDS
         if (!__syncthreads_or(work)) break;  // every wave of the workgroup is done
+        copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_ptr(q + C::NSLOT - 1), wid, lane);
 
         // ---- tile metadata: track starts and lengths, start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
@@ -522,7 +558,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         store_fb<C, FE>(ws, Bs, 32, hh, cc);
                     }
                 }
-                advance();
+                advance(false);
 
                 // ---- stage: output projection of this chunk, K split over chunks.  The
                 // 16-bit modes accumulate straight into the residual registers; the
@@ -577,7 +613,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             }
                     }
                 }
-                advance();
+                advance(false);
             }
         }
 
@@ -644,7 +680,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         }
                 }
             }
-            advance();
+            advance(false);
         }
         // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
         // operand, output row q of column cc is output q of track cc
@@ -678,7 +714,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             }
             t += k;
         }
-        advance();
+        advance(true);
     }
     if (errbits && lane == 0) atomicOr(err, errbits);
 }
