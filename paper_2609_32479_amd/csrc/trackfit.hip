@@ -68,8 +68,9 @@ enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
 
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kRmsEps = 1e-6f;
-// |gate pre-activation| is clamped to 80 (scaled by log2 e in the 16-bit
-// modes) so that exp stays finite; the change in the gate is below exp(-80).
+// The fp32 gate clamps |pre-activation| to 80 and the 16-bit head clamps the
+// SiLU exponent to 80 log2(e), so that exp stays finite; the change in the
+// result is below exp(-80).
 constexpr float kGateClamp = 80.0f * kLog2e;
 constexpr int kLdsBytesMax = 160 * 1024;
 constexpr int kCopyBytes = 1024;  // one wave-wide 16-byte-per-lane copy
@@ -182,9 +183,38 @@ __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirs
 // Lane mask (wave-uniform, 64 bits) of the lanes whose stream has bit p set:
 // lanes 0-31 follow b0, lanes 32-63 follow b1.
 __device__ __forceinline__ unsigned long long half_mask(unsigned b0, unsigned b1, int p) {
-    const unsigned long long lo = ((b0 >> p) & 1u) ? 0x00000000ffffffffull : 0ull;
-    const unsigned long long hi = ((b1 >> p) & 1u) ? 0xffffffff00000000ull : 0ull;
-    return lo | hi;
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 m = {(unsigned)((int)(b0 << (31 - p)) >> 31), (unsigned)((int)(b1 << (31 - p)) >> 31)};
+    return __builtin_bit_cast(unsigned long long, m);
+}
+
+// Redo of the forward scan from position P on, up to (not including) position
+// `end` (wave-uniform), from state fr; nested so that it stops at `end`
+// without a loop.  The empty asm keeps each step a branch (not a select).
+template <int P, int SP>
+__device__ __forceinline__ void rerun_fwd(float &fr, float *Fs, const float *CF, const float *AX, int end) {
+    if constexpr (P < SP) {
+        if (P < end) {
+            asm volatile("");
+            fr = fmaf(CF[P], fr, AX[P]);
+            Fs[P] = fr;
+            rerun_fwd<P + 1, SP>(fr, Fs, CF, AX, end);
+        }
+    }
+}
+
+// Redo of the reverse scan from position P down, while the position is above
+// `last` (wave-uniform).
+template <int P>
+__device__ __forceinline__ void rerun_bwd(float &br, float *Bs, const float *CF, const float *AX, int last) {
+    if constexpr (P >= 0) {
+        if (P > last) {
+            asm volatile("");
+            br = fmaf(CF[P], br, AX[P]);
+            Bs[P] = br;
+            rerun_bwd<P - 1>(br, Bs, CF, AX, last);
+        }
+    }
 }
 
 // v in lanes outside m, 0 in lanes of m: one v_cndmask with the mask in SGPRs.
@@ -222,13 +252,24 @@ __device__ __forceinline__ void split_operand(const float *v, typename F::T &hi,
 }
 
 // Scan outputs of one lane (stream hh, channel cc of the chunk) to the [f; b]
-// buffer: row = hit slot of position p, column = col0 + cc.
+// buffer: row = hit slot of position p, column = col0 + cc.  Positions p and
+// p + 1 (p even) sit in slots s and s + 1; 16-bit values are converted in pairs.
 template <class C, class E>
 __device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int hh, int cc) {
+    E *fb = reinterpret_cast<E *>(ws) + col0 + cc;
 #pragma unroll
-    for (int p = 0; p < C::SP; ++p) {
+    for (int p = 0; p < C::SP; p += 2) {
         const int s = 32 * (p >> 4) + 8 * ((p >> 2) & 3) + 4 * hh + (p & 3);
-        reinterpret_cast<E *>(ws)[s * C::FBS + col0 + cc] = (E)v[p];
+        if constexpr (sizeof(E) == 2) {
+            typedef E e2 __attribute__((ext_vector_type(2)));
+            typedef float f2 __attribute__((ext_vector_type(2)));
+            const e2 pr = __builtin_convertvector((f2){v[p], v[p + 1]}, e2);
+            fb[s * C::FBS] = pr.x;
+            fb[(s + 1) * C::FBS] = pr.y;
+        } else {
+            fb[s * C::FBS] = v[p];
+            fb[(s + 1) * C::FBS] = v[p + 1];
+        }
     }
 }
 
@@ -241,23 +282,23 @@ __device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int
 // out because the compiler, which cannot tell the ring slots apart, would
 // otherwise wait for every such load before each LDS access; the kernel keeps
 // the count itself (wait_vmcnt).  The kernel has no other use of M0.
-__device__ __forceinline__ void lds_dma16(const void *gsrc, const char *ldst) {
-    const unsigned a = (unsigned)(uintptr_t)(__attribute__((address_space(3))) const char *)ldst;
+__device__ __forceinline__ void lds_dma16(const void *gsrc, unsigned lds_addr) {
     // one wait state between the M0 write and its use by the load
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
                  :
-                 : "s"(__builtin_amdgcn_readfirstlane(a)), "v"(gsrc)
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gsrc)
                  : "memory", "m0");
 }
 
+// slot_lds: LDS byte address of the slot.
 template <class C>
-__device__ __forceinline__ void copy_stage(const unsigned char *stages, int s, char *slot, int wid, int lane) {
+__device__ __forceinline__ void copy_stage(const unsigned char *stages, int s, unsigned slot_lds, int wid, int lane) {
     const unsigned char *src = stages + (size_t)s * C::STAGE + lane * 16;
 #pragma unroll
     for (int i = 0; i < C::LPW; ++i) {
         int piece = wid + i * C::WAVES;
         piece = piece < C::COPIES ? piece : C::COPIES - 1;
-        lds_dma16(src + piece * kCopyBytes, slot + piece * kCopyBytes);
+        lds_dma16(src + piece * kCopyBytes, slot_lds + piece * kCopyBytes);
     }
 }
 
@@ -306,8 +347,11 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     for (int i = threadIdx.x; i < D; i += 64 * C::WAVES) reinterpret_cast<float4 *>(smem)[i] = P.emb[i];
     const int S = P.n_stages;
     auto slot_ptr = [&](int q) -> char * { return smem + C::SLOT0 + (q % C::NSLOT) * C::STAGE; };
+    // LDS byte address of the slot of stage q
+    const unsigned smem_lds = (unsigned)(uintptr_t)(__attribute__((address_space(3))) char *)smem;
+    auto slot_lds = [&](int q) -> unsigned { return smem_lds + C::SLOT0 + (q % C::NSLOT) * C::STAGE; };
 #pragma unroll
-    for (int q = 0; q < C::NSLOT - 1; ++q) copy_stage<C>(P.stages, q % S, slot_ptr(q), wid, lane);
+    for (int q = 0; q < C::NSLOT - 1; ++q) copy_stage<C>(P.stages, q % S, slot_lds(q), wid, lane);
 
     // Stage q (counted across tiles; a tile iteration takes S stages) lives in
     // slot q % NSLOT.  At the end of stage q every wave waits for its share of
@@ -324,7 +368,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         else
             wait_vmcnt<(C::NSLOT - 2) * C::LPW>();
         lds_barrier();
-        if (!last) copy_stage<C>(P.stages, (q + C::NSLOT) % S, slot_ptr(q + C::NSLOT), wid, lane);
+        if (!last) copy_stage<C>(P.stages, (q + C::NSLOT) % S, slot_lds(q + C::NSLOT), wid, lane);
         ++q;
     };
     auto slot = [&]() -> const char * { return slot_ptr(q); };
@@ -375,7 +419,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         const bool work = t < g_end;
         wait_vmcnt<0>();                     // stages q .. q + NSLOT - 2 are in LDS
         if (!__syncthreads_or(work)) break;  // every wave of the workgroup is done
-        copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_ptr(q + C::NSLOT - 1), wid, lane);
+        copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_lds(q + C::NSLOT - 1), wid, lane);
 
         // ---- tile metadata: track starts and lengths, start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
@@ -467,13 +511,16 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     const char *sl = slot();
                     const FT *wf = reinterpret_cast<const FT *>(sl);
                     const float *bias = reinterpret_cast<const float *>(sl + C::G1_FR * C::FRAG);
+                    // candidate and gate pre-activation, accumulated onto their biases
+                    const float bxv = bias[cc];
+                    const float bgv = bias[32 + cc];
                     f32x16 ax[HT], gx[HT];
 #pragma unroll
                     for (int nt = 0; nt < HT; ++nt)
 #pragma unroll
                         for (int q = 0; q < 16; ++q) {
-                            ax[nt][q] = 0.f;
-                            gx[nt][q] = 0.f;
+                            ax[nt][q] = bxv;
+                            gx[nt][q] = bgv;
                         }
 #pragma unroll
                     for (int ks = 0; ks < KS1; ++ks) {
@@ -485,78 +532,68 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
                         }
                     }
-                    const float bxv = bias[cc];
-                    const float bgv = bias[32 + cc];
+                    // gate a = sigmoid(g): the update adds a x and keeps cf = 1 - a of the state
                     float AX[HT * 16], CF[HT * 16];
 #pragma unroll
                     for (int nt = 0; nt < HT; ++nt)
 #pragma unroll
                         for (int q = 0; q < 16; ++q) {
-                            const float x = ax[nt][q] + bxv;
-                            float e, a;  // e = exp(-gate), a = sigmoid(gate) = 1 / (1 + e)
+                            const float g = gx[nt][q];
+                            float a, cf;
                             if constexpr (C::HALF) {
-                                // hardware exp2 / reciprocal; the bias holds -log2(e) * b
-                                e = __builtin_amdgcn_exp2f(
-                                    __builtin_amdgcn_fmed3f(fmaf(gx[nt][q], -kLog2e, bgv), -kGateClamp, kGateClamp));
+                                // hardware exp2 and reciprocal; exp2 of a large argument is inf
+                                // (a = 0, cf = 1) or 0 (a = 1, cf = 0)
+                                const float e = __builtin_amdgcn_exp2f(g * -kLog2e);
                                 a = __builtin_amdgcn_rcpf(1.0f + e);
+                                cf = 1.0f - a;
                             } else {
-                                // correctly rounded division and library exp for the fp32 model
-                                e = expf(-__builtin_amdgcn_fmed3f(gx[nt][q] + bgv, -80.0f, 80.0f));
+                                // library exp and correctly rounded division for the fp32 model
+                                const float e = expf(-__builtin_amdgcn_fmed3f(g, -80.0f, 80.0f));
                                 a = 1.0f / (1.0f + e);
+                                cf = e * a;
                             }
-                            AX[nt * 16 + q] = a * x;
-                            CF[nt * 16 + q] = e * a;
+                            AX[nt * 16 + q] = a * ax[nt][q];
+                            CF[nt * 16 + q] = cf;
                         }
+                    // Forward and reverse scans along this lane's stream, interleaved.  A
+                    // track start (forward) or end (reverse) drops the carried state: its
+                    // coefficient is zeroed in the lanes of that stream.  The masks are
+                    // formed where they are used (the asm hides the loop invariance that
+                    // would otherwise keep all of them in scalar registers).
+                    unsigned ms0 = sb0, ms1 = sb1, me0 = eb0, me1 = eb1;
+                    int rf_end = fs1, rb_last = le0;
+                    asm volatile("" : "+s"(ms0), "+s"(ms1), "+s"(me0), "+s"(me1), "+s"(rf_end), "+s"(rb_last));
+                    float Fs[HT * 16], Bs[HT * 16];
+                    {
+                        float f = 0.f, b = 0.f;
+#pragma unroll
+                        for (int i = 0; i < SP; ++i) {
+                            const int pb = SP - 1 - i;
+                            f = fmaf(zero_lanes(CF[i], half_mask(ms0, ms1, i)), f, AX[i]);
+                            b = fmaf(zero_lanes(CF[pb], half_mask(me0, me1, pb)), b, AX[pb]);
+                            Fs[i] = f;
+                            Bs[pb] = b;
+                        }
+                    }
+                    if (cross) {
+                        // The track straddling the two streams: stream 1 redoes its forward
+                        // scan up to its first track start from the true state at the end of
+                        // stream 0, stream 0 its reverse scan back to its last track end from
+                        // the true state at the start of stream 1, with the operations of an
+                        // unsplit scan.  One lane swap brings both states across.
+                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(Bs[0]),
+                                                                         __float_as_uint(Fs[SP - 1]), false, false);
+                        if (hh) {
+                            float fr = __uint_as_float(xs[0]);  // Fs[SP - 1] of the lane in stream 0
+                            rerun_fwd<0, SP>(fr, Fs, CF, AX, rf_end);
+                        } else {
+                            float br = __uint_as_float(xs[1]);  // Bs[0] of the lane in stream 1
+                            rerun_bwd<SP - 1>(br, Bs, CF, AX, rb_last);
+                        }
+                    }
                     wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
-                    // forward scan along this lane's stream
-                    {
-                        float Fs[HT * 16];
-                        float f = 0.f;
-#pragma unroll
-                        for (int p = 0; p < SP; ++p) {
-                            // a track start drops the carried state: f = 0 * f + a x
-                            f = fmaf(zero_lanes(CF[p], half_mask(sb0, sb1, p)), f, AX[p]);
-                            Fs[p] = f;
-                        }
-                        if (cross) {
-                            // the track straddling the two streams: redo the head of stream 1
-                            // up to its first track start from the true state at the end of
-                            // stream 0, with the same operations as an unsplit scan
-                            float fr = __shfl_xor(Fs[SP - 1], 32);
-#pragma unroll
-                            for (int p = 0; p < SP; ++p) {
-                                if (p < fs1) {
-                                    fr = fmaf(CF[p], fr, AX[p]);
-                                    if (hh) Fs[p] = fr;
-                                }
-                            }
-                        }
-                        store_fb<C, FE>(ws, Fs, 0, hh, cc);
-                    }
-                    // reverse scan
-                    {
-                        float Bs[HT * 16];
-                        float b = 0.f;
-#pragma unroll
-                        for (int p = SP - 1; p >= 0; --p) {
-                            // a track end drops the state carried from the next track
-                            b = fmaf(zero_lanes(CF[p], half_mask(eb0, eb1, p)), b, AX[p]);
-                            Bs[p] = b;
-                        }
-                        if (cross) {
-                            // and redo the tail of stream 0 back to its last track end from
-                            // the true reverse state at the start of stream 1
-                            float br = __shfl_xor(Bs[0], 32);
-#pragma unroll
-                            for (int p = SP - 1; p >= 0; --p) {
-                                if (p > le0) {
-                                    br = fmaf(CF[p], br, AX[p]);
-                                    if (!hh) Bs[p] = br;
-                                }
-                            }
-                        }
-                        store_fb<C, FE>(ws, Bs, 32, hh, cc);
-                    }
+                    store_fb<C, FE>(ws, Fs, 0, hh, cc);
+                    store_fb<C, FE>(ws, Bs, 32, hh, cc);
                 }
                 advance(false);
 
@@ -822,7 +859,6 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const Geom G = op == OP_BF16 ? geom_d<OP_BF16>(D, ht) : op == OP_F16 ? geom_d<OP_F16>(D, ht) : geom_d<OP_F32>(D, ht);
     const int K = half ? 16 : 2, KL = K / 2, KS1 = D / K, KS2 = 64 / K, RPK = 16 / KL;
     const int MT = D / 32, NCH = D / 32;
-    const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
 
     // blob views
     const size_t dd = (size_t)D;
@@ -875,7 +911,7 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
                             w.elem((double)Wi[(size_t)row * D + in] * g[in]);
                         }
             for (int c = 0; c < 32; ++c) w.f32(bi[32 * ch + c]);
-            for (int c = 0; c < 32; ++c) w.f32(gs * bi[D + 32 * ch + c]);
+            for (int c = 0; c < 32; ++c) w.f32(bi[D + 32 * ch + c]);
             // output projection A fragments: lane (g, c) value u of k-step kk of
             // block m holds W[out 32 m + c][column of [f; b] channel
             // q = kk K + g KL + u of the chunk]; then bout[D]
