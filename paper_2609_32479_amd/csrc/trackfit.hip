@@ -98,31 +98,37 @@ struct KCfg {
     static constexpr int KPB = 32 / K;           // k-steps per 32-channel block
     static constexpr int EB = HALF ? 2 : 4;      // operand element bytes
     static constexpr int FRAG = 64 * KL * EB;    // one wave-wide operand fragment
-    // weight stages (all padded to STAGE bytes)
-    static constexpr int G1_FR = 2 * KS1;        // candidate + gate fragments of a chunk
-    static constexpr int G2_FR = MT * KS2;       // output-projection fragments of a chunk
-    static constexpr int G1_BYTES = G1_FR * FRAG + 64 * 4;  // + bx[32], bg[32]
-    static constexpr int G2_BYTES = G2_FR * FRAG + D * 4;   // + bout[D]
-    static constexpr int STAGE = round_up(cmax(G1_BYTES, G2_BYTES), kCopyBytes);
-    static constexpr int KSPS_RAW = (STAGE - D * 4) / (MT * FRAG);   // head-1 k-steps per stage
-    static constexpr int KSPS = (KSPS_RAW >= KS1 ? KS1 : KSPS_RAW / KPB * KPB);
-    static constexpr int NH1 = KS1 / KSPS;       // head-1 stages
-    static constexpr int COPIES = STAGE / kCopyBytes;
     // waves per workgroup and per SIMD
     static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 8 : 4;
-    static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;  // copies per wave per stage
     // wave-private LDS: [f; b] buffer, aliased by the pooling scratch
     static constexpr int FBS = HALF ? 72 : 65;   // row stride of [f; b] (elements)
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
     static constexpr int FB_BYTES = CAP * FBS * EB;
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
     static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 2 * MAXTR * 4;
+    static constexpr int EMB_BYTES = D * 16;
+    static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES;  // for the stage ring
+    // Weight stages, all padded to STAGE bytes.  A chunk's input and output
+    // projections share one stage (one barrier per chunk) when two such stages
+    // fit in the ring; otherwise each has its own.
+    static constexpr int G1_FR = 2 * KS1;        // candidate + gate fragments of a chunk
+    static constexpr int G2_FR = MT * KS2;       // output-projection fragments of a chunk
+    static constexpr int G1_BYTES = G1_FR * FRAG + 64 * 4;  // + bx[32], bg[32]
+    static constexpr int G2_BYTES = G2_FR * FRAG + D * 4;   // + bout[D]
+    static constexpr int MERGED_STAGE = round_up(round_up(G1_BYTES, 16) + G2_BYTES, kCopyBytes);
+    static constexpr bool MERGE = RING_BYTES / MERGED_STAGE >= 2;
+    static constexpr int STAGE = MERGE ? MERGED_STAGE : round_up(cmax(G1_BYTES, G2_BYTES), kCopyBytes);
+    static constexpr int G2_OFF = MERGE ? round_up(G1_BYTES, 16) : 0;  // output projection in its stage
+    static constexpr int KSPS_RAW = (STAGE - D * 4) / (MT * FRAG);   // head-1 k-steps per stage
+    static constexpr int KSPS = (KSPS_RAW >= KS1 ? KS1 : KSPS_RAW / KPB * KPB);
+    static constexpr int NH1 = KS1 / KSPS;       // head-1 stages
+    static constexpr int COPIES = STAGE / kCopyBytes;
+    static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;  // copies per wave per stage
     // workgroup LDS: embedding table, a ring of stage slots, wave regions.  The
     // ring is as deep as LDS allows (at most 4 slots): stages s + 1 ..
     // s + NSLOT - 1 are resident or in flight while stage s is computed.
-    static constexpr int EMB_BYTES = D * 16;
     static constexpr int SLOT0 = EMB_BYTES;
-    static constexpr int NSLOT_FIT = (kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES) / STAGE;
+    static constexpr int NSLOT_FIT = RING_BYTES / STAGE;
     static constexpr int NSLOT = NSLOT_FIT > 4 ? 4 : NSLOT_FIT;
     static_assert(NSLOT >= 2, "stage ring");
     static constexpr int WAVE0 = SLOT0 + NSLOT * STAGE;
@@ -169,7 +175,7 @@ struct DevParams {
     const float4 *emb;           // [D] (w_x, w_y, w_z, b) with the min-max map folded in
     const unsigned char *stages; // n_stages x STAGE bytes, in the order the kernel walks them
     int n_layers;
-    int n_stages;                // 2 * n_layers * NCH + NH1 + 1
+    int n_stages;                // (MERGE ? 1 : 2) * n_layers * NCH + NH1 + 1
 };
 
 __device__ __forceinline__ void wave_lds_sync() {
@@ -186,35 +192,6 @@ __device__ __forceinline__ unsigned long long half_mask(unsigned b0, unsigned b1
     typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
     const u32x2 m = {(unsigned)((int)(b0 << (31 - p)) >> 31), (unsigned)((int)(b1 << (31 - p)) >> 31)};
     return __builtin_bit_cast(unsigned long long, m);
-}
-
-// Redo of the forward scan from position P on, up to (not including) position
-// `end` (wave-uniform), from state fr; nested so that it stops at `end`
-// without a loop.  The empty asm keeps each step a branch (not a select).
-template <int P, int SP>
-__device__ __forceinline__ void rerun_fwd(float &fr, float *Fs, const float *CF, const float *AX, int end) {
-    if constexpr (P < SP) {
-        if (P < end) {
-            asm volatile("");
-            fr = fmaf(CF[P], fr, AX[P]);
-            Fs[P] = fr;
-            rerun_fwd<P + 1, SP>(fr, Fs, CF, AX, end);
-        }
-    }
-}
-
-// Redo of the reverse scan from position P down, while the position is above
-// `last` (wave-uniform).
-template <int P>
-__device__ __forceinline__ void rerun_bwd(float &br, float *Bs, const float *CF, const float *AX, int last) {
-    if constexpr (P >= 0) {
-        if (P > last) {
-            asm volatile("");
-            br = fmaf(CF[P], br, AX[P]);
-            Bs[P] = br;
-            rerun_bwd<P - 1>(br, Bs, CF, AX, last);
-        }
-    }
 }
 
 // v in lanes outside m, 0 in lanes of m: one v_cndmask with the mask in SGPRs.
@@ -423,8 +400,6 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 
         // ---- tile metadata: track starts and lengths, start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
-        bool cross = false;
-        int fs1 = SP, le0 = -1;
         f32x16 r[MT][HT];
         if (work) {
             const int nxt = __shfl_down(off, 1);
@@ -451,10 +426,6 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             sb1 = unsigned(vstart >> SP) & spm;
             eb0 = unsigned(emask) & spm;
             eb1 = unsigned(emask >> SP) & spm;
-            // one track may straddle the two streams (tile hit SP is not a start)
-            cross = n > SP && !((smask >> SP) & 1ull);
-            fs1 = sb1 ? __builtin_ctz(sb1) : SP;       // fwd rerun: stream 1, p < fs1
-            le0 = eb0 ? 31 - __builtin_clz(eb0) : -1;  // bwd rerun: stream 0, p > le0
 
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
@@ -511,26 +482,29 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     const char *sl = slot();
                     const FT *wf = reinterpret_cast<const FT *>(sl);
                     const float *bias = reinterpret_cast<const float *>(sl + C::G1_FR * C::FRAG);
-                    // candidate and gate pre-activation, accumulated onto their biases
+                    // candidate and gate pre-activation (zero accumulators cost no moves)
                     const float bxv = bias[cc];
-                    const float bgv = bias[32 + cc];
+                    const float bgv = bias[32 + cc];  // -log2(e) b in the 16-bit modes
                     f32x16 ax[HT], gx[HT];
 #pragma unroll
                     for (int nt = 0; nt < HT; ++nt)
 #pragma unroll
                         for (int q = 0; q < 16; ++q) {
-                            ax[nt][q] = bxv;
-                            gx[nt][q] = bgv;
+                            ax[nt][q] = 0.f;
+                            gx[nt][q] = 0.f;
                         }
+                    // gate first, so that its exponentials can overlap the candidate's products
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        const FT bg = wf[(KS1 + ks) * 64 + lane];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
+                    }
 #pragma unroll
                     for (int ks = 0; ks < KS1; ++ks) {
                         const FT bx = wf[ks * 64 + lane];
-                        const FT bg = wf[(KS1 + ks) * 64 + lane];
 #pragma unroll
-                        for (int nt = 0; nt < HT; ++nt) {
-                            ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
-                            gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
-                        }
+                        for (int nt = 0; nt < HT; ++nt) ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
                     }
                     // gate a = sigmoid(g): the update adds a x and keeps cf = 1 - a of the state
                     float AX[HT * 16], CF[HT * 16];
@@ -543,16 +517,16 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             if constexpr (C::HALF) {
                                 // hardware exp2 and reciprocal; exp2 of a large argument is inf
                                 // (a = 0, cf = 1) or 0 (a = 1, cf = 0)
-                                const float e = __builtin_amdgcn_exp2f(g * -kLog2e);
+                                const float e = __builtin_amdgcn_exp2f(fmaf(g, -kLog2e, bgv));
                                 a = __builtin_amdgcn_rcpf(1.0f + e);
                                 cf = 1.0f - a;
                             } else {
                                 // library exp and correctly rounded division for the fp32 model
-                                const float e = expf(-__builtin_amdgcn_fmed3f(g, -80.0f, 80.0f));
+                                const float e = expf(-__builtin_amdgcn_fmed3f(g + bgv, -80.0f, 80.0f));
                                 a = 1.0f / (1.0f + e);
                                 cf = e * a;
                             }
-                            AX[nt * 16 + q] = a * ax[nt][q];
+                            AX[nt * 16 + q] = a * (ax[nt][q] + bxv);
                             CF[nt * 16 + q] = cf;
                         }
                     // Forward and reverse scans along this lane's stream, interleaved.  A
@@ -561,47 +535,55 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     // formed where they are used (the asm hides the loop invariance that
                     // would otherwise keep all of them in scalar registers).
                     unsigned ms0 = sb0, ms1 = sb1, me0 = eb0, me1 = eb1;
-                    int rf_end = fs1, rb_last = le0;
-                    asm volatile("" : "+s"(ms0), "+s"(ms1), "+s"(me0), "+s"(me1), "+s"(rf_end), "+s"(rb_last));
-                    float Fs[HT * 16], Bs[HT * 16];
+                    asm volatile("" : "+s"(ms0), "+s"(ms1), "+s"(me0), "+s"(me1));
+                    float Fs[HT * 16], Bs[HT * 16], CFf[HT * 16], CFb[HT * 16];
                     {
                         float f = 0.f, b = 0.f;
 #pragma unroll
                         for (int i = 0; i < SP; ++i) {
                             const int pb = SP - 1 - i;
-                            f = fmaf(zero_lanes(CF[i], half_mask(ms0, ms1, i)), f, AX[i]);
-                            b = fmaf(zero_lanes(CF[pb], half_mask(me0, me1, pb)), b, AX[pb]);
+                            CFf[i] = zero_lanes(CF[i], half_mask(ms0, ms1, i));
+                            CFb[pb] = zero_lanes(CF[pb], half_mask(me0, me1, pb));
+                            f = fmaf(CFf[i], f, AX[i]);
+                            b = fmaf(CFb[pb], b, AX[pb]);
                             Fs[i] = f;
                             Bs[pb] = b;
                         }
                     }
-                    if (cross) {
-                        // The track straddling the two streams: stream 1 redoes its forward
-                        // scan up to its first track start from the true state at the end of
-                        // stream 0, stream 0 its reverse scan back to its last track end from
-                        // the true state at the start of stream 1, with the operations of an
-                        // unsplit scan.  One lane swap brings both states across.
+                    {
+                        // A track may straddle the two streams: both scans run again from the
+                        // true boundary states, the end of stream 0 (forward, into stream 1)
+                        // and the start of stream 1 (reverse, into stream 0); the outer
+                        // boundaries keep their zero state.  With the zeroed coefficients
+                        // this reproduces every other position exactly, so the result is
+                        // that of one unsplit scan (and a tile without a straddling track
+                        // gets its first pass back).  One lane swap brings both states
+                        // across.
                         const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(Bs[0]),
                                                                          __float_as_uint(Fs[SP - 1]), false, false);
-                        if (hh) {
-                            float fr = __uint_as_float(xs[0]);  // Fs[SP - 1] of the lane in stream 0
-                            rerun_fwd<0, SP>(fr, Fs, CF, AX, rf_end);
-                        } else {
-                            float br = __uint_as_float(xs[1]);  // Bs[0] of the lane in stream 1
-                            rerun_bwd<SP - 1>(br, Bs, CF, AX, rb_last);
+                        float f = hh ? __uint_as_float(xs[0]) : 0.f;  // Fs[SP - 1] of stream 0
+                        float b = hh ? 0.f : __uint_as_float(xs[1]);  // Bs[0] of stream 1
+#pragma unroll
+                        for (int i = 0; i < SP; ++i) {
+                            const int pb = SP - 1 - i;
+                            f = fmaf(CFf[i], f, AX[i]);
+                            b = fmaf(CFb[pb], b, AX[pb]);
+                            Fs[i] = f;
+                            Bs[pb] = b;
                         }
                     }
                     wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
                     store_fb<C, FE>(ws, Fs, 0, hh, cc);
                     store_fb<C, FE>(ws, Bs, 32, hh, cc);
                 }
-                advance(false);
+                if constexpr (!C::MERGE) advance(false);
 
                 // ---- stage: output projection of this chunk, K split over chunks.  The
                 // 16-bit modes accumulate straight into the residual registers; the
                 // fp32 model sums the chunk in fresh accumulators and adds it once.
                 if (work) {
-                    const char *sl = slot();
+                    const char *sl = slot() + C::G2_OFF;
+                    if constexpr (C::MERGE) wave_lds_sync();  // this wave's [f; b] stores are visible
                     const FT *wo = reinterpret_cast<const FT *>(sl);
                     f32x16 part[C::HALF ? 1 : MT][HT];
                     if constexpr (!C::HALF) {
@@ -679,8 +661,17 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     wave_lds_sync();
                     for (int tr = hh; tr < k; tr += 2) {
                         const int s0 = t_start[tr], len = t_len[tr];
+                        // in order of u, eight independent reads at a time (rows past the
+                        // track's end are read in bounds and not added)
                         float sum = 0.f;
-                        for (int u = 0; u < len; ++u) sum += stage[(s0 + u) * C::STS + cc];
+                        for (int u0 = 0; u0 < len; u0 += 8) {
+                            float v[8];
+#pragma unroll
+                            for (int i = 0; i < 8; ++i) v[i] = stage[(s0 + (u0 + i < len ? u0 + i : len - 1)) * C::STS + cc];
+#pragma unroll
+                            for (int i = 0; i < 8; ++i)
+                                if (u0 + i < len) sum += v[i];
+                        }
                         pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
                     }
                     wave_lds_sync();
@@ -797,12 +788,12 @@ struct StageWriter {
 
 // Stage geometry of one instance, for the host.
 struct Geom {
-    int stage, ksps, nh1;
+    int stage, ksps, nh1, merge, g2_off;
 };
 template <int D, int OP, int HT>
 Geom geom() {
     using C = KCfg<D, OP, HT>;
-    return {C::STAGE, C::KSPS, C::NH1};
+    return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF};
 }
 template <int D, int OP>
 Geom geom_ht(int ht) {
@@ -859,6 +850,7 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const Geom G = op == OP_BF16 ? geom_d<OP_BF16>(D, ht) : op == OP_F16 ? geom_d<OP_F16>(D, ht) : geom_d<OP_F32>(D, ht);
     const int K = half ? 16 : 2, KL = K / 2, KS1 = D / K, KS2 = 64 / K, RPK = 16 / KL;
     const int MT = D / 32, NCH = D / 32;
+    const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
 
     // blob views
     const size_t dd = (size_t)D;
@@ -872,7 +864,7 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const float *W1 = blob + 4 * dd + (size_t)L * lstride;
     const float *b1 = W1 + dd * dd, *W2 = b1 + dd, *b2 = W2 + 5 * dd;
 
-    const int n_stages = 2 * L * NCH + G.nh1 + 1;
+    const int n_stages = (G.merge ? 1 : 2) * L * NCH + G.nh1 + 1;
     const size_t emb_bytes = (size_t)D * 16;
     const size_t emb_off = 0, st_off = (emb_bytes + 255) & ~size_t(255);
     const size_t err_off = st_off + (size_t)n_stages * G.stage;
@@ -911,11 +903,13 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
                             w.elem((double)Wi[(size_t)row * D + in] * g[in]);
                         }
             for (int c = 0; c < 32; ++c) w.f32(bi[32 * ch + c]);
-            for (int c = 0; c < 32; ++c) w.f32(bi[D + 32 * ch + c]);
+            for (int c = 0; c < 32; ++c) w.f32(gs * bi[D + 32 * ch + c]);
             // output projection A fragments: lane (g, c) value u of k-step kk of
             // block m holds W[out 32 m + c][column of [f; b] channel
             // q = kk K + g KL + u of the chunk]; then bout[D]
-            StageWriter w2{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            // (in the stage of the input projection, at g2_off, when stages are merged)
+            StageWriter w2{op, G.merge ? hb.data() + st_off + (size_t)(s - 1) * G.stage + G.g2_off
+                                       : hb.data() + st_off + (size_t)s++ * G.stage};
             for (int m = 0; m < MT; ++m)
                 for (int kk = 0; kk < KS2; ++kk)
                     for (int lane = 0; lane < 64; ++lane)
