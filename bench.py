@@ -12,7 +12,6 @@ import json
 import os
 import sys
 import time
-from concurrent.futures import ProcessPoolExecutor
 
 import numpy as np
 
@@ -36,32 +35,6 @@ def algorithmic_flops(n_layers, d, n_hits, n_tracks):
 def algorithmic_bytes(n_hits, n_tracks):
     """12 B per hit read, 4 B per track of offsets, 20 B per track written."""
     return 12.0 * n_hits + 4.0 * (n_tracks + 1) + 20.0 * n_tracks
-
-
-def _chunk(args):
-    name, c, n = args
-    h, l, _ = ts.make_track_chunk(ts.workload(name), c, n)
-    return h, l
-
-
-def generate(w, n_tracks, workers):
-    chunks = []
-    done, c = 0, 0
-    while done < n_tracks:
-        n = min(ts.TRACK_CHUNK, n_tracks - done)
-        chunks.append((w.name, c, n))
-        done += n
-        c += 1
-    if workers > 1 and len(chunks) > 1:
-        with ProcessPoolExecutor(workers) as ex:
-            parts = list(ex.map(_chunk, chunks))
-    else:
-        parts = [_chunk(a) for a in chunks]
-    hits = np.concatenate([p[0] for p in parts])
-    lengths = np.concatenate([p[1] for p in parts])
-    offs = np.zeros(n_tracks + 1, np.int64)
-    np.cumsum(lengths, out=offs[1:])
-    return hits, offs.astype(np.int32)
 
 
 def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
@@ -102,7 +75,7 @@ def main():
     ap.add_argument("--mode", default=None, help="library mode: fp32, bf16 or bf16_f16act")
     ap.add_argument("--n-tracks", type=int, default=None, help="override the workload's track count")
     ap.add_argument("--batch", type=int, default=None, help="tracks per fit_tracks call")
-    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
@@ -124,7 +97,7 @@ def main():
     workers = min(16, os.cpu_count() or 1)
 
     t0 = time.perf_counter()
-    hits, offs = generate(w, n_tracks, workers)
+    hits, offs = ts.make_tracks(w, n_tracks=n_tracks, workers=workers)
     blob = ts.make_weights(w)
     print(f"[bench] generated {n_tracks} tracks / {hits.shape[0]} hits in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)

@@ -15,26 +15,26 @@
 //    residual stream of the tile (slots x d, fp32) stays in registers for all
 //    layers; nothing but hits, offsets and the five outputs touches HBM.
 //  * All waves of a workgroup walk the same sequence of weight "stages" (the
-//    input projection of a 32-channel chunk, the output projection of that
-//    chunk, the head) in lockstep.  Each stage is copied once per workgroup
-//    from L2 into a double-buffered LDS ring, prefetched into registers one
-//    stage ahead, so matrix-core operands come from LDS and the copy of stage
-//    s+1 overlaps the compute of stage s.  Weights are stored in the device
-//    already in per-lane fragment order, so every copy and every operand read
-//    is a contiguous 1 KiB per wave.
+//    input and output projections of a 32-channel chunk, together or apart,
+//    then the head) in lockstep.  Each stage is copied once per workgroup from
+//    L2 straight into a ring of LDS slots (global_load_lds, up to three stages
+//    ahead), so matrix-core operands come from LDS and the copies overlap the
+//    compute.  Weights are stored in the device already in per-lane fragment
+//    order, so every copy and every operand read is a contiguous 1 KiB per
+//    wave.
 //  * Projections run on 32x32 matrix cores: v_mfma_f32_32x32x16_{bf16,f16}
 //    for the 16-bit modes, v_mfma_f32_32x32x2_f32 for the fp32 model.  The
 //    residual stream is held transposed (channels on MFMA rows, hits on
-//    columns), which is exactly the A-operand layout of the input projection,
+//    columns), which is exactly the operand layout of the input projection,
 //    so the norm output feeds the matrix core without any data movement.
 //  * The input projection puts hits on MFMA rows.  Hit slots are assigned to
 //    rows so that each lane's 16 accumulator rows per 32-hit tile are
 //    consecutive hits of one of two streams (lanes 0-31: first half of the
-//    tile, lanes 32-63: second half).  The scan along the track therefore runs
-//    serially in registers, one channel per lane; the single track that may
-//    straddle the two streams is finished with one cross-half exchange of the
-//    boundary state and a rerun of its steps in the second stream, so every
-//    track sees the same sequence of operations wherever it sits in a tile.
+//    tile, lanes 32-63: second half).  Both scans therefore run serially in
+//    registers, one channel per lane; the one track that may straddle the two
+//    streams is finished by a second pass from the true boundary states,
+//    which reproduces an unsplit scan exactly, so every track sees the same
+//    operations wherever it sits in a tile.
 //  * Scan outputs go through a wave-private LDS buffer once per 32-channel
 //    chunk (the only transpose), and the output projection for that chunk is
 //    accumulated into the residual registers (K split over chunks).

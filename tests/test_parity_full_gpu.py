@@ -1,0 +1,78 @@
+"""GPU parity at every workload's full size, in the launch configuration the
+benchmark times (the streamed deployment workload: 32 calls of 262 144 tracks
+captured in one HIP graph), checked against the fp64 oracle on a seeded sample
+of tracks, track by track.
+"""
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import tracksynth as ts
+from tests.parity import TOL, assert_parity
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+SAMPLE = {"tiny_d32_fp32": 256, "d128x4_fp32_65k": 1024, "d256x6_bf16_1m": 256,
+          "long64_d128x4_bf16_200k": 384, "deploy_d128x4_bf16_8m": 2048}
+WORKERS = min(16, os.cpu_count() or 1)
+
+
+@pytest.fixture(scope="module")
+def tf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32479_amd as tf
+    return tf
+
+
+def _launch(tf, W, h, o, n_tracks, batch):
+    """fit_tracks over the whole batch, as the benchmark launches it."""
+    out = torch.full((n_tracks, 5), float("nan"), dtype=torch.float32, device=h.device)
+    starts = list(range(0, n_tracks, batch))
+    if len(starts) == 1:
+        tf.fit_tracks(h, o, W, out=out, n_tracks=n_tracks)
+        torch.cuda.synchronize()
+        return out
+    side = torch.cuda.Stream()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        tf.fit_tracks(h, o, W, out=out, n_tracks=min(batch, n_tracks), stream=side)  # warm-up
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=side):
+            for s0 in starts:
+                tf.fit_tracks(h, o[s0:], W, out=out[s0:], n_tracks=min(batch, n_tracks - s0), stream=side)
+    out.fill_(float("nan"))
+    torch.cuda.synchronize()
+    graph.replay()
+    torch.cuda.synchronize()
+    return out
+
+
+@pytest.mark.parametrize("name", list(ts.WORKLOADS))
+def test_full_size_sampled(tf, name):
+    w = ts.WORKLOADS[name]
+    print(f"[full] {name}: {w.n_tracks} tracks", flush=True)
+    hits, offs = ts.make_tracks(w, workers=WORKERS)
+    n = offs.size - 1
+    blob = ts.make_weights(w)
+    W = tf.Weights(blob, w.n_layers, w.d_model, tf.MODE_FOR_WEIGHTS[w.dtype], max_hits=w.len_max)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    out = _launch(tf, W, h, o, n, w.batch or n).cpu().numpy()
+    assert tf.device_error(W) == 0
+    assert np.all(np.isfinite(out)), "a track was not written"
+
+    # seeded sample, always with the first and last track and a shortest and longest one
+    L = np.diff(offs)
+    rng = np.random.default_rng(11)
+    sel = set(rng.choice(n, size=min(SAMPLE[name], n), replace=False).tolist())
+    sel |= {0, n - 1, int(np.argmin(L)), int(np.argmax(L))}
+    sel = np.array(sorted(sel))
+    sh = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+    so = np.concatenate([[0], np.cumsum(L[sel])]).astype(np.int32)
+    ref = oracle.fit_tracks(sh, so, blob, w.n_layers, w.d_model)
+    emax, l2 = assert_parity(out[sel], ref, TOL[w.dtype], f"{name} full size, {sel.size} sampled tracks")
+    print(f"[full] {name}: {sel.size} sampled, max col err {emax.max():.3g}", flush=True)

@@ -187,25 +187,38 @@ def make_track_chunk(w: Workload, chunk: int, n: int, seed: int | None = None, s
     return hits, length.astype(np.int32), truth
 
 
+def _chunk_job(args):
+    w, chunk, n, seed, smear = args
+    return make_track_chunk(w, chunk, n, seed, smear)
+
+
 def make_tracks(w, n_tracks: int | None = None, seed: int | None = None, smear: bool = True,
-                with_truth: bool = False):
+                with_truth: bool = False, workers: int = 1):
     """Generate the first ``n_tracks`` tracks of a workload (default: all).
 
     Returns (hits float32 [H,3], offsets int32 [N+1]) and, if requested, the
-    truth perigee parameters float64 [N,5].
+    truth perigee parameters float64 [N,5].  ``workers`` > 1 generates the
+    fixed-size chunks in that many processes (same result: every chunk has its
+    own seeded streams).
     """
     w = workload(w)
     n_tracks = w.n_tracks if n_tracks is None else int(n_tracks)
-    hits_parts, len_parts, truth_parts = [], [], []
+    jobs = []
     done, chunk = 0, 0
     while done < n_tracks:
         n = min(TRACK_CHUNK, n_tracks - done)
-        h, l, t = make_track_chunk(w, chunk, n, seed, smear)
-        hits_parts.append(h)
-        len_parts.append(l)
-        truth_parts.append(t)
+        jobs.append((w, chunk, n, seed, smear))
         done += n
         chunk += 1
+    if workers > 1 and len(jobs) > 1:
+        from concurrent.futures import ProcessPoolExecutor
+        with ProcessPoolExecutor(min(workers, len(jobs))) as ex:
+            parts = list(ex.map(_chunk_job, jobs))
+    else:
+        parts = [_chunk_job(j) for j in jobs]
+    hits_parts = [p[0] for p in parts]
+    len_parts = [p[1] for p in parts]
+    truth_parts = [p[2] for p in parts]
     lengths = np.concatenate(len_parts) if len_parts else np.zeros(0, np.int32)
     offsets = np.zeros(n_tracks + 1, dtype=np.int64)
     np.cumsum(lengths, out=offsets[1:])
