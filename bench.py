@@ -75,6 +75,8 @@ def main():
     ap.add_argument("--mode", default=None, help="library mode: fp32, bf16 or bf16_f16act")
     ap.add_argument("--n-tracks", type=int, default=None, help="override the workload's track count")
     ap.add_argument("--batch", type=int, default=None, help="tracks per fit_tracks call")
+    ap.add_argument("--max-hits", type=int, default=None,
+                    help="tf_config.max_hits (default: the workload's longest track)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -106,7 +108,7 @@ def main():
     h = torch.from_numpy(hits).to(dev)
     o = torch.from_numpy(offs).to(dev)
     out = torch.empty((n_tracks, 5), dtype=torch.float32, device=dev)
-    W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=w.len_max)
+    W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=args.max_hits or w.len_max)
     starts = list(range(0, n_tracks, batch))
 
     def step(stream=None):

@@ -105,7 +105,7 @@ struct KCfg {
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
     static constexpr int FB_BYTES = CAP * FBS * EB;
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
-    static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 2 * MAXTR * 4;
+    static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 4 * MAXTR * 4;
     static constexpr int EMB_BYTES = D * 16;
     static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES;  // for the stage ring
     // Weight stages, all padded to STAGE bytes.  A chunk's input and output
@@ -314,8 +314,11 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     char *ws = smem + C::WAVE0 + wid * C::WAVE_BYTES;
     float *stage = reinterpret_cast<float *>(ws);                           // [CAP][STS]
     float *pblk = stage + CAP * C::STS;                                     // [MAXTR][STS]
-    int *t_start = reinterpret_cast<int *>(ws + C::WAVE_BYTES - 2 * MAXTR * 4);
+    // the tile's tracks: first tile row, length, first hit row, track index
+    int *t_start = reinterpret_cast<int *>(ws + C::WAVE_BYTES - 4 * MAXTR * 4);
     int *t_len = t_start + MAXTR;
+    int *t_off = t_len + MAXTR;
+    int *t_id = t_off + MAXTR;
 
     const int hh = lane >> 5;  // lane half
     const int cc = lane & 31;  // lane column
@@ -359,65 +362,94 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     int errbits = 0;
     const float qnan = __builtin_nanf("");
 
+    // Tiles are packed first-fit from a window of the wave's tracks: the first
+    // track not yet fitted (t) and the WIN - 1 after it, in track order; bit i
+    // of `taken` marks track t + i as fitted into an earlier tile (or refused).
+    // The first track of the window always fits, so every tile makes progress,
+    // and a track's result does not depend on the tile it lands in.
+    constexpr int WIN = 32;
     int t = g_begin;
+    unsigned taken = 0;
     for (;;) {
-        // ---- pick the tile: the longest run of whole tracks t.. with <= CAP hits.
-        // Tracks that cannot be fitted are flagged and skipped here.
-        int k = 0, n = 0, base = 0, off = 0;
+        int k = 0, n = 0;      // tracks and hit rows of the tile
+        unsigned sel = 0;      // window tracks of the tile
+        int off = 0, len = 0;  // lane i < WIN: first hit row and length of track t + i
         while (t < g_end) {
+            // slide the window past its leading fitted tracks
+            const int sh = taken == ~0u ? WIN : __builtin_ctz(~taken);
+            taken = sh == WIN ? 0u : taken >> sh;
+            t += sh;
+            if (t >= g_end) break;
             const int idx = t + lane;
             off = 0;
-            if (lane <= MAXTR && idx <= g_end) off = offsets[idx];
-            base = uniform(off);
-            const int prev = __shfl_up(off, 1);
-            const bool ok = lane >= 1 && lane <= MAXTR && idx <= g_end && off >= prev &&
-                            (long long)off - base <= CAP && (long long)off <= n_hits_total && base >= 0;
-            const unsigned long long okm = __ballot(ok);
-            k = __builtin_ctzll(~(okm >> 1));
-            if (k == 0) {
-                // rows outside [0, n_hits), an end offset before its start, or
-                // more hits than a tile holds
-                const int off1 = __builtin_amdgcn_readlane(off, 1);
-                const bool bad = base < 0 || off1 < base || (long long)off1 > n_hits_total;
-                errbits |= bad ? TF_DEVERR_BAD_OFFSETS : TF_DEVERR_TOO_LONG;
-                if (lane < 5) out[(size_t)t * 5 + lane] = qnan;
-                t += 1;
-                continue;
+            if (lane <= WIN && idx <= g_end) off = offsets[idx];
+            const int nxt = __shfl_down(off, 1);
+            len = nxt - off;
+            const bool fresh = lane < WIN && idx < g_end && !((taken >> (lane & 31)) & 1u);
+            // tracks that cannot be fitted: rows outside [0, n_hits), an end
+            // before the start, no hits, or more hits than a tile holds
+            const bool bad = off < 0 || nxt < off || (long long)nxt > n_hits_total;
+            const bool empty = !bad && len == 0;
+            const bool too_long = !bad && len > CAP;
+            const unsigned long long bad_m = __ballot(fresh && bad);
+            const unsigned long long empty_m = __ballot(fresh && empty);
+            const unsigned long long long_m = __ballot(fresh && too_long);
+            if (bad_m | empty_m | long_m) {
+                errbits |= (bad_m ? TF_DEVERR_BAD_OFFSETS : 0) | (empty_m ? TF_DEVERR_EMPTY_TRACK : 0) |
+                           (long_m ? TF_DEVERR_TOO_LONG : 0);
+                if (fresh && (bad || empty || too_long)) {
+#pragma unroll
+                    for (int e = 0; e < 5; ++e) out[(size_t)idx * 5 + e] = qnan;
+                }
+                taken |= unsigned(bad_m | empty_m | long_m);
             }
-            n = __builtin_amdgcn_readlane(off, k) - base;
-            if (n == 0) {  // all k tracks are empty
-                errbits |= TF_DEVERR_EMPTY_TRACK;
-                for (int e = lane; e < 5 * k; e += 64) out[(size_t)t * 5 + e] = qnan;
-                t += k;
-                continue;
+            // first-fit in track order
+            unsigned cand = unsigned(__ballot(fresh && !bad && !empty && !too_long));
+            int rows = 0;
+            while (cand) {
+                const int i = __builtin_ctz(cand);
+                cand &= cand - 1u;
+                const int li = __builtin_amdgcn_readlane(len, i);
+                if (rows + li <= CAP) {
+                    sel |= 1u << i;
+                    rows += li;
+                    if (++k == MAXTR || rows == CAP) break;
+                }
             }
-            break;
+            if (k > 0) {
+                n = rows;
+                taken |= sel;
+                break;
+            }
         }
-        const bool work = t < g_end;
+        const bool work = k > 0;
         wait_vmcnt<0>();                     // stages q .. q + NSLOT - 2 are in LDS
         if (!__syncthreads_or(work)) break;  // every wave of the workgroup is done
         copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_lds(q + C::NSLOT - 1), wid, lane);
 
-        // ---- tile metadata: track starts and lengths, start/end masks per stream
+        // ---- tile metadata: the tile's tracks in window order, on consecutive
+        // tile rows; start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
         f32x16 r[MT][HT];
         if (work) {
-            const int nxt = __shfl_down(off, 1);
-            if (lane < k) {
-                t_start[lane] = off - base;
-                t_len[lane] = nxt - off;
+            const bool mine = lane < WIN && ((sel >> (lane & 31)) & 1u);
+            const int v = mine ? len : 0;
+            int incl = v;  // inclusive prefix sum of the selected lengths over lanes
+#pragma unroll
+            for (int d = 1; d < WIN; d <<= 1) {
+                const int y = __shfl_up(incl, d);
+                if (lane >= d) incl += y;
+            }
+            const int row0 = incl - v;
+            if (mine) {
+                const int j = __builtin_popcount(sel & ((1u << (lane & 31)) - 1u));
+                t_start[j] = row0;
+                t_len[j] = len;
+                t_off[j] = off;
+                t_id[j] = t + lane;
             }
             unsigned long long smask = 0;
-            bool empty = false;
-            for (int j = 0; j < k; ++j) {
-                const int sj = __builtin_amdgcn_readlane(off, j) - base;
-                const int lj = __builtin_amdgcn_readlane(off, j + 1) - base - sj;
-                if (lj > 0)
-                    smask |= 1ull << sj;
-                else
-                    empty = true;
-            }
-            if (empty) errbits |= TF_DEVERR_EMPTY_TRACK;
+            for (unsigned m = sel; m; m &= m - 1u) smask |= 1ull << __builtin_amdgcn_readlane(row0, __builtin_ctz(m));
             const unsigned long long valid = n >= 64 ? ~0ull : ((1ull << n) - 1);
             const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
             const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
@@ -426,14 +458,17 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             sb1 = unsigned(vstart >> SP) & spm;
             eb0 = unsigned(emask) & spm;
             eb1 = unsigned(emask >> SP) & spm;
+            wave_lds_sync();  // the track table is written
 
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
-                const int th = slot_to_hit<SP>(32 * nt + cc);
+                const int th = slot_to_hit<SP>(32 * nt + cc);  // tile row
                 float hx = 0.f, hy = 0.f, hz = 0.f;
                 if (th < n) {
-                    const float *hp = hits + ((size_t)base + th) * 3;
+                    // the track holding tile row th, and the row's hit
+                    const int j = __builtin_popcountll(smask & ((2ull << th) - 1ull)) - 1;
+                    const float *hp = hits + ((size_t)t_off[j] + (th - t_start[j])) * 3;
                     hx = hp[0];
                     hy = hp[1];
                     hz = hp[2];
@@ -730,7 +765,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 if constexpr (C::HALF) o = F::mma(a, b_lo, o);
             }
             if (cc < k) {
-                float *op = out + (size_t)(t + cc) * 5;
+                float *op = out + (size_t)t_id[cc] * 5;
                 if (hh == 0) {
                     op[0] = o[0] + b2[0];
                     op[1] = o[1] + b2[1];
@@ -740,7 +775,6 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     op[4] = o[0] + b2[4];
                 }
             }
-            t += k;
         }
         advance(true);
     }
