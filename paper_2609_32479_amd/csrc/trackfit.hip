@@ -57,6 +57,7 @@ typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
 typedef __attribute__((ext_vector_type(8))) float f32x8;
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 // Matrix-core operand types.  OP_F32: fp32 weights and operands
@@ -122,6 +123,10 @@ struct KCfg {
     static constexpr int KSPS_RAW = (STAGE - D * 4) / (MT * FRAG);   // head-1 k-steps per stage
     static constexpr int KSPS = (KSPS_RAW >= KS1 ? KS1 : KSPS_RAW / KPB * KPB);
     static constexpr int NH1 = KS1 / KSPS;       // head-1 stages
+    // A tile of at most 16 tracks runs the head on 16x16x32 products (16
+    // track columns; the 16-bit modes), otherwise on 32x32 ones.
+    static constexpr bool HEAD16 = HALF && MAXTR <= 16;
+    static constexpr int UB = D / 16;            // 16-unit blocks of the head's hidden layer
     static constexpr int COPIES = STAGE / kCopyBytes;
     static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;  // copies per wave per stage
     // workgroup LDS: embedding table, a ring of stage slots, wave regions.  The
@@ -145,6 +150,9 @@ template <> struct Frag<OP_BF16> {
     static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
     }
+    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
     static __device__ __forceinline__ T pack(const float *v) {
         f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
         return __builtin_convertvector(f, bf16x8);
@@ -155,6 +163,9 @@ template <> struct Frag<OP_F16> {
     typedef _Float16 E;
     static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
         return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
     }
     static __device__ __forceinline__ T pack(const float *v) {
         f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
@@ -673,11 +684,20 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 
         // ---- head, transposed: hid^T = W1 p^T (hidden units on rows, tracks on
         // columns), pooled 32 channels at a time through wave-private LDS
-        f32x16 hid[MT];
+        f32x16 hid[C::HEAD16 ? 1 : MT];  // 32x32 head: units 32 m + 8 (q/4) + 4 hh + q%4 of track cc
+        f32x4 hq[C::HEAD16 ? C::UB : 1];  // 16x16 head: units 16 ub + 4 hg + i of track hcol
+        const int hcol = lane & 15, hg = lane >> 4;
+        if constexpr (C::HEAD16) {
 #pragma unroll
-        for (int m = 0; m < MT; ++m)
+            for (int ub = 0; ub < C::UB; ++ub)
 #pragma unroll
-            for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
+                for (int i = 0; i < 4; ++i) hq[ub][i] = 0.f;
+        } else {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
+        }
         const int prow = cc < MAXTR ? cc : MAXTR - 1;  // columns past the tile's tracks repeat the last
         for (int j = 0; j < C::NH1; ++j) {
             if (work) {
@@ -710,22 +730,50 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
                     }
                     wave_lds_sync();
-#pragma unroll
-                    for (int kb = 0; kb < KPB; ++kb) {
+                    if constexpr (C::HEAD16) {
+                        // one 32-channel k-step: lane (hg, hcol) holds channels 8 hg .. + 7 of track hcol
                         float v[8];
 #pragma unroll
-                        for (int u = 0; u < KL; ++u) v[u] = pblk[prow * C::STS + kb * K + hh * KL + u];
+                        for (int u = 0; u < 8; ++u) v[u] = pblk[hcol * C::STS + 8 * hg + u];
                         FT b_hi, b_lo;
                         split_operand<F>(v, b_hi, b_lo);
 #pragma unroll
-                        for (int mu = 0; mu < MT; ++mu) {
-                            const FT a = w1[((bl * KPB + kb) * MT + mu) * 64 + lane];
-                            hid[mu] = F::mma(a, b_hi, hid[mu]);
-                            if constexpr (C::HALF) hid[mu] = F::mma(a, b_lo, hid[mu]);
+                        for (int ub = 0; ub < C::UB; ++ub) {
+                            const FT a = w1[(bl * C::UB + ub) * 64 + lane];
+                            hq[ub] = F::mma16(a, b_hi, hq[ub]);
+                            hq[ub] = F::mma16(a, b_lo, hq[ub]);
+                        }
+                    } else {
+#pragma unroll
+                        for (int kb = 0; kb < KPB; ++kb) {
+                            float v[8];
+#pragma unroll
+                            for (int u = 0; u < KL; ++u) v[u] = pblk[prow * C::STS + kb * K + hh * KL + u];
+                            FT b_hi, b_lo;
+                            split_operand<F>(v, b_hi, b_lo);
+#pragma unroll
+                            for (int mu = 0; mu < MT; ++mu) {
+                                const FT a = w1[((bl * KPB + kb) * MT + mu) * 64 + lane];
+                                hid[mu] = F::mma(a, b_hi, hid[mu]);
+                                if constexpr (C::HALF) hid[mu] = F::mma(a, b_lo, hid[mu]);
+                            }
                         }
                     }
                 }
-                if (j == C::NH1 - 1) {
+                if constexpr (C::HEAD16) {
+                  if (j == C::NH1 - 1) {
+                    // bias and SiLU: lane (hg, hcol) holds units 16 ub + 4 hg + i of track hcol
+                    const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
+#pragma unroll
+                    for (int ub = 0; ub < C::UB; ++ub)
+#pragma unroll
+                        for (int i = 0; i < 4; ++i) {
+                            const float v = hq[ub][i] + b1[16 * ub + 4 * hg + i];
+                            hq[ub][i] = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
+                                                                  __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
+                        }
+                  }
+                } else if (j == C::NH1 - 1) {
                     // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
                     const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
@@ -747,7 +795,40 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         }
         // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
         // operand, output row q of column cc is output q of track cc
-        if (work) {
+        if constexpr (C::HEAD16) {
+          if (work) {
+            // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
+            // stored W2 fragments follow that order); output rows 4 hg + i
+            const FT *w2 = reinterpret_cast<const FT *>(slot());
+            const float *b2 = reinterpret_cast<const float *>(slot() + (D / 32) * C::FRAG);
+            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int kb = 0; kb < D / 32; ++kb) {
+                float v[8];
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    v[i] = hq[2 * kb][i];
+                    v[4 + i] = hq[2 * kb + 1][i];
+                }
+                FT b_hi, b_lo;
+                split_operand<F>(v, b_hi, b_lo);
+                const FT a = w2[kb * 64 + lane];
+                o = F::mma16(a, b_hi, o);
+                o = F::mma16(a, b_lo, o);
+            }
+            if (hcol < k) {
+                float *op = out + (size_t)t_id[hcol] * 5;
+                if (hg == 0) {
+                    op[0] = o[0] + b2[0];
+                    op[1] = o[1] + b2[1];
+                    op[2] = o[2] + b2[2];
+                    op[3] = o[3] + b2[3];
+                } else if (hg == 1) {
+                    op[4] = o[0] + b2[4];
+                }
+            }
+          }
+        } else if (work) {
             const FT *w2 = reinterpret_cast<const FT *>(slot());
             const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
             f32x16 o;
@@ -822,12 +903,12 @@ struct StageWriter {
 
 // Stage geometry of one instance, for the host.
 struct Geom {
-    int stage, ksps, nh1, merge, g2_off;
+    int stage, ksps, nh1, merge, g2_off, head16;
 };
 template <int D, int OP, int HT>
 Geom geom() {
     using C = KCfg<D, OP, HT>;
-    return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF};
+    return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF, C::HEAD16 ? 1 : 0};
 }
 template <int D, int OP>
 Geom geom_ht(int ht) {
@@ -956,34 +1037,64 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
             for (int c = 0; c < D; ++c) w2.f32(bo[c]);
         }
     }
-    // head layer 1 A fragments, KSPS k-steps per stage: lane (g, c) value u of
-    // k-step ks, unit tile mu holds W1[unit 32 mu + c][channel ks K + g KL + u];
-    // then b1[D]
-    for (int j = 0; j < G.nh1; ++j) {
+    if (G.head16) {
+        // 16x16x32 head.  Layer 1 A fragments, KSPS / 2 32-channel blocks per
+        // stage: lane value u of block bl, unit block ub holds
+        // W1[unit 16 ub + lane % 16][channel 32 bl + 8 (lane / 16) + u]; then b1[D]
+        const int bps = G.ksps / 2;
+        for (int j = 0; j < G.nh1; ++j) {
+            StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            for (int bl = 0; bl < bps; ++bl)
+                for (int ub = 0; ub < D / 16; ++ub)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int u = 0; u < 8; ++u) {
+                            const int ch = 32 * (j * bps + bl) + 8 * (lane / 16) + u;
+                            w.elem(W1[(size_t)(16 * ub + lane % 16) * D + ch]);
+                        }
+            for (int c = 0; c < D; ++c) w.f32(b1[c]);
+        }
+        // layer 2 A fragments: lane value u of k-step kb holds W2[output lane % 16]
+        // [unit 16 (2 kb + u / 4) + 4 (lane / 16) + u % 4] (zero for outputs >= 5),
+        // the order of the hidden accumulators; then b2[5]
         StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
-        for (int kl = 0; kl < G.ksps; ++kl)
-            for (int mu = 0; mu < MT; ++mu)
-                for (int lane = 0; lane < 64; ++lane)
-                    for (int u = 0; u < KL; ++u) {
-                        const int ks = j * G.ksps + kl;
-                        w.elem(W1[(size_t)(32 * mu + lane % 32) * D + ks * K + (lane / 32) * KL + u]);
-                    }
-        for (int c = 0; c < D; ++c) w.f32(b1[c]);
-    }
-    // head layer 2 A fragments: lane (g, c) value u of k-step ks holds
-    // W2[output c][unit 32 m + 8 i + 4 g + j] (zero for c >= 5), the same unit
-    // order as the hidden accumulators; then b2[5]
-    {
-        StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
-        for (int ks = 0; ks < KS1; ++ks)
+        for (int kb = 0; kb < D / 32; ++kb)
             for (int lane = 0; lane < 64; ++lane)
-                for (int u = 0; u < KL; ++u) {
-                    const int gg = lane / 32, c = lane % 32;
-                    const int reg = (ks % RPK) * KL + u, m = ks / RPK;
-                    const int unit = 32 * m + 8 * (reg / 4) + 4 * gg + (reg % 4);
-                    w.elem(c < 5 ? (double)W2[(size_t)c * D + unit] : 0.0);
+                for (int u = 0; u < 8; ++u) {
+                    const int o = lane % 16;
+                    const int unit = 16 * (2 * kb + u / 4) + 4 * (lane / 16) + u % 4;
+                    w.elem(o < 5 ? (double)W2[(size_t)o * D + unit] : 0.0);
                 }
         for (int c = 0; c < 5; ++c) w.f32(b2[c]);
+    } else {
+        // head layer 1 A fragments, KSPS k-steps per stage: lane (g, c) value u of
+        // k-step ks, unit tile mu holds W1[unit 32 mu + c][channel ks K + g KL + u];
+        // then b1[D]
+        for (int j = 0; j < G.nh1; ++j) {
+            StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            for (int kl = 0; kl < G.ksps; ++kl)
+                for (int mu = 0; mu < MT; ++mu)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int u = 0; u < KL; ++u) {
+                            const int ks = j * G.ksps + kl;
+                            w.elem(W1[(size_t)(32 * mu + lane % 32) * D + ks * K + (lane / 32) * KL + u]);
+                        }
+            for (int c = 0; c < D; ++c) w.f32(b1[c]);
+        }
+        // head layer 2 A fragments: lane (g, c) value u of k-step ks holds
+        // W2[output c][unit 32 m + 8 i + 4 g + j] (zero for c >= 5), the same unit
+        // order as the hidden accumulators; then b2[5]
+        {
+            StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            for (int ks = 0; ks < KS1; ++ks)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int u = 0; u < KL; ++u) {
+                        const int gg = lane / 32, c = lane % 32;
+                        const int reg = (ks % RPK) * KL + u, m = ks / RPK;
+                        const int unit = 32 * m + 8 * (reg / 4) + 4 * gg + (reg % 4);
+                        w.elem(c < 5 ? (double)W2[(size_t)c * D + unit] : 0.0);
+                    }
+            for (int c = 0; c < 5; ++c) w.f32(b2[c]);
+        }
     }
 
     tf_weights *wt = new (std::nothrow) tf_weights();
