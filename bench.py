@@ -23,6 +23,17 @@ import tracksynth as ts  # noqa: E402
 METRIC = "tracks/sec (encoder+head forward) on 1 MI355X; MFMA util / HBM GB/s vs peak"
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6, "bf16_f16act": 2516.6}  # dense MFMA, MI355X datasheet
 PEAK_HBM_GBS = 8000.0
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc", "trackfit.hip")
+COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
+
+# HBM bytes per launch of the deployment workload's 262 144-track call, from two
+# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of this script with
+# --copy-calibration, each scaled by the same counter's reading for a plain
+# device copy of known size (profiles/ holds the summary).  Valid only for the
+# kernel source whose SHA-256 is recorded; otherwise traffic is reported null.
+TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "batch": 262144, "calls_per_step": 32,
+           "kernel_sha256": "d5cbee2132ac69f6ca2f1c26d7e4111519221321c58d8976014d2e5cf1a6403c",
+           "fetch_bytes": 50678127, "write_bytes": 5293904}
 
 
 def algorithmic_flops(n_layers, d, n_hits, n_tracks):
@@ -66,6 +77,22 @@ def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
             "parity_max_col_err_on_sample": err}
 
 
+def traffic_bytes(w, batch, calls):
+    """Counter-derived HBM bytes per launch, when they were taken on this kernel
+    source and this launch shape; else None."""
+    if TRAFFIC is None or calls != TRAFFIC["calls_per_step"] or batch != TRAFFIC["batch"]:
+        return None
+    if w.name != TRAFFIC["workload"] or kernel_source_sha256() != TRAFFIC["kernel_sha256"]:
+        return None
+    return TRAFFIC["fetch_bytes"] + TRAFFIC["write_bytes"]
+
+
+def kernel_source_sha256():
+    import hashlib
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -81,6 +108,8 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help=f"after the timed region, run a plain {COPY_MIB} MiB device copy (for counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -182,7 +211,7 @@ def main():
                    "max_hits": W.max_hits,
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved_tflops / peak, "traffic": None,
+                     "frac": achieved_tflops / peak, "traffic": traffic_bytes(w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
@@ -192,6 +221,12 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, blob, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
+    if args.copy_calibration:
+        src = torch.ones(COPY_MIB * (1 << 20) // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            torch.neg(src, out=dst)  # reads and writes COPY_MIB MiB
+        torch.cuda.synchronize()
     print(json.dumps(res), flush=True)
 
 
