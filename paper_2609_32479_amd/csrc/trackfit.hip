@@ -100,7 +100,7 @@ struct KCfg {
     static constexpr int EB = HALF ? 2 : 4;      // operand element bytes
     static constexpr int FRAG = 64 * KL * EB;    // one wave-wide operand fragment
     // waves per workgroup and per SIMD
-    static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 8 : 4;
+    static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 12 : 4;
     // wave-private LDS: [f; b] buffer, aliased by the pooling scratch
     static constexpr int FBS = HALF ? 72 : 65;   // row stride of [f; b] (elements)
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
@@ -239,25 +239,21 @@ __device__ __forceinline__ void split_operand(const float *v, typename F::T &hi,
     }
 }
 
-// Scan outputs of one lane (stream hh, channel cc of the chunk) to the [f; b]
-// buffer: row = hit slot of position p, column = col0 + cc.  Positions p and
-// p + 1 (p even) sit in slots s and s + 1; 16-bit values are converted in pairs.
+// Positions p and p + 1 (p even) of one lane's scan outputs to the [f; b]
+// buffer (rows = hit slots s and s + 1 of the positions, column col0 + cc).
 template <class C, class E>
-__device__ __forceinline__ void store_fb(char *ws, const float *v, int col0, int hh, int cc) {
+__device__ __forceinline__ void store_fb_pair(char *ws, int p, float v0, float v1, int col0, int hh, int cc) {
     E *fb = reinterpret_cast<E *>(ws) + col0 + cc;
-#pragma unroll
-    for (int p = 0; p < C::SP; p += 2) {
-        const int s = 32 * (p >> 4) + 8 * ((p >> 2) & 3) + 4 * hh + (p & 3);
-        if constexpr (sizeof(E) == 2) {
-            typedef E e2 __attribute__((ext_vector_type(2)));
-            typedef float f2 __attribute__((ext_vector_type(2)));
-            const e2 pr = __builtin_convertvector((f2){v[p], v[p + 1]}, e2);
-            fb[s * C::FBS] = pr.x;
-            fb[(s + 1) * C::FBS] = pr.y;
-        } else {
-            fb[s * C::FBS] = v[p];
-            fb[(s + 1) * C::FBS] = v[p + 1];
-        }
+    const int s = 32 * (p >> 4) + 8 * ((p >> 2) & 3) + 4 * hh + (p & 3);
+    if constexpr (sizeof(E) == 2) {
+        typedef E e2 __attribute__((ext_vector_type(2)));
+        typedef float f2 __attribute__((ext_vector_type(2)));
+        const e2 pr = __builtin_convertvector((f2){v0, v1}, e2);
+        fb[s * C::FBS] = pr.x;
+        fb[(s + 1) * C::FBS] = pr.y;
+    } else {
+        fb[s * C::FBS] = v0;
+        fb[(s + 1) * C::FBS] = v1;
     }
 }
 
@@ -605,10 +601,13 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         // that of one unsplit scan (and a tile without a straddling track
                         // gets its first pass back).  One lane swap brings both states
                         // across.
+                        // Each pair of positions goes to the [f; b] buffer as soon as it is
+                        // final, which keeps few scan outputs live.
                         const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(Bs[0]),
                                                                          __float_as_uint(Fs[SP - 1]), false, false);
                         float f = hh ? __uint_as_float(xs[0]) : 0.f;  // Fs[SP - 1] of stream 0
                         float b = hh ? 0.f : __uint_as_float(xs[1]);  // Bs[0] of stream 1
+                        wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
 #pragma unroll
                         for (int i = 0; i < SP; ++i) {
                             const int pb = SP - 1 - i;
@@ -616,11 +615,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             b = fmaf(CFb[pb], b, AX[pb]);
                             Fs[i] = f;
                             Bs[pb] = b;
+                            if (i & 1) {
+                                store_fb_pair<C, FE>(ws, i - 1, Fs[i - 1], Fs[i], 0, hh, cc);
+                                store_fb_pair<C, FE>(ws, pb, Bs[pb], Bs[pb + 1], 32, hh, cc);
+                            }
                         }
                     }
-                    wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
-                    store_fb<C, FE>(ws, Fs, 0, hh, cc);
-                    store_fb<C, FE>(ws, Bs, 32, hh, cc);
                 }
                 if constexpr (!C::MERGE) advance(false);
 
