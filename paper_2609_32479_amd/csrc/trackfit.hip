@@ -535,6 +535,10 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             ax[nt][q] = 0.f;
                             gx[nt][q] = 0.f;
                         }
+                    // matrix-core phases run at raised wave priority, so that a wave
+                    // entering one gets the SIMD's issue slots ahead of the vector work
+                    // of the other waves
+                    __builtin_amdgcn_s_setprio(1);
                     // gate first, so that its exponentials can overlap the candidate's products
 #pragma unroll
                     for (int ks = 0; ks < KS1; ++ks) {
@@ -548,6 +552,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 #pragma unroll
                         for (int nt = 0; nt < HT; ++nt) ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
                     }
+                    __builtin_amdgcn_s_setprio(0);
                     // gate a = sigmoid(g): the update adds a x and keeps cf = 1 - a of the state
                     float AX[HT * 16], CF[HT * 16];
 #pragma unroll
@@ -630,6 +635,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 if (work) {
                     const char *sl = slot() + C::G2_OFF;
                     if constexpr (C::MERGE) wave_lds_sync();  // this wave's [f; b] stores are visible
+                    __builtin_amdgcn_s_setprio(1);
                     const FT *wo = reinterpret_cast<const FT *>(sl);
                     f32x16 part[C::HALF ? 1 : MT][HT];
                     if constexpr (!C::HALF) {
@@ -678,6 +684,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             }
                     }
                 }
+                __builtin_amdgcn_s_setprio(0);
                 advance(false);
             }
         }
