@@ -32,8 +32,8 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # device copy of known size (profiles/ holds the summary).  Valid only for the
 # kernel source whose SHA-256 is recorded; otherwise traffic is reported null.
 TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "batch": 262144, "calls_per_step": 32,
-           "kernel_sha256": "d5cbee2132ac69f6ca2f1c26d7e4111519221321c58d8976014d2e5cf1a6403c",
-           "fetch_bytes": 50678127, "write_bytes": 5293904}
+           "kernel_sha256": "e937ddb7d9793af8b96fadf6ac45ab5be68c89b6f46da6b32a1065cc4612a048",
+           "fetch_bytes": 50702062, "write_bytes": 5538656}
 
 
 def algorithmic_flops(n_layers, d, n_hits, n_tracks):

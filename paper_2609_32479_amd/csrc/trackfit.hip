@@ -101,6 +101,11 @@ struct KCfg {
     static constexpr int FRAG = 64 * KL * EB;    // one wave-wide operand fragment
     // waves per workgroup and per SIMD
     static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 12 : 4;
+    // Three waves per SIMD leave 168 registers a wave.  Under that budget the
+    // kernel re-derives lane-dependent values where they are used and defines
+    // its per-tile register arrays on every path, so that nothing is held (or
+    // spilled) across tiles.
+    static constexpr bool TIGHT = WAVES > 4;
     // wave-private LDS: [f; b] buffer, aliased by the pooling scratch
     static constexpr int FBS = HALF ? 72 : 65;   // row stride of [f; b] (elements)
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
@@ -195,6 +200,13 @@ __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// The lane index, read afresh: values derived from it are formed where they
+// are used instead of being held in registers across the whole kernel.
+__device__ __forceinline__ int fresh_lane() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
 __device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
 
 // Lane mask (wave-uniform, 64 bits) of the lanes whose stream has bit p set:
@@ -437,7 +449,15 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         // ---- tile metadata: the tile's tracks in window order, on consecutive
         // tile rows; start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
-        f32x16 r[MT][HT];
+        f32x16 r[MT][HT];  // the residual stream (a wave without a tile keeps zeros)
+        if constexpr (C::TIGHT) {
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) r[m][nt][q] = 0.f;
+        }
         if (work) {
             const bool mine = lane < WIN && ((sel >> (lane & 31)) & 1u);
             const int v = mine ? len : 0;
@@ -449,7 +469,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             }
             const int row0 = incl - v;
             if (mine) {
-                const int j = __builtin_popcount(sel & ((1u << (lane & 31)) - 1u));
+                const int j = __builtin_amdgcn_mbcnt_lo(sel, 0);  // selected tracks before this one
                 t_start[j] = row0;
                 t_len[j] = len;
                 t_off[j] = off;
@@ -470,7 +490,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
-                const int th = slot_to_hit<SP>(32 * nt + cc);  // tile row
+                const int th = slot_to_hit<SP>(32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31));  // tile row
                 float hx = 0.f, hy = 0.f, hz = 0.f;
                 if (th < n) {
                     // the track holding tile row th, and the row's hit
@@ -493,6 +513,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         // ---- layers
         for (int l = 0; l < P.n_layers; ++l) {
             FT yf[HT][KS1];
+            if constexpr (C::TIGHT) {
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) yf[nt][ks] = FT{};
+            }
             if (work) {
                 // RMSNorm: each lane holds half the channels of hit slot 32 nt + cc
 #pragma unroll
@@ -691,176 +717,182 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 
         // ---- head, transposed: hid^T = W1 p^T (hidden units on rows, tracks on
         // columns), pooled 32 channels at a time through wave-private LDS
-        f32x16 hid[C::HEAD16 ? 1 : MT];  // 32x32 head: units 32 m + 8 (q/4) + 4 hh + q%4 of track cc
-        f32x4 hq[C::HEAD16 ? C::UB : 1];  // 16x16 head: units 16 ub + 4 hg + i of track hcol
-        const int hcol = lane & 15, hg = lane >> 4;
-        if constexpr (C::HEAD16) {
+        {  // the head re-derives its lane values (see KCfg::TIGHT)
+            const int lane = C::TIGHT ? fresh_lane() : int(threadIdx.x & 63);
+            const int hh = lane >> 5, cc = lane & 31;
+            f32x16 hid[C::HEAD16 ? 1 : MT];  // 32x32 head: units 32 m + 8 (q/4) + 4 hh + q%4 of track cc
+            f32x4 hq[C::HEAD16 ? C::UB : 1];  // 16x16 head: units 16 ub + 4 hg + i of track hcol
+            const int hcol = lane & 15, hg = lane >> 4;
+            if constexpr (C::HEAD16) {
 #pragma unroll
-            for (int ub = 0; ub < C::UB; ++ub)
+                for (int ub = 0; ub < C::UB; ++ub)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) hq[ub][i] = 0.f;
-        } else {
+                    for (int i = 0; i < 4; ++i) hq[ub][i] = 0.f;
+            } else {
 #pragma unroll
-            for (int m = 0; m < MT; ++m)
+                for (int m = 0; m < MT; ++m)
 #pragma unroll
-                for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
-        }
-        const int prow = cc < MAXTR ? cc : MAXTR - 1;  // columns past the tile's tracks repeat the last
-        for (int j = 0; j < C::NH1; ++j) {
-            if (work) {
-                const FT *w1 = reinterpret_cast<const FT *>(slot());
+                    for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
+            }
+            const int prow = cc < MAXTR ? cc : MAXTR - 1;  // columns past the tile's tracks repeat the last
+            // unrolled, so that the residual block pooled at each step is a fixed register block
 #pragma unroll
-                for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
-                    const int m = j * (C::KSPS / KPB) + bl;  // channel block being pooled
-                    wave_lds_sync();
+            for (int j = 0; j < C::NH1; ++j) {
+                if (work) {
+                    const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
-                    for (int nt = 0; nt < HT; ++nt) {
-                        const int th = slot_to_hit<SP>(32 * nt + cc);
+                    for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
+                        const int m = j * (C::KSPS / KPB) + bl;  // channel block being pooled
+                        wave_lds_sync();
 #pragma unroll
-                        for (int q = 0; q < 16; ++q)
-                            stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
-                    }
-                    wave_lds_sync();
-                    for (int tr = hh; tr < k; tr += 2) {
-                        const int s0 = t_start[tr], len = t_len[tr];
-                        // in order of u, eight independent reads at a time (rows past the
-                        // track's end are read in bounds and not added)
-                        float sum = 0.f;
-                        for (int u0 = 0; u0 < len; u0 += 8) {
+                        for (int nt = 0; nt < HT; ++nt) {
+                            const int th = slot_to_hit<SP>(32 * nt + cc);
+#pragma unroll
+                            for (int q = 0; q < 16; ++q)
+                                stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
+                        }
+                        wave_lds_sync();
+                        for (int tr = hh; tr < k; tr += 2) {
+                            const int s0 = t_start[tr], len = t_len[tr];
+                            // in order of u, eight independent reads at a time (rows past the
+                            // track's end are read in bounds and not added)
+                            float sum = 0.f;
+                            for (int u0 = 0; u0 < len; u0 += 8) {
+                                float v[8];
+#pragma unroll
+                                for (int i = 0; i < 8; ++i) v[i] = stage[(s0 + (u0 + i < len ? u0 + i : len - 1)) * C::STS + cc];
+#pragma unroll
+                                for (int i = 0; i < 8; ++i)
+                                    if (u0 + i < len) sum += v[i];
+                            }
+                            pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
+                        }
+                        wave_lds_sync();
+                        if constexpr (C::HEAD16) {
+                            // one 32-channel k-step: lane (hg, hcol) holds channels 8 hg .. + 7 of track hcol
                             float v[8];
 #pragma unroll
-                            for (int i = 0; i < 8; ++i) v[i] = stage[(s0 + (u0 + i < len ? u0 + i : len - 1)) * C::STS + cc];
-#pragma unroll
-                            for (int i = 0; i < 8; ++i)
-                                if (u0 + i < len) sum += v[i];
-                        }
-                        pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
-                    }
-                    wave_lds_sync();
-                    if constexpr (C::HEAD16) {
-                        // one 32-channel k-step: lane (hg, hcol) holds channels 8 hg .. + 7 of track hcol
-                        float v[8];
-#pragma unroll
-                        for (int u = 0; u < 8; ++u) v[u] = pblk[hcol * C::STS + 8 * hg + u];
-                        FT b_hi, b_lo;
-                        split_operand<F>(v, b_hi, b_lo);
-#pragma unroll
-                        for (int ub = 0; ub < C::UB; ++ub) {
-                            const FT a = w1[(bl * C::UB + ub) * 64 + lane];
-                            hq[ub] = F::mma16(a, b_hi, hq[ub]);
-                            hq[ub] = F::mma16(a, b_lo, hq[ub]);
-                        }
-                    } else {
-#pragma unroll
-                        for (int kb = 0; kb < KPB; ++kb) {
-                            float v[8];
-#pragma unroll
-                            for (int u = 0; u < KL; ++u) v[u] = pblk[prow * C::STS + kb * K + hh * KL + u];
+                            for (int u = 0; u < 8; ++u) v[u] = pblk[hcol * C::STS + 8 * hg + u];
                             FT b_hi, b_lo;
                             split_operand<F>(v, b_hi, b_lo);
 #pragma unroll
-                            for (int mu = 0; mu < MT; ++mu) {
-                                const FT a = w1[((bl * KPB + kb) * MT + mu) * 64 + lane];
-                                hid[mu] = F::mma(a, b_hi, hid[mu]);
-                                if constexpr (C::HALF) hid[mu] = F::mma(a, b_lo, hid[mu]);
+                            for (int ub = 0; ub < C::UB; ++ub) {
+                                const FT a = w1[(bl * C::UB + ub) * 64 + lane];
+                                hq[ub] = F::mma16(a, b_hi, hq[ub]);
+                                hq[ub] = F::mma16(a, b_lo, hq[ub]);
+                            }
+                        } else {
+#pragma unroll
+                            for (int kb = 0; kb < KPB; ++kb) {
+                                float v[8];
+#pragma unroll
+                                for (int u = 0; u < KL; ++u) v[u] = pblk[prow * C::STS + kb * K + hh * KL + u];
+                                FT b_hi, b_lo;
+                                split_operand<F>(v, b_hi, b_lo);
+#pragma unroll
+                                for (int mu = 0; mu < MT; ++mu) {
+                                    const FT a = w1[((bl * KPB + kb) * MT + mu) * 64 + lane];
+                                    hid[mu] = F::mma(a, b_hi, hid[mu]);
+                                    if constexpr (C::HALF) hid[mu] = F::mma(a, b_lo, hid[mu]);
+                                }
                             }
                         }
                     }
-                }
-                if constexpr (C::HEAD16) {
-                  if (j == C::NH1 - 1) {
-                    // bias and SiLU: lane (hg, hcol) holds units 16 ub + 4 hg + i of track hcol
-                    const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
+                    if constexpr (C::HEAD16) {
+                      if (j == C::NH1 - 1) {
+                        // bias and SiLU: lane (hg, hcol) holds units 16 ub + 4 hg + i of track hcol
+                        const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
-                    for (int ub = 0; ub < C::UB; ++ub)
+                        for (int ub = 0; ub < C::UB; ++ub)
 #pragma unroll
-                        for (int i = 0; i < 4; ++i) {
-                            const float v = hq[ub][i] + b1[16 * ub + 4 * hg + i];
-                            hq[ub][i] = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
-                                                                  __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
-                        }
-                  }
-                } else if (j == C::NH1 - 1) {
-                    // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
-                    const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
-#pragma unroll
-                    for (int mu = 0; mu < MT; ++mu)
-#pragma unroll
-                        for (int q = 0; q < 16; ++q) {
-                            const float v = hid[mu][q] + b1[32 * mu + 8 * (q >> 2) + 4 * hh + (q & 3)];
-                            float sv;  // SiLU(v) = v / (1 + exp(-v))
-                            if constexpr (C::HALF)
-                                sv = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
+                            for (int i = 0; i < 4; ++i) {
+                                const float v = hq[ub][i] + b1[16 * ub + 4 * hg + i];
+                                hq[ub][i] = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
                                                                       __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
-                            else
-                                sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
-                            hid[mu][q] = sv;
-                        }
+                            }
+                      }
+                    } else if (j == C::NH1 - 1) {
+                        // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
+                        const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
+#pragma unroll
+                        for (int mu = 0; mu < MT; ++mu)
+#pragma unroll
+                            for (int q = 0; q < 16; ++q) {
+                                const float v = hid[mu][q] + b1[32 * mu + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                                float sv;  // SiLU(v) = v / (1 + exp(-v))
+                                if constexpr (C::HALF)
+                                    sv = v * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(
+                                                                          __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
+                                else
+                                    sv = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
+                                hid[mu][q] = sv;
+                            }
+                    }
                 }
+                advance(false);
             }
-            advance(false);
-        }
-        // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
-        // operand, output row q of column cc is output q of track cc
-        if constexpr (C::HEAD16) {
-          if (work) {
-            // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
-            // stored W2 fragments follow that order); output rows 4 hg + i
-            const FT *w2 = reinterpret_cast<const FT *>(slot());
-            const float *b2 = reinterpret_cast<const float *>(slot() + (D / 32) * C::FRAG);
-            f32x4 o = {0.f, 0.f, 0.f, 0.f};
+            // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
+            // operand, output row q of column cc is output q of track cc
+            if constexpr (C::HEAD16) {
+              if (work) {
+                // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
+                // stored W2 fragments follow that order); output rows 4 hg + i
+                const FT *w2 = reinterpret_cast<const FT *>(slot());
+                const float *b2 = reinterpret_cast<const float *>(slot() + (D / 32) * C::FRAG);
+                f32x4 o = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int kb = 0; kb < D / 32; ++kb) {
-                float v[8];
+                for (int kb = 0; kb < D / 32; ++kb) {
+                    float v[8];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    v[i] = hq[2 * kb][i];
-                    v[4 + i] = hq[2 * kb + 1][i];
+                    for (int i = 0; i < 4; ++i) {
+                        v[i] = hq[2 * kb][i];
+                        v[4 + i] = hq[2 * kb + 1][i];
+                    }
+                    FT b_hi, b_lo;
+                    split_operand<F>(v, b_hi, b_lo);
+                    const FT a = w2[kb * 64 + lane];
+                    o = F::mma16(a, b_hi, o);
+                    o = F::mma16(a, b_lo, o);
                 }
-                FT b_hi, b_lo;
-                split_operand<F>(v, b_hi, b_lo);
-                const FT a = w2[kb * 64 + lane];
-                o = F::mma16(a, b_hi, o);
-                o = F::mma16(a, b_lo, o);
-            }
-            if (hcol < k) {
-                float *op = out + (size_t)t_id[hcol] * 5;
-                if (hg == 0) {
-                    op[0] = o[0] + b2[0];
-                    op[1] = o[1] + b2[1];
-                    op[2] = o[2] + b2[2];
-                    op[3] = o[3] + b2[3];
-                } else if (hg == 1) {
-                    op[4] = o[0] + b2[4];
+                if (hcol < k) {
+                    float *op = out + (size_t)t_id[hcol] * 5;
+                    if (hg == 0) {
+                        op[0] = o[0] + b2[0];
+                        op[1] = o[1] + b2[1];
+                        op[2] = o[2] + b2[2];
+                        op[3] = o[3] + b2[3];
+                    } else if (hg == 1) {
+                        op[4] = o[0] + b2[4];
+                    }
                 }
-            }
-          }
-        } else if (work) {
-            const FT *w2 = reinterpret_cast<const FT *>(slot());
-            const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
-            f32x16 o;
+              }
+            } else if (work) {
+                const FT *w2 = reinterpret_cast<const FT *>(slot());
+                const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
+                f32x16 o;
 #pragma unroll
-            for (int q = 0; q < 16; ++q) o[q] = 0.f;
+                for (int q = 0; q < 16; ++q) o[q] = 0.f;
 #pragma unroll
-            for (int ks = 0; ks < KS1; ++ks) {
-                float v[8];
+                for (int ks = 0; ks < KS1; ++ks) {
+                    float v[8];
 #pragma unroll
-                for (int u = 0; u < KL; ++u) v[u] = hid[ks / RPK][(ks % RPK) * KL + u];
-                FT b_hi, b_lo;
-                split_operand<F>(v, b_hi, b_lo);
-                const FT a = w2[ks * 64 + lane];
-                o = F::mma(a, b_hi, o);
-                if constexpr (C::HALF) o = F::mma(a, b_lo, o);
-            }
-            if (cc < k) {
-                float *op = out + (size_t)t_id[cc] * 5;
-                if (hh == 0) {
-                    op[0] = o[0] + b2[0];
-                    op[1] = o[1] + b2[1];
-                    op[2] = o[2] + b2[2];
-                    op[3] = o[3] + b2[3];
-                } else {
-                    op[4] = o[0] + b2[4];
+                    for (int u = 0; u < KL; ++u) v[u] = hid[ks / RPK][(ks % RPK) * KL + u];
+                    FT b_hi, b_lo;
+                    split_operand<F>(v, b_hi, b_lo);
+                    const FT a = w2[ks * 64 + lane];
+                    o = F::mma(a, b_hi, o);
+                    if constexpr (C::HALF) o = F::mma(a, b_lo, o);
+                }
+                if (cc < k) {
+                    float *op = out + (size_t)t_id[cc] * 5;
+                    if (hh == 0) {
+                        op[0] = o[0] + b2[0];
+                        op[1] = o[1] + b2[1];
+                        op[2] = o[2] + b2[2];
+                        op[3] = o[3] + b2[3];
+                    } else {
+                        op[4] = o[0] + b2[4];
+                    }
                 }
             }
         }
