@@ -45,6 +45,12 @@ def lib():
                                      ctypes.c_size_t, dp, ctypes.c_int]
         L.orc_threads.restype = ctypes.c_int
         L.orc_threads.argtypes = [ctypes.c_int]
+        L.orc_seed_from_points.restype = ctypes.c_int
+        L.orc_seed_from_points.argtypes = [dp, ctypes.c_double, dp]
+        L.orc_seed_features_hit.restype = None
+        L.orc_seed_features_hit.argtypes = [dp, ctypes.c_double, dp, dp]
+        L.orc_seed_tracks.restype = ctypes.c_long
+        L.orc_seed_tracks.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_double, dp, dp]
         _lib = L
     return _lib
 
@@ -143,3 +149,43 @@ def fit_tracks(hits, offsets, blob, n_layers, d, n_threads=0):
 
 def threads(n_threads=0) -> int:
     return int(lib().orc_threads(int(n_threads)))
+
+
+# ---------------------------------------------------------------------------
+# Analytic three-hit seed and per-hit seed residual features (Sec. Method,
+# Analytic seed); fp64.
+# ---------------------------------------------------------------------------
+
+def seed_from_points(points, b_tesla):
+    """Seed (d0, z0, phi, theta, q/p) from three points [3, 3] (fp64 in mm);
+    NaN if no circle passes through them."""
+    p, pp = _d(np.asarray(points, dtype=np.float64).reshape(9))
+    out = np.empty(5)
+    lib().orc_seed_from_points(pp, float(b_tesla), out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return out
+
+
+def seed_features_hit(seed, b_tesla, hit):
+    """(asinh dU, asinh dV, helix path length) of one hit against a seed."""
+    s, ps = _d(seed)
+    h, ph = _d(np.asarray(hit, dtype=np.float64).reshape(3))
+    out = np.empty(3)
+    lib().orc_seed_features_hit(ps, float(b_tesla), ph, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return out
+
+
+def seed_tracks(hits, offsets, b_tesla, features=True):
+    """Packed batch (float32 hits): returns (seeds [N, 5], features [H, 3] or
+    None, number of tracks without a seed).  Feature row r belongs to hit row
+    offsets[0] + r."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    n = offsets.size - 1
+    seeds = np.empty((max(n, 0), 5))
+    dp = ctypes.POINTER(ctypes.c_double)
+    feats = np.empty((int(offsets[-1] - offsets[0]) if n > 0 else 0, 3)) if features else None
+    rc = lib().orc_seed_tracks(ph, offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n, float(b_tesla),
+                               seeds.ctypes.data_as(dp), feats.ctypes.data_as(dp) if features else None)
+    if rc < 0:
+        raise ValueError("oracle rejected its arguments")
+    return seeds, feats, int(rc)

@@ -8,10 +8,10 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 
 def build(verbose: bool = False) -> str:
-    src = os.path.join(HERE, "oracle.c")
+    srcs = [os.path.join(HERE, f) for f in ("oracle.c", "seed.c")]
     tmp = LIB + ".tmp"
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", "-Wextra",
-           src, "-o", tmp, "-lm"]
+           *srcs, "-o", tmp, "-lm"]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
