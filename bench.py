@@ -6,6 +6,9 @@ mean pool, head) over the workload's batch stream: for the deployment workload
 8,388,608 synthetic helix tracks in 32 fit_tracks calls of 262,144 tracks,
 captured once in a HIP graph and replayed.  Inputs are resident in HBM before
 the timed region.  Prints one JSON line.
+
+``--path seed`` instead times the analytic three-hit seed with its per-hit
+residual features (tf_seed_tracks) over the same tracks, one call per step.
 """
 import argparse
 import json
@@ -93,6 +96,120 @@ def kernel_source_sha256():
         return hashlib.sha256(f.read()).hexdigest()
 
 
+SEED_METRIC = "tracks/sec (fp64 three-hit seed + per-hit residual features) on 1 MI355X; HBM GB/s vs peak"
+SEED_SRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc", "seed.hip")
+# HBM bytes of one tf_seed_tracks call over the whole deployment workload, from
+# FETCH_SIZE / WRITE_SIZE runs of this script's seed path with --copy-calibration
+# (scaled as for the encoder); valid only for the recorded source.
+SEED_TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "n_tracks": 8388608,
+                "kernel_sha256": "0c35360525fc4d780d486b8f00cad12a6b0bc32d655328daf811ca9424b4fcab",
+                "fetch_bytes": 2675781353, "write_bytes": 1780067216}
+
+
+def seed_algorithmic_bytes(n_hits, n_tracks):
+    """Offsets (4 B per track), every hit read once (12 B), a float32 feature
+    triple written per hit (12 B), a float64 seed written per track (40 B)."""
+    return 4.0 * (n_tracks + 1) + 24.0 * n_hits + 40.0 * n_tracks
+
+
+def seed_cpu_baseline(w, hits, offs, seconds, gpu_seeds):
+    """Time the fp64 seed oracle (one thread) on a bounded, seeded sample."""
+    import oracle
+    n_all = offs.size - 1
+    rng = np.random.default_rng(7)
+
+    def run(sel):
+        L = offs[sel + 1] - offs[sel]
+        h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+        o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+        t0 = time.perf_counter()
+        seeds, _, _ = oracle.seed_tracks(h, o, w.b_field)
+        return seeds, time.perf_counter() - t0
+
+    idx = np.sort(rng.choice(n_all, size=min(4096, n_all), replace=False))
+    _, dt = run(idx)
+    n = int(min(n_all, max(4096, 4096 * seconds / max(dt, 1e-4))))
+    sel = np.sort(rng.choice(n_all, size=n, replace=False))
+    ref, dt = run(sel)
+    g = gpu_seeds[sel]
+    g[:, 2] -= np.round((g[:, 2] - ref[:, 2]) / (2 * np.pi)) * 2 * np.pi
+    rms = np.sqrt(np.mean(ref ** 2, axis=0))
+    err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), rms)))
+    return {"value": n / dt, "unit": "tracks/s", "cores": 1, "kind": "oracle",
+            "sample": f"{n} tracks drawn without replacement (seed 7) from the {n_all}-track workload, "
+                      f"fp64 C oracle with features, {dt:.1f} s wall",
+            "parity_max_col_err_on_sample": err}
+
+
+def seed_traffic_bytes(w, n_tracks):
+    import hashlib
+    with open(SEED_SRC, "rb") as f:
+        sha = hashlib.sha256(f.read()).hexdigest()
+    if w.name != SEED_TRAFFIC["workload"] or n_tracks != SEED_TRAFFIC["n_tracks"] or sha != SEED_TRAFFIC["kernel_sha256"]:
+        return None
+    return SEED_TRAFFIC["fetch_bytes"] + SEED_TRAFFIC["write_bytes"]
+
+
+def bench_seed(args, w, hits, offs):
+    import torch
+    import paper_2609_32479_amd as tf
+    dev = torch.device("cuda:0")
+    h = torch.from_numpy(hits).to(dev)
+    o = torch.from_numpy(offs).to(dev)
+    n_tracks = offs.size - 1
+    n_hits = int(offs[-1] - offs[0])
+    seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
+    feats = torch.empty((n_hits, 3), dtype=torch.float32, device=dev)
+    flags = torch.zeros(1, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    def step():
+        tf.seed_tracks(h, o, w.b_field, seeds=seeds, feats=feats, flags=flags, stream=stream)
+
+    for _ in range(max(args.warmup, 1)):
+        step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record(stream)
+    for _ in range(args.steps):
+        step()
+    e1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    byts = seed_algorithmic_bytes(n_hits, n_tracks)
+    gbs = byts / (ms_per_step / 1e3) / 1e9
+    res = {
+        "metric": SEED_METRIC, "value": n_tracks / (ms_per_step / 1e3), "unit": "tracks/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "f64",
+        "data": "synthetic helix tracks (2 T solenoid, seeded)",
+        "config": {"workload": w.name, "n_tracks": n_tracks, "n_hits": n_hits, "calls_per_step": 1,
+                   "b_tesla": w.b_field, "features": True},
+        "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                     "frac": gbs / PEAK_HBM_GBS, "traffic": seed_traffic_bytes(w, n_tracks), "kernel": "tf_seed_kernel",
+                     "kernel_avg_ms": ms_per_step, "bytes_per_launch": byts},
+        "host_wall_s": wall,
+        "device_error_flags": int(flags.item()),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = seed_cpu_baseline(w, hits, offs, args.cpu_seconds, seeds.cpu().numpy())
+    if args.copy_calibration:
+        copy_calibration(dev)
+    print(json.dumps(res), flush=True)
+
+
+def copy_calibration(dev):
+    """A plain elementwise device copy of known size, for scaling HBM counters."""
+    import torch
+    src = torch.ones(COPY_MIB * (1 << 20) // 4, dtype=torch.float32, device=dev)
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        torch.neg(src, out=dst)  # reads and writes COPY_MIB MiB
+    torch.cuda.synchronize()
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -108,6 +225,8 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
+    ap.add_argument("--path", default="encoder", choices=["encoder", "seed"],
+                    help="encoder: fit_tracks (default); seed: tf_seed_tracks with features")
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"after the timed region, run a plain {COPY_MIB} MiB device copy (for counter calibration)")
     args = ap.parse_args()
@@ -129,9 +248,12 @@ def main():
 
     t0 = time.perf_counter()
     hits, offs = ts.make_tracks(w, n_tracks=n_tracks, workers=workers)
-    blob = ts.make_weights(w)
     print(f"[bench] generated {n_tracks} tracks / {hits.shape[0]} hits in {time.perf_counter() - t0:.1f} s",
           file=sys.stderr, flush=True)
+    if args.path == "seed":
+        bench_seed(args, w, hits, offs)
+        return
+    blob = ts.make_weights(w)
 
     dev = torch.device("cuda:0")
     h = torch.from_numpy(hits).to(dev)
@@ -222,11 +344,7 @@ def main():
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, blob, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
     if args.copy_calibration:
-        src = torch.ones(COPY_MIB * (1 << 20) // 4, dtype=torch.float32, device=dev)
-        dst = torch.empty_like(src)
-        for _ in range(3):
-            torch.neg(src, out=dst)  # reads and writes COPY_MIB MiB
-        torch.cuda.synchronize()
+        copy_calibration(dev)
     print(json.dumps(res), flush=True)
 
 

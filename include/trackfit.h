@@ -142,6 +142,52 @@ tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, 
  * TF_DEVERR_* bits seen since the last clear. */
 tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear);
 
+/*
+ * Analytic three-hit seed of every track, and optionally the per-hit seed
+ * residual features (Sec. Method, "Analytic seed"; fp64 throughout, as the
+ * paper computes the seed).
+ *
+ * Seed: the circle through the track's first three hits in the transverse
+ * plane gives pT = 0.299792458 * b_tesla * R[m] and the charge (field along
+ * +z: a positive track turns clockwise seen from +z), its closest approach to
+ * the z axis the perigee (d0, phi), and the transverse arc lengths of the
+ * first and third hit from the perigee give theta and z0.  Conventions: the
+ * perigee point is d0 * (-sin phi, cos phi) and phi the direction of motion
+ * there; theta in (0, pi); q/p in 1/GeV.
+ * Features of each hit: asinh(dU), asinh(dV) and the helix path length from
+ * the perigee (mm), where (dU, dV) is the hit's residual to the seed helix in
+ * the curvilinear frame of the helix (dU transverse, dV along the other
+ * direction normal to the motion), in mm.
+ *
+ * hits      device, float32 [n_hits][3] = (x, y, z) in mm, time-ordered within
+ *           each track (the first three hits make the seed).  Read only.
+ * n_hits    rows of hits (bounds every read).
+ * offsets   device, int32 [n_tracks + 1], as for fit_tracks.  Read only.
+ * n_tracks  host scalar >= 0.  0 is a no-op returning TF_OK.
+ * b_tesla   host scalar > 0: solenoid field along +z.
+ * seeds     device, float64 [n_tracks][5]: d0 [mm], z0 [mm], phi, theta,
+ *           q/p [1/GeV].  Every row is written.
+ * features  device, float32 [offsets[n_tracks] - offsets[0]][3], or NULL to
+ *           skip them: row r belongs to hit row offsets[0] + r.
+ * flags     device int32 or NULL: OR-ed with TF_SEED_* bits of the tracks that
+ *           got NaN seeds (their features are NaN too, unless their offsets
+ *           are bad, in which case their rows are not written).
+ * stream    HIP stream (0 = null stream).
+ *
+ * Asynchronous, allocates nothing (graph-capturable).  Outputs must not
+ * overlap the inputs.  Errors: TF_EINVAL (null pointers with n_tracks > 0,
+ * negative sizes, b_tesla <= 0), TF_EHIP (launch failure).
+ */
+tf_status tf_seed_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                         double b_tesla, double *seeds, float *features, int32_t *flags, hipStream_t stream);
+
+/* Bits of tf_seed_tracks' flags. */
+#define TF_SEED_TOO_SHORT 1    /* fewer than three hits */
+#define TF_SEED_NO_CIRCLE 2    /* two of the first three hits coincide in the transverse plane, or the
+                                  three are collinear */
+#define TF_SEED_BAD_OFFSETS 4  /* decreasing offsets, or rows outside [0, n_hits) or outside
+                                  [offsets[0], offsets[n_tracks]) */
+
 /* Static description of a status code. */
 const char *tf_status_string(tf_status s);
 

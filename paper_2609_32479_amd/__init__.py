@@ -14,7 +14,7 @@ import torch  # noqa: F401  -- load torch's HIP runtime before the library (one 
 
 __all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_size",
            "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS",
-           "TrackfitError", "lib"]
+           "TrackfitError", "lib", "seed_tracks", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtrackfit.so")
 
@@ -25,9 +25,10 @@ DTYPES = {"fp32": TF_FP32, "bf16": TF_BF16, "bf16_f16act": TF_BF16_F16ACT}
 # bf16 weights run with fp16 activation operands (see include/trackfit.h).
 MODE_FOR_WEIGHTS = {"fp32": "fp32", "bf16": "bf16_f16act"}
 DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS = 1, 2, 4
+SEED_TOO_SHORT, SEED_NO_CIRCLE, SEED_BAD_OFFSETS = 1, 2, 4
 
 EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_max_hits",
-            "fit_tracks", "tf_get_device_error", "tf_status_string")
+            "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks")
 
 
 class TrackfitError(RuntimeError):
@@ -66,6 +67,8 @@ def lib():
         L.tf_get_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
         L.tf_status_string.restype = ctypes.c_char_p
         L.tf_status_string.argtypes = [ctypes.c_int]
+        L.tf_seed_tracks.restype = ctypes.c_int
+        L.tf_seed_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, ctypes.c_double, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -159,3 +162,45 @@ def device_error(weights: Weights, stream=None, clear: bool = True) -> int:
     _check(lib().tf_get_device_error(weights.handle, _stream_handle(stream), ctypes.byref(v), int(clear)),
            "tf_get_device_error")
     return int(v.value)
+
+
+def seed_tracks(hits: torch.Tensor, offsets: torch.Tensor, b_tesla: float, features: bool = True,
+                seeds: torch.Tensor | None = None, feats: torch.Tensor | None = None,
+                flags: torch.Tensor | None = None, n_tracks: int | None = None, stream=None):
+    """Enqueue the analytic three-hit seed (and the per-hit residual features)
+    of a packed batch on ``stream`` (default: current stream).
+
+    hits float32 [H, 3] and offsets int32 [N+1] on the GPU.  Returns
+    (seeds float64 [N, 5], features float32 [offsets[N] - offsets[0], 3] or
+    None).  ``flags`` (int32 GPU tensor of one element) is OR-ed with the
+    SEED_* bits of tracks without a seed.
+    """
+    if not (hits.is_cuda and offsets.is_cuda):
+        raise ValueError("hits and offsets must be GPU tensors")
+    if hits.dtype != torch.float32 or offsets.dtype != torch.int32:
+        raise TypeError("hits must be float32 and offsets int32")
+    if not (hits.is_contiguous() and offsets.is_contiguous()) or hits.dim() != 2 or hits.shape[1] != 3:
+        raise ValueError("hits must be a contiguous [H, 3] tensor and offsets contiguous")
+    n = offsets.numel() - 1 if n_tracks is None else int(n_tracks)
+    if n < 0 or n + 1 > offsets.numel():
+        raise ValueError("n_tracks does not fit the offsets array")
+    if seeds is None:
+        seeds = torch.empty((n, 5), dtype=torch.float64, device=hits.device)
+    elif not (seeds.is_cuda and seeds.dtype == torch.float64 and seeds.is_contiguous() and seeds.numel() >= 5 * n):
+        raise ValueError("seeds must be a contiguous float64 GPU tensor with room for [N, 5]")
+    fptr = None
+    if features:
+        if feats is None:  # sized from the offsets (a device read: pass feats to stay asynchronous)
+            rows = int(offsets[n].item() - offsets[0].item()) if n > 0 else 0
+            feats = torch.empty((max(rows, 0), 3), dtype=torch.float32, device=hits.device)
+        elif not (feats.is_cuda and feats.dtype == torch.float32 and feats.is_contiguous()):
+            raise ValueError("feats must be a contiguous float32 GPU tensor with a row per hit of the batch")
+        fptr = feats.data_ptr()
+    else:
+        feats = None
+    if flags is not None and not (flags.is_cuda and flags.dtype == torch.int32 and flags.numel() >= 1):
+        raise ValueError("flags must be an int32 GPU tensor")
+    _check(lib().tf_seed_tracks(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, float(b_tesla),
+                                seeds.data_ptr(), fptr, flags.data_ptr() if flags is not None else None,
+                                _stream_handle(stream)), "tf_seed_tracks")
+    return seeds, feats

@@ -71,3 +71,10 @@ def test_argument_checks_without_gpu(tf):
     assert L.fit_tracks(None, 0, None, 0, None, None, None) == tf.TF_EINVAL
     assert L.tf_get_device_error(None, None, None, 0) == tf.TF_EINVAL
     L.tf_weights_destroy(None)   # no-op
+    # tf_seed_tracks: checks made before any launch
+    assert L.tf_seed_tracks(None, 0, None, 0, 2.0, None, None, None, None) == tf.TF_OK      # no tracks
+    assert L.tf_seed_tracks(None, 0, None, -1, 2.0, None, None, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, -1, None, 0, 2.0, None, None, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, 0, None, 0, 0.0, None, None, None, None) == tf.TF_EINVAL  # field
+    assert L.tf_seed_tracks(None, 0, None, 0, float("nan"), None, None, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, 10, None, 5, 2.0, None, None, None, None) == tf.TF_EINVAL  # null pointers
