@@ -39,7 +39,20 @@ def lib():
             fn.restype = None
             fn.argtypes = [dp, dp, ctypes.c_int, ctypes.c_int, dp]
         L.orc_track_forward.restype = ctypes.c_int
-        L.orc_track_forward.argtypes = [fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, dp, dp, dp]
+        L.orc_track_forward.argtypes = [fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, dp, dp, dp, dp]
+        L.orc_track_states.restype = ctypes.c_long
+        L.orc_track_states.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp, ctypes.c_size_t, dp,
+                                       ctypes.c_int]
+        L.orc_readout_blob_size.restype = ctypes.c_size_t
+        L.orc_readout_blob_size.argtypes = [ctypes.c_int]
+        L.orc_median_odd.restype = ctypes.c_double
+        L.orc_median_odd.argtypes = [dp, ctypes.c_int]
+        L.orc_decode.restype = None
+        L.orc_decode.argtypes = [dp, dp, dp]
+        L.orc_readout_track.restype = None
+        L.orc_readout_track.argtypes = [dp, ctypes.c_int, fp, dp, dp, dp]
+        L.orc_readout_tracks.restype = ctypes.c_long
+        L.orc_readout_tracks.argtypes = [dp, ctypes.c_int32, ctypes.c_int, fp, ctypes.c_size_t, dp, dp, dp]
         L.orc_fit_tracks.restype = ctypes.c_long
         L.orc_fit_tracks.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
                                      ctypes.c_size_t, dp, ctypes.c_int]
@@ -118,8 +131,10 @@ def scan_backward(x, a):
     return _scan(lib().orc_scan_backward, x, a)
 
 
-def track_forward(hits, blob, n_layers, d):
-    """One track: returns (out5, pooled [d], residual stream after the last layer [L, d])."""
+def track_forward(hits, blob, n_layers, d, with_states=False):
+    """One track: returns (out5, pooled [d], residual stream after the last layer [L, d])
+    and, if asked, the last layer's end states [2d] (forward at the last hit,
+    reverse at the first hit)."""
     hits, ph = _f(np.asarray(hits).reshape(-1, 3))
     blob, pb = _f(blob)
     assert blob.size == blob_size(n_layers, d)
@@ -127,10 +142,13 @@ def track_forward(hits, blob, n_layers, d):
     out = np.empty(5)
     pooled = np.empty(d)
     resid = np.empty((max(L, 1), d))
+    states = np.empty(2 * d)
     dp = ctypes.POINTER(ctypes.c_double)
     rc = lib().orc_track_forward(ph, L, n_layers, d, pb, out.ctypes.data_as(dp),
-                                 pooled.ctypes.data_as(dp), resid.ctypes.data_as(dp))
-    return out, pooled, (resid[:L] if rc == 0 else None)
+                                 pooled.ctypes.data_as(dp), resid.ctypes.data_as(dp),
+                                 states.ctypes.data_as(dp) if (with_states and n_layers > 0) else None)
+    res = (out, pooled, (resid[:L] if rc == 0 else None))
+    return res + (states,) if with_states else res
 
 
 def fit_tracks(hits, offsets, blob, n_layers, d, n_threads=0):
@@ -189,3 +207,54 @@ def seed_tracks(hits, offsets, b_tesla, features=True):
     if rc < 0:
         raise ValueError("oracle rejected its arguments")
     return seeds, feats, int(rc)
+
+
+# ---------------------------------------------------------------------------
+# The paper's readout and decode (Sec. Encoder, last paragraph; Sec. Losses).
+# ---------------------------------------------------------------------------
+
+def track_states(hits, offsets, blob, n_layers, d, n_threads=0):
+    """Packed batch: the last layer's end states [N, 2d] (NaN rows for empty tracks)."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    blob, pb = _f(blob)
+    n = offsets.size - 1
+    st = np.empty((max(n, 0), 2 * d))
+    rc = lib().orc_track_states(ph, offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n, n_layers, d,
+                                pb, blob.size, st.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(n_threads))
+    if rc < 0:
+        raise ValueError("oracle rejected its arguments")
+    return st
+
+
+def readout_blob_size(d):
+    return int(lib().orc_readout_blob_size(int(d)))
+
+
+def median_odd(v):
+    v, pv = _d(v)
+    return float(lib().orc_median_odd(pv, v.size))
+
+
+def decode(seed, med):
+    s, ps = _d(seed)
+    m, pm = _d(med)
+    out = np.empty(5)
+    lib().orc_decode(ps, pm, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
+    return out
+
+
+def readout_tracks(states, seeds, head_blob, d):
+    """states [N, 2d], seeds [N, 5] -> (quantiles [N, 35], decoded [N, 5])."""
+    st, pst = _d(np.asarray(states).reshape(-1, 2 * d))
+    sd, psd = _d(np.asarray(seeds).reshape(-1, 5))
+    hb, phb = _f(head_blob)
+    n = st.shape[0]
+    assert sd.shape[0] == n
+    q = np.empty((n, 35))
+    out = np.empty((n, 5))
+    dp = ctypes.POINTER(ctypes.c_double)
+    rc = lib().orc_readout_tracks(pst, n, d, phb, hb.size, psd, q.ctypes.data_as(dp), out.ctypes.data_as(dp))
+    if rc < 0:
+        raise ValueError("oracle rejected its arguments")
+    return q, out

@@ -136,15 +136,20 @@ static void to_double(const float *src, size_t n, double *dst) {
  * One track through the whole model.  hits: [L][3] float (x, y, z) in mm.
  * out5 receives the five head outputs (d0, z0, phi, theta, q/p order).
  * pooled (length d) and resid ([L][d], the residual stream after the last
- * layer) are optional outputs for the tests.  Returns 0, or -1 if L < 1
- * (then out5 is NaN: the mean over zero hits is undefined).
+ * layer) are optional outputs for the tests.  states (length 2d, optional)
+ * receives the last layer's end states read by the paper's own readout
+ * (Sec. Encoder, last paragraph): the forward state at the last hit, then
+ * the reverse state at the first hit.  Returns 0, or -1 if L < 1 (then out5,
+ * pooled and states are NaN: the mean over zero hits is undefined).
  */
 int orc_track_forward(const float *hits, int L, int n_layers, int d, const float *blob,
-                      double *out5, double *pooled, double *resid) {
+                      double *out5, double *pooled, double *resid, double *states) {
     if (L < 1) {
         for (int k = 0; k < 5; ++k) out5[k] = NAN;
         if (pooled)
             for (int j = 0; j < d; ++j) pooled[j] = NAN;
+        if (states)
+            for (int j = 0; j < 2 * d; ++j) states[j] = NAN;
         return -1;
     }
     orc_params P;
@@ -188,6 +193,10 @@ int orc_track_forward(const float *hits, int L, int n_layers, int d, const float
         /* forward and reverse scans, Eq. (2) */
         orc_scan_forward(x, a, L, d, f);
         orc_scan_backward(x, a, L, d, b);
+        if (states && l == n_layers - 1) {
+            memcpy(states, f + (size_t)(L - 1) * d, sizeof(double) * dd);
+            memcpy(states + dd, b, sizeof(double) * dd);
+        }
         /* merge the two directions: r <- r + W_out [f; b] + b_out */
         to_double(P.outW + off, dd * 2 * dd, Wd);
         to_double(P.outb + off, dd, bd);
@@ -240,7 +249,35 @@ long orc_fit_tracks(const float *hits, const int32_t *offsets, int32_t n_tracks,
     for (int32_t i = 0; i < n_tracks; ++i) {
         int L = offsets[i + 1] - offsets[i];
         if (orc_track_forward(hits + (size_t)offsets[i] * 3, L, n_layers, d, blob, out + (size_t)i * 5,
-                              NULL, NULL) != 0)
+                              NULL, NULL, NULL) != 0)
+            bad += 1;
+    }
+    (void)n_threads;
+    return bad;
+}
+
+/* Packed batch of the paper readout's inputs: states [n_tracks][2d] (forward
+ * state at the last hit, reverse state at the first hit, of the last layer).
+ * Returns the number of tracks with no hits (NaN rows), or -1 for bad
+ * arguments.  With n_layers = 0 there are no states and every row is NaN. */
+long orc_track_states(const float *hits, const int32_t *offsets, int32_t n_tracks, int n_layers, int d,
+                      const float *blob, size_t n_floats, double *states, int n_threads) {
+    if (n_tracks < 0 || d <= 0 || n_layers < 0 || !blob || (n_tracks > 0 && (!hits || !offsets || !states)))
+        return -1;
+    if (n_floats != orc_blob_size(n_layers, d)) return -1;
+    long bad = 0;
+#ifdef _OPENMP
+    int nt = n_threads > 0 ? n_threads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nt) reduction(+ : bad)
+#endif
+    for (int32_t i = 0; i < n_tracks; ++i) {
+        int L = offsets[i + 1] - offsets[i];
+        double out5[5];
+        double *st = states + (size_t)i * 2 * d;
+        if (n_layers == 0)
+            for (int j = 0; j < 2 * d; ++j) st[j] = NAN;
+        if (orc_track_forward(hits + (size_t)offsets[i] * 3, L, n_layers, d, blob, out5, NULL, NULL,
+                              n_layers > 0 ? st : NULL) != 0)
             bad += 1;
     }
     (void)n_threads;

@@ -43,7 +43,7 @@ def bidir_scan(x, a):
     return f, b
 
 
-def track_forward(hits, blob, n_layers, d, eps=1e-6):
+def track_forward(hits, blob, n_layers, d, eps=1e-6, states_out=None):
     P = ts.split_blob(blob, n_layers, d)
     X = np.asarray(hits, dtype=np.float64).reshape(-1, 3)
     lo = np.array([-1000.0, -1000.0, -3000.0])
@@ -58,7 +58,31 @@ def track_forward(hits, blob, n_layers, d, eps=1e-6):
         x, gate = z[:, :d], z[:, d:2 * d]
         f, b = bidir_scan(x, expit(gate))
         r = r + np.concatenate([f, b], axis=1) @ P[p + "out.W"].T + P[p + "out.b"]
+        last_states = np.concatenate([f[-1], b[0]])
+    if states_out is not None and n_layers > 0:
+        states_out[:] = last_states
     pooled = r.mean(axis=0)
     h = pooled @ P["head.W1"].T + P["head.b1"]
     h = h * expit(h)
     return h @ P["head.W2"].T + P["head.b2"], pooled, r
+
+
+def readout(states, seed, head_blob, d, eps=1e-6):
+    """The paper's readout and decode, restated with numpy: RMSNorm over the 2d
+    end states, SiLU hidden layer, 35 quantiles, per-parameter median of seven,
+    seed-anchored decode (phi wrapped to [-pi, pi), scale-free q/p with
+    epsilon 0.02 / GeV)."""
+    sizes = [2 * d, d * 2 * d, d, 35 * d, 35]
+    parts = np.split(np.asarray(head_blob, dtype=np.float64), np.cumsum(sizes)[:-1])
+    g, W1, b1, W2, b2 = parts[0], parts[1].reshape(d, 2 * d), parts[2], parts[3].reshape(35, d), parts[4]
+    z = np.asarray(states, dtype=np.float64)
+    y = g * z / np.sqrt(np.mean(z * z) + eps)
+    h = W1 @ y + b1
+    h = h * expit(h)
+    q = W2 @ h + b2
+    med = np.median(q.reshape(5, 7), axis=1)
+    s = np.asarray(seed, dtype=np.float64)
+    out = s + med
+    out[2] = (out[2] + np.pi) % (2 * np.pi) - np.pi
+    out[4] = s[4] + med[4] * (abs(s[4]) + 0.02)
+    return q, out

@@ -32,7 +32,7 @@ import numpy as np
 __all__ = [
     "Workload", "WORKLOADS", "workload", "make_tracks", "make_track_chunk",
     "make_weights", "blob_layout", "blob_size", "round_to_bf16", "TRACK_CHUNK",
-    "KAPPA_GEV_PER_T_M",
+    "KAPPA_GEV_PER_T_M", "readout_layout", "make_readout_weights",
 ]
 
 # pT [GeV] = KAPPA * B [T] * R [m] for a unit-charge particle.
@@ -303,3 +303,28 @@ def split_blob(blob: np.ndarray, n_layers: int, d: int) -> dict:
         o += n
     assert o == blob.size
     return out
+
+
+def readout_layout(d: int):
+    """Blob of the paper's readout head (Sec. Encoder, last paragraph): RMSNorm
+    gain over the 2d end states, a d-wide hidden layer, 35 quantile outputs
+    (seven per parameter, parameter p owning outputs 7p..7p+6)."""
+    return [("ro.norm.g", (2 * d,), 2 * d, "g"), ("ro.W1", (d, 2 * d), 2 * d, "w"), ("ro.b1", (d,), 2 * d, "b"),
+            ("ro.W2", (35, d), d, "w"), ("ro.b2", (35,), d, "b")]
+
+
+def make_readout_weights(w, seed: int | None = None) -> np.ndarray:
+    """float32 blob of the readout head for a workload's width (fp32 values,
+    drawn like the encoder's: N(0, 1/fan_in), U(+-fan_in^-1/2), gains U(0.5, 1.5))."""
+    w = workload(w)
+    rng = np.random.default_rng(w.weight_seed + 100 if seed is None else seed)
+    parts = []
+    for _, shape, fan_in, kind in readout_layout(w.d_model):
+        n = int(np.prod(shape))
+        if kind == "w":
+            parts.append(rng.normal(0.0, fan_in ** -0.5, n))
+        elif kind == "b":
+            parts.append(rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n))
+        else:
+            parts.append(rng.uniform(0.5, 1.5, n))
+    return np.concatenate(parts).astype(np.float32)
