@@ -132,6 +132,25 @@ int32_t tf_max_hits(const tf_weights *w);
 tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                      const tf_weights *w, float *out, hipStream_t stream);
 
+/*
+ * The paper's readout input instead of the pooled head (Sec. Encoder, last
+ * paragraph: the forward state at the outermost hit and the reverse state at
+ * the innermost hit of the last layer, concatenated).  Runs the same encoder
+ * as fit_tracks and stops after the last layer's scans: that layer's output
+ * projection and the pooled head are not evaluated.
+ *
+ * states   device, float32 [n_tracks][2 d]: columns 0 .. d-1 hold the last
+ *          layer's forward scan state at the track's last hit, columns
+ *          d .. 2d-1 its reverse scan state at the track's first hit (both
+ *          before the output projection).  Every row is written; rejected
+ *          tracks (as for fit_tracks) get NaN rows.  Must not overlap the
+ *          inputs.
+ * Other arguments, asynchrony and device errors as for fit_tracks.
+ * Errors: as fit_tracks, and TF_EUNSUPPORTED for a model with no layers.
+ */
+tf_status fit_tracks_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                            const tf_weights *w, float *states, hipStream_t stream);
+
 /* Bits of the sticky device error word. */
 #define TF_DEVERR_EMPTY_TRACK 1   /* a track with zero hits */
 #define TF_DEVERR_TOO_LONG 2      /* a track longer than tf_max_hits */
@@ -187,6 +206,59 @@ tf_status tf_seed_tracks(const float *hits, int64_t n_hits, const int32_t *offse
                                   three are collinear */
 #define TF_SEED_BAD_OFFSETS 4  /* decreasing offsets, or rows outside [0, n_hits) or outside
                                   [offsets[0], offsets[n_tracks]) */
+
+/*
+ * The paper's readout and decode (Sec. Encoder, last paragraph: RMSNorm of the
+ * end states, a two-layer head with hidden width d and SiLU, 35 outputs;
+ * Sec. Losses: seven quantiles per parameter, the median as point estimate;
+ * Sec. Method: the prediction is a correction to the analytic seed).
+ *
+ * Opaque: the head's weights in kernel order on the device.  Owned by the
+ * library.
+ */
+typedef struct tf_readout tf_readout;
+
+/* Number of floats of a readout head blob for width d (0 if invalid):
+ * norm.g[2d], W1[d][2d], b1[d], W2[35][d], b2[35] (row-major [out][in]).
+ * Output 7 p + i of W2 is quantile i of parameter p (d0, z0, phi, theta, q/p
+ * order), the quantiles in increasing order of their levels. */
+size_t tf_readout_blob_size(int32_t d);
+
+/* Copy a readout head blob to the current device.  d: 32, 64, 128 or 256.
+ * host_blob is only read during the call; *out receives a handle freed with
+ * tf_readout_destroy.  Synchronous; allocates device memory.
+ * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d)),
+ * TF_EUNSUPPORTED (other d), TF_ENOMEM, TF_EHIP.  On error *out is NULL. */
+tf_status tf_readout_create(int32_t d, const float *host_blob, size_t n_floats, tf_readout **out);
+
+/* Free a handle (NULL is a no-op).  Synchronises the device first. */
+void tf_readout_destroy(tf_readout *h);
+
+/*
+ * Readout, median and decode of a batch of tracks:
+ *   y = g (.) z / sqrt(mean(z^2) + 1e-6),  h = SiLU(W1 y + b1),
+ *   q = W2 h + b2,  m_p = median(q[7p .. 7p+6]),
+ *   d0, z0, theta: seed + m;  phi: seed + m wrapped to [-pi, pi);
+ *   q/p: seed + m * (|seed| + 0.02 / GeV).
+ * The head runs in fp32 (matrix cores, fp32 accumulation); the decode in fp64.
+ *
+ * states    device, float32 [n_tracks][2d], as written by fit_tracks_states
+ *           (d of the handle).  Read only.
+ * n_tracks  host scalar >= 0.  0 is a no-op returning TF_OK.
+ * seeds     device, float64 [n_tracks][5], as written by tf_seed_tracks.
+ * h         handle from tf_readout_create (same device).
+ * quantiles device, float32 [n_tracks][35] or NULL to skip them: q per track.
+ * out       device, float64 [n_tracks][5]: the decoded d0 [mm], z0 [mm], phi,
+ *           theta, q/p [1/GeV].  Every row is written.  A track whose states
+ *           or seed hold a NaN gets NaN in the affected outputs.
+ * stream    HIP stream (0 = null stream).
+ *
+ * Asynchronous, allocates nothing (graph-capturable).  Outputs must not
+ * overlap the inputs.  Errors: TF_EINVAL (null pointers with n_tracks > 0,
+ * n_tracks < 0), TF_EHIP (launch failure).
+ */
+tf_status tf_decode_tracks(const float *states, int32_t n_tracks, const double *seeds, const tf_readout *h,
+                           float *quantiles, double *out, hipStream_t stream);
 
 /* Static description of a status code. */
 const char *tf_status_string(tf_status s);

@@ -14,7 +14,8 @@ import torch  # noqa: F401  -- load torch's HIP runtime before the library (one 
 
 __all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_size",
            "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS",
-           "TrackfitError", "lib", "seed_tracks", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
+           "TrackfitError", "lib", "seed_tracks", "fit_tracks_states", "Readout", "decode_tracks",
+           "readout_blob_size", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtrackfit.so")
 
@@ -28,7 +29,8 @@ DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS = 1, 2, 4
 SEED_TOO_SHORT, SEED_NO_CIRCLE, SEED_BAD_OFFSETS = 1, 2, 4
 
 EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_max_hits",
-            "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks")
+            "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks", "fit_tracks_states",
+            "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks")
 
 
 class TrackfitError(RuntimeError):
@@ -63,12 +65,22 @@ def lib():
         L.tf_max_hits.argtypes = [vp]
         L.fit_tracks.restype = ctypes.c_int
         L.fit_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, vp]
+        L.fit_tracks_states.restype = ctypes.c_int
+        L.fit_tracks_states.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, vp]
         L.tf_get_device_error.restype = ctypes.c_int
         L.tf_get_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
         L.tf_status_string.restype = ctypes.c_char_p
         L.tf_status_string.argtypes = [ctypes.c_int]
         L.tf_seed_tracks.restype = ctypes.c_int
         L.tf_seed_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, ctypes.c_double, vp, vp, vp, vp]
+        L.tf_readout_blob_size.restype = ctypes.c_size_t
+        L.tf_readout_blob_size.argtypes = [ctypes.c_int32]
+        L.tf_readout_create.restype = ctypes.c_int
+        L.tf_readout_create.argtypes = [ctypes.c_int32, vp, ctypes.c_size_t, ctypes.POINTER(vp)]
+        L.tf_readout_destroy.restype = None
+        L.tf_readout_destroy.argtypes = [vp]
+        L.tf_decode_tracks.restype = ctypes.c_int
+        L.tf_decode_tracks.argtypes = [vp, ctypes.c_int32, vp, vp, vp, vp, vp]
         _lib = L
     return _lib
 
@@ -127,15 +139,8 @@ class Weights:
             pass
 
 
-def fit_tracks(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights, out: torch.Tensor | None = None,
-               n_tracks: int | None = None, stream=None) -> torch.Tensor:
-    """Enqueue one fit of a packed batch on ``stream`` (default: current stream).
-
-    hits    float32 [H, 3] on the GPU; offsets int32 [N+1] on the GPU (absolute
-    row offsets, may start above 0); returns out float32 [N, 5].  ``n_tracks``
-    defaults to offsets.numel() - 1 (a prefix of a longer offsets array may be
-    given instead).
-    """
+def _batch(hits: torch.Tensor, offsets: torch.Tensor, n_tracks: int | None) -> int:
+    """Check a packed batch's tensors; returns the number of tracks."""
     if not (hits.is_cuda and offsets.is_cuda):
         raise ValueError("hits and offsets must be GPU tensors")
     if hits.dtype != torch.float32 or offsets.dtype != torch.int32:
@@ -147,12 +152,42 @@ def fit_tracks(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights, out:
     n = offsets.numel() - 1 if n_tracks is None else int(n_tracks)
     if n < 0 or n + 1 > offsets.numel():
         raise ValueError("n_tracks does not fit the offsets array")
+    return n
+
+
+def _out(out: torch.Tensor | None, n: int, width: int, device, dtype=torch.float32) -> torch.Tensor:
     if out is None:
-        out = torch.empty((n, 5), dtype=torch.float32, device=hits.device)
-    elif not (out.is_cuda and out.dtype == torch.float32 and out.is_contiguous() and out.numel() >= 5 * n):
-        raise ValueError("out must be a contiguous float32 GPU tensor with room for [N, 5]")
+        return torch.empty((n, width), dtype=dtype, device=device)
+    if not (out.is_cuda and out.dtype == dtype and out.is_contiguous() and out.numel() >= width * n):
+        raise ValueError(f"output must be a contiguous {dtype} GPU tensor with room for [N, {width}]")
+    return out
+
+
+def fit_tracks(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights, out: torch.Tensor | None = None,
+               n_tracks: int | None = None, stream=None) -> torch.Tensor:
+    """Enqueue one fit of a packed batch on ``stream`` (default: current stream).
+
+    hits    float32 [H, 3] on the GPU; offsets int32 [N+1] on the GPU (absolute
+    row offsets, may start above 0); returns out float32 [N, 5].  ``n_tracks``
+    defaults to offsets.numel() - 1 (a prefix of a longer offsets array may be
+    given instead).
+    """
+    n = _batch(hits, offsets, n_tracks)
+    out = _out(out, n, 5, hits.device)
     _check(lib().fit_tracks(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, weights.handle,
                             out.data_ptr(), _stream_handle(stream)), "fit_tracks")
+    return out
+
+
+def fit_tracks_states(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights,
+                      out: torch.Tensor | None = None, n_tracks: int | None = None, stream=None) -> torch.Tensor:
+    """Enqueue the encoder up to the last layer's scans; returns float32
+    [N, 2d]: the forward state at each track's last hit, then the reverse
+    state at its first hit (the paper's readout input)."""
+    n = _batch(hits, offsets, n_tracks)
+    out = _out(out, n, 2 * weights.d_model, hits.device)
+    _check(lib().fit_tracks_states(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, weights.handle,
+                                   out.data_ptr(), _stream_handle(stream)), "fit_tracks_states")
     return out
 
 
@@ -204,3 +239,65 @@ def seed_tracks(hits: torch.Tensor, offsets: torch.Tensor, b_tesla: float, featu
                                 seeds.data_ptr(), fptr, flags.data_ptr() if flags is not None else None,
                                 _stream_handle(stream)), "tf_seed_tracks")
     return seeds, feats
+
+
+def readout_blob_size(d: int) -> int:
+    return int(lib().tf_readout_blob_size(int(d)))
+
+
+class Readout:
+    """Device-resident readout head (tf_readout handle) on the current device."""
+
+    def __init__(self, blob, d: int):
+        import numpy as np
+        arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
+        h = ctypes.c_void_p()
+        _check(lib().tf_readout_create(int(d), arr.ctypes.data, arr.size, ctypes.byref(h)), "tf_readout_create")
+        self._h = h
+        self.d = int(d)
+
+    @property
+    def handle(self):
+        return self._h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().tf_readout_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def decode_tracks(states: torch.Tensor, seeds: torch.Tensor, readout: Readout, quantiles: bool = False,
+                  out: torch.Tensor | None = None, q: torch.Tensor | None = None, stream=None):
+    """Enqueue the readout head, the medians and the seed-anchored decode.
+
+    states float32 [N, 2d] (fit_tracks_states), seeds float64 [N, 5]
+    (seed_tracks), both on the GPU.  Returns (out float64 [N, 5], quantiles
+    float32 [N, 35] or None).
+    """
+    if not (states.is_cuda and seeds.is_cuda):
+        raise ValueError("states and seeds must be GPU tensors")
+    if states.dtype != torch.float32 or seeds.dtype != torch.float64:
+        raise TypeError("states must be float32 and seeds float64")
+    if not (states.is_contiguous() and seeds.is_contiguous()):
+        raise ValueError("states and seeds must be contiguous")
+    n = states.shape[0]
+    if states.dim() != 2 or states.shape[1] != 2 * readout.d:
+        raise ValueError(f"states must have shape [N, {2 * readout.d}]")
+    if seeds.numel() < 5 * n:
+        raise ValueError("seeds must hold [N, 5]")
+    out = _out(out, n, 5, states.device, torch.float64)
+    qptr = None
+    if quantiles:
+        q = _out(q, n, 35, states.device)
+        qptr = q.data_ptr()
+    else:
+        q = None
+    _check(lib().tf_decode_tracks(states.data_ptr(), n, seeds.data_ptr(), readout.handle, qptr, out.data_ptr(),
+                                  _stream_handle(stream)), "tf_decode_tracks")
+    return out, q

@@ -47,6 +47,7 @@
 #include <cstdint>
 #include <cstring>
 #include <new>
+#include <type_traits>
 #include <vector>
 
 #include "trackfit.h"
@@ -313,7 +314,12 @@ __device__ __forceinline__ void wait_vmcnt() {
     __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
 }
 
-template <int D, int OP, int HT_>
+// STATES: instead of the pooled head, write each track's last-layer end states
+// (the paper's own readout input): out is then [n_tracks][2d], the forward
+// state at the track's last hit in columns 0..d-1 and the reverse state at its
+// first hit in columns d..2d-1.  The last layer's output projection and the
+// head, whose results nothing reads in this form, are skipped.
+template <int D, int OP, int HT_, bool STATES>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
                           amdgpu_waves_per_eu(KCfg<D, OP, HT_>::WAVES / 4, KCfg<D, OP, HT_>::WAVES / 4)))
 void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
@@ -325,6 +331,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
     constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK, KPB = C::KPB, NCH = C::NCH;
     constexpr int MAXTR = C::MAXTR;
+    constexpr int OUTW = STATES ? 2 * D : 5;  // floats per output row
 
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
     const int lane = threadIdx.x & 63;
@@ -418,7 +425,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                            (long_m ? TF_DEVERR_TOO_LONG : 0);
                 if (fresh && (bad || empty || too_long)) {
 #pragma unroll
-                    for (int e = 0; e < 5; ++e) out[(size_t)idx * 5 + e] = qnan;
+                    for (int e = 0; e < OUTW; ++e) out[(size_t)idx * OUTW + e] = qnan;
                 }
                 taken |= unsigned(bad_m | empty_m | long_m);
             }
@@ -449,6 +456,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         // ---- tile metadata: the tile's tracks in window order, on consecutive
         // tile rows; start/end masks per stream
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
+        unsigned st0 = 0, st1 = 0;  // per stream: tile rows that start a track
         f32x16 r[MT][HT];  // the residual stream (a wave without a tile keeps zeros)
         if constexpr (C::TIGHT) {
 #pragma unroll
@@ -475,12 +483,16 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 t_off[j] = off;
                 t_id[j] = t + lane;
             }
-            unsigned long long smask = 0;
+            unsigned long long smask = 0;  // tile rows that start a track
             for (unsigned m = sel; m; m &= m - 1u) smask |= 1ull << __builtin_amdgcn_readlane(row0, __builtin_ctz(m));
             const unsigned long long valid = n >= 64 ? ~0ull : ((1ull << n) - 1);
             const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
             const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
             const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
+            if constexpr (STATES) {
+                st0 = unsigned(smask) & spm;
+                st1 = unsigned(smask >> SP) & spm;
+            }
             sb0 = unsigned(vstart) & spm;
             sb1 = unsigned(vstart >> SP) & spm;
             eb0 = unsigned(emask) & spm;
@@ -510,8 +522,10 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             }
         }
 
-        // ---- layers
-        for (int l = 0; l < P.n_layers; ++l) {
+        // ---- layers.  With STATES the last layer is a copy of its own (LAST): it
+        // stops after the scans, so the residual is dead from its norm on.
+        auto layer = [&](auto last_c) {
+            constexpr bool LAST = decltype(last_c)::value;
             FT yf[HT][KS1];
             if constexpr (C::TIGHT) {
 #pragma unroll
@@ -639,17 +653,52 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         float f = hh ? __uint_as_float(xs[0]) : 0.f;  // Fs[SP - 1] of stream 0
                         float b = hh ? 0.f : __uint_as_float(xs[1]);  // Bs[0] of stream 1
                         wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
+                        if constexpr (!LAST) {
 #pragma unroll
-                        for (int i = 0; i < SP; ++i) {
-                            const int pb = SP - 1 - i;
-                            f = fmaf(CFf[i], f, AX[i]);
-                            b = fmaf(CFb[pb], b, AX[pb]);
-                            Fs[i] = f;
-                            Bs[pb] = b;
-                            if (i & 1) {
-                                store_fb_pair<C, FE>(ws, i - 1, Fs[i - 1], Fs[i], 0, hh, cc);
-                                store_fb_pair<C, FE>(ws, pb, Bs[pb], Bs[pb + 1], 32, hh, cc);
+                            for (int i = 0; i < SP; ++i) {
+                                const int pb = SP - 1 - i;
+                                f = fmaf(CFf[i], f, AX[i]);
+                                b = fmaf(CFb[pb], b, AX[pb]);
+                                Fs[i] = f;
+                                Bs[pb] = b;
+                                if (i & 1) {
+                                    store_fb_pair<C, FE>(ws, i - 1, Fs[i - 1], Fs[i], 0, hh, cc);
+                                    store_fb_pair<C, FE>(ws, pb, Bs[pb], Bs[pb + 1], 32, hh, cc);
+                                }
                             }
+                        } else {
+                            // Last layer, end states only, in fp32: the forward state at
+                            // a track's last row goes to scratch row j (its index in the
+                            // tile), the reverse state at its first row to row MAXTR + j;
+                            // every other position writes a dummy row.  The track of a
+                            // row is the number of track starts up to it, less one:
+                            // counted up along the forward scan and down along the
+                            // reverse one.
+                            // (the asm keeps the compiler from hoisting every position's
+                            // row out of the chunk loop into registers)
+                            unsigned sw = hh ? st1 : st0;  // this stream's track starts
+                            unsigned ew = hh ? eb1 : eb0;  // and ends
+                            int jf = hh ? __builtin_popcount(st0) - 1 : -1;
+                            int jr = jf + __builtin_popcount(sw);
+                            asm volatile("" : "+v"(sw), "+v"(ew), "+v"(jf), "+v"(jr));
+                            constexpr int DUMMY = CAP * C::STS;  // first pooled row, unused here
+#pragma unroll
+                            for (int i = 0; i < SP; ++i) {
+                                const int pb = SP - 1 - i;
+                                f = fmaf(CFf[i], f, AX[i]);
+                                b = fmaf(CFb[pb], b, AX[pb]);
+                                const unsigned si = (sw >> i) & 1u, ei = (ew >> i) & 1u, sr = (sw >> pb) & 1u;
+                                jf += int(si);
+                                // (selects written as products, which stay branch-free)
+                                stage[DUMMY + cc + int(ei) * (jf * C::STS - DUMMY)] = f;
+                                stage[DUMMY + cc + int(sr) * ((MAXTR + jr) * C::STS - DUMMY)] = b;
+                                jr -= int(sr);
+                                __builtin_amdgcn_sched_barrier(0);  // one position at a time
+                            }
+                            wave_lds_sync();
+                            // rows of the tile's tracks out, f in the low lane half, b in the high
+                            for (int j = 0; j < k; ++j)
+                                out[(size_t)t_id[j] * OUTW + hh * D + 32 * ch + cc] = stage[(hh * MAXTR + j) * C::STS + cc];
                         }
                     }
                 }
@@ -658,7 +707,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 // ---- stage: output projection of this chunk, K split over chunks.  The
                 // 16-bit modes accumulate straight into the residual registers; the
                 // fp32 model sums the chunk in fresh accumulators and adds it once.
-                if (work) {
+                if (work && !LAST) {
                     const char *sl = slot() + C::G2_OFF;
                     if constexpr (C::MERGE) wave_lds_sync();  // this wave's [f; b] stores are visible
                     __builtin_amdgcn_s_setprio(1);
@@ -713,6 +762,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 __builtin_amdgcn_s_setprio(0);
                 advance(false);
             }
+        };
+        if constexpr (STATES) {
+            for (int l = 0; l + 1 < P.n_layers; ++l) layer(std::false_type{});
+            layer(std::true_type{});
+        } else {
+            for (int l = 0; l < P.n_layers; ++l) layer(std::false_type{});
         }
 
         // ---- head, transposed: hid^T = W1 p^T (hidden units on rows, tracks on
@@ -738,7 +793,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // unrolled, so that the residual block pooled at each step is a fixed register block
 #pragma unroll
             for (int j = 0; j < C::NH1; ++j) {
-                if (work) {
+                if (work && !STATES) {
                     const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
                     for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
@@ -834,7 +889,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
             // operand, output row q of column cc is output q of track cc
             if constexpr (C::HEAD16) {
-              if (work) {
+              if (work && !STATES) {
                 // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
                 // stored W2 fragments follow that order); output rows 4 hg + i
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
@@ -866,7 +921,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     }
                 }
               }
-            } else if (work) {
+            } else if (work && !STATES) {
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
                 const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
                 f32x16 o;
@@ -1177,7 +1232,7 @@ extern "C" void tf_weights_destroy(tf_weights *w) {
 extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
 
 namespace {
-template <int D, int OP, int HT>
+template <int D, int OP, int HT, bool STATES>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                   const tf_weights *w, float *out, hipStream_t stream) {
     using C = KCfg<D, OP, HT>;
@@ -1188,30 +1243,44 @@ hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int
     const long long cap = (long long)w->cu_count;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, STATES>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
                        hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, w->err);
     return hipGetLastError();
 }
 
-template <int D, int OP>
+template <int D, int OP, bool STATES>
 hipError_t launch_ht(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                      const tf_weights *w, float *out, hipStream_t stream) {
     if constexpr (D <= 128) {
-        if (w->max_hits == 64) return launch<D, OP, 2>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        if (w->max_hits == 64) return launch<D, OP, 2, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
     }
-    return launch<D, OP, 1>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    return launch<D, OP, 1, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
 }
 
-template <int D>
+template <int D, bool STATES>
 hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                     const tf_weights *w, float *out, hipStream_t stream) {
     switch (w->dtype) {
-        case TF_BF16: return launch_ht<D, OP_BF16>(hits, n_hits, offsets, n_tracks, w, out, stream);
-        case TF_BF16_F16ACT: return launch_ht<D, OP_F16>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16: return launch_ht<D, OP_BF16, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16_F16ACT: return launch_ht<D, OP_F16, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
         default:
-            if constexpr (D <= 128) return launch_ht<D, OP_F32>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            if constexpr (D <= 128) return launch_ht<D, OP_F32, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
             return hipErrorNotSupported;
     }
+}
+
+template <bool STATES>
+tf_status launch_any(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                     const tf_weights *w, float *out, hipStream_t stream) {
+    hipError_t e;
+    switch (w->d) {
+        case 32: e = launch_d<32, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 64: e = launch_d<64, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 128: e = launch_d<128, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 256: e = launch_d<256, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        default: return TF_EUNSUPPORTED;
+    }
+    return e == hipSuccess ? TF_OK : TF_EHIP;
 }
 }  // namespace
 
@@ -1220,15 +1289,16 @@ extern "C" tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t
     if (!w || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
     if (n_tracks == 0) return TF_OK;
     if (!offsets || !out || (!hits && n_hits > 0)) return TF_EINVAL;
-    hipError_t e;
-    switch (w->d) {
-        case 32: e = launch_d<32>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 64: e = launch_d<64>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 128: e = launch_d<128>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 256: e = launch_d<256>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        default: return TF_EUNSUPPORTED;
-    }
-    return e == hipSuccess ? TF_OK : TF_EHIP;
+    return launch_any<false>(hits, n_hits, offsets, n_tracks, w, out, stream);
+}
+
+extern "C" tf_status fit_tracks_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                                       const tf_weights *w, float *states, hipStream_t stream) {
+    if (!w || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
+    if (w->n_layers < 1) return TF_EUNSUPPORTED;  // no scan, no states
+    if (n_tracks == 0) return TF_OK;
+    if (!offsets || !states || (!hits && n_hits > 0)) return TF_EINVAL;
+    return launch_any<true>(hits, n_hits, offsets, n_tracks, w, states, stream);
 }
 
 extern "C" tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear) {

@@ -78,3 +78,21 @@ def test_argument_checks_without_gpu(tf):
     assert L.tf_seed_tracks(None, 0, None, 0, 0.0, None, None, None, None) == tf.TF_EINVAL  # field
     assert L.tf_seed_tracks(None, 0, None, 0, float("nan"), None, None, None, None) == tf.TF_EINVAL
     assert L.tf_seed_tracks(None, 10, None, 5, 2.0, None, None, None, None) == tf.TF_EINVAL  # null pointers
+
+
+def test_readout_and_states_argument_checks_without_gpu(tf):
+    import oracle
+    L = tf.lib()
+    for d in (32, 64, 128, 256):
+        assert L.tf_readout_blob_size(d) == oracle.readout_blob_size(d) == 2 * d + 2 * d * d + d + 35 * d + 35
+    assert L.tf_readout_blob_size(0) == 0
+    h = ctypes.c_void_p()
+    blob = (ctypes.c_float * 10)()
+    assert L.tf_readout_create(128, blob, 10, ctypes.byref(h)) == tf.TF_EINVAL          # wrong size
+    assert L.tf_readout_create(128, None, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL
+    assert L.tf_readout_create(128, blob, 10, None) == tf.TF_EINVAL
+    assert L.tf_readout_create(96, blob, L.tf_readout_blob_size(96), ctypes.byref(h)) == tf.TF_EUNSUPPORTED
+    assert h.value is None
+    L.tf_readout_destroy(None)   # no-op
+    assert L.tf_decode_tracks(None, 0, None, None, None, None, None) == tf.TF_EINVAL    # null handle
+    assert L.fit_tracks_states(None, 0, None, 0, None, None, None) == tf.TF_EINVAL      # null handle

@@ -1,0 +1,287 @@
+"""GPU parity of the paper's readout path against the fp64 oracle, element by
+element: the encoder's last-layer end states (fit_tracks_states), the readout
+head with its medians and seed-anchored decode (tf_decode_tracks) on the
+oracle's own states, and the chain seed -> states -> decode end to end, plus
+the edge cases (length 1 and maximum, ragged batches, rejected tracks, NaN
+inputs, tile independence).
+"""
+import dataclasses
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import tracksynth as ts
+from tests.parity import TOL
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+THREADS = int(os.environ.get("ORACLE_THREADS", "0"))
+N_STATES = {"tiny_d32_fp32": 256, "d128x4_fp32_65k": 2048, "d256x6_bf16_1m": 512,
+            "long64_d128x4_bf16_200k": 512, "deploy_d128x4_bf16_8m": 2048}
+# The head and the decode run in fp32 on fp32 states; against the fp64 oracle
+# on the same (fp32-valued) states the differences are fp32 roundings.  A
+# quantile is the end of two dot products (2d terms, then d), so its rounding
+# is bounded by about u * (2d + d) relative to the sum of the terms' magnitudes
+# (u = 2^-24), which for these random heads is a few times the column's scale:
+# the quantiles are held to u * 2d * 2 per column.  The decoded parameters are
+# held to the fp32 model's output tolerance.
+DECODE_TOL = 1e-5
+
+
+def quantile_tol(d):
+    return 2.0 ** -24 * (2 * d) * 2
+
+
+@pytest.fixture(scope="module")
+def tf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32479_amd as tf
+    return tf
+
+
+def colerr(g, r):
+    """Per column: max |g - r| / max(|r|, rms of the column); NaN patterns must match."""
+    g = np.asarray(g, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    assert g.shape == r.shape
+    assert np.array_equal(np.isnan(g), np.isnan(r))
+    ok = ~np.isnan(r).any(axis=1)
+    g, r = g[ok], r[ok]
+    if r.shape[0] == 0:
+        return np.zeros(r.shape[1])
+    rms = np.sqrt(np.mean(r ** 2, axis=0))
+    return np.max(np.abs(g - r) / np.maximum(np.abs(r), np.maximum(rms, 1e-300)), axis=0)
+
+
+def state_err(g, r):
+    """Largest |g - r| over a track's 2d end states, in units of that track's
+    state RMS: the scale the readout's RMSNorm divides by, hence the error
+    that reaches the head.  NaN rows must match."""
+    g = np.asarray(g, dtype=np.float64)
+    r = np.asarray(r, dtype=np.float64)
+    assert g.shape == r.shape
+    assert np.array_equal(np.isnan(g), np.isnan(r))
+    ok = ~np.isnan(r).any(axis=1)
+    g, r = g[ok], r[ok]
+    if r.shape[0] == 0:
+        return 0.0
+    rms = np.sqrt(np.mean(r ** 2, axis=1, keepdims=True))
+    return float(np.max(np.abs(g - r) / rms))
+
+
+def wrap_phi(g, r):
+    """phi of g brought to the branch of r (2 pi apart is the same angle)."""
+    g = np.array(g, dtype=np.float64)
+    d = g[:, 2] - r[:, 2]
+    g[:, 2] -= np.round(np.nan_to_num(d) / (2 * np.pi)) * 2 * np.pi
+    return g
+
+
+def _weights(tf, w, max_hits=None):
+    blob = ts.make_weights(w)
+    W = tf.Weights(blob, w.n_layers, w.d_model, tf.MODE_FOR_WEIGHTS[w.dtype],
+                   w.len_max if max_hits is None else max_hits)
+    return W, blob
+
+
+def _states(tf, W, hits, offs, n_tracks=None):
+    h = torch.from_numpy(np.ascontiguousarray(hits, dtype=np.float32)).cuda()
+    o = torch.from_numpy(np.ascontiguousarray(offs, dtype=np.int32)).cuda()
+    s = tf.fit_tracks_states(h, o, W, n_tracks=n_tracks)
+    torch.cuda.synchronize()
+    return s.cpu().numpy()
+
+
+def _ref_states(w, hits, offs, blob):
+    return oracle.track_states(hits, offs, blob, w.n_layers, w.d_model, n_threads=THREADS)
+
+
+@pytest.mark.parametrize("name", list(ts.WORKLOADS))
+def test_states_match_oracle(tf, name):
+    w = ts.WORKLOADS[name]
+    print(f"[states] {name} n={N_STATES[name]}", flush=True)
+    W, blob = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=N_STATES[name])
+    g = _states(tf, W, hits, offs)
+    r = _ref_states(w, hits, offs, blob)
+    assert g.shape == (N_STATES[name], 2 * w.d_model)
+    e = state_err(g, r)
+    print(f"[states] {name}: max err {e:.3g} of the track's state rms", flush=True)
+    assert e <= TOL[w.dtype]
+    assert tf.device_error(W) == 0
+
+
+@pytest.mark.parametrize("name,L,max_hits", [("deploy_d128x4_bf16_8m", 1, 32), ("deploy_d128x4_bf16_8m", 32, 32),
+                                             ("deploy_d128x4_bf16_8m", 64, 64), ("d128x4_fp32_65k", 1, 64),
+                                             ("d128x4_fp32_65k", 64, 64), ("tiny_d32_fp32", 64, 64),
+                                             ("d256x6_bf16_1m", 32, 32)])
+def test_states_fixed_lengths(tf, name, L, max_hits):
+    """Length 1 (forward and reverse state of one step coincide) and the maximum."""
+    w = dataclasses.replace(ts.WORKLOADS[name], len_min=L, len_max=L, n_det_layers=max(L, 8))
+    print(f"[states-fixed] {name} L={L} max_hits={max_hits}", flush=True)
+    W, blob = _weights(tf, w, max_hits=max_hits)
+    hits, offs = ts.make_tracks(w, n_tracks=300)
+    g = _states(tf, W, hits, offs)
+    r = _ref_states(w, hits, offs, blob)
+    assert state_err(g, r) <= TOL[w.dtype]
+    if L == 1:
+        d = w.d_model
+        assert np.array_equal(g[:, :d], g[:, d:])
+
+
+@pytest.mark.parametrize("name,max_hits", [("deploy_d128x4_bf16_8m", 32), ("deploy_d128x4_bf16_8m", 64),
+                                           ("d128x4_fp32_65k", 64)])
+def test_states_ragged_small_batches_and_bad_tracks(tf, name, max_hits):
+    w0 = ts.WORKLOADS[name]
+    print(f"[states-ragged] {name} max_hits={max_hits}", flush=True)
+    W, blob = _weights(tf, w0, max_hits=max_hits)
+    w = dataclasses.replace(w0, len_min=1, len_max=max_hits, n_det_layers=max_hits)
+    hits, offs = ts.make_tracks(w, n_tracks=700)
+    r_all = _ref_states(w, hits, offs, blob)
+    for n in (1, 2, 33, 700):
+        g = _states(tf, W, hits, offs[: n + 1])
+        assert state_err(g, r_all[:n]) <= TOL[w.dtype], n
+    # track 5 emptied, track 9 one hit too long: NaN rows, neighbours unchanged
+    Lk = np.diff(offs)
+    Lk[5], Lk[9] = 0, max_hits + 1
+    rows = []
+    for i in range(700):
+        src = np.arange(offs[i], offs[i + 1])
+        rows.append(np.resize(src, Lk[i]) if Lk[i] else src[:0])
+    h2 = hits[np.concatenate(rows)]
+    o2 = np.concatenate([[0], np.cumsum(Lk)]).astype(np.int32)
+    g = _states(tf, W, h2, o2)
+    assert np.all(np.isnan(g[[5, 9]]))
+    good = np.ones(700, bool)
+    good[[5, 9]] = False
+    assert state_err(g[good], r_all[good]) <= TOL[w.dtype]
+    assert tf.device_error(W) == (tf.DEVERR_EMPTY_TRACK | tf.DEVERR_TOO_LONG)
+
+
+def test_states_do_not_depend_on_tile_neighbours(tf):
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, _ = _weights(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=3000)
+    a = _states(tf, W, hits, offs)
+    assert np.array_equal(a, _states(tf, W, hits, offs))
+    perm = np.random.default_rng(3).permutation(3000)
+    L = np.diff(offs)
+    hp = np.concatenate([hits[offs[i]:offs[i + 1]] for i in perm])
+    op = np.concatenate([[0], np.cumsum(L[perm])]).astype(np.int32)
+    assert np.array_equal(_states(tf, W, hp, op), a[perm])
+
+
+def _decode(tf, R, states, seeds, quantiles=True):
+    st = torch.from_numpy(np.ascontiguousarray(states, dtype=np.float32)).cuda()
+    sd = torch.from_numpy(np.ascontiguousarray(seeds, dtype=np.float64)).cuda()
+    out, q = tf.decode_tracks(st, sd, R, quantiles=quantiles)
+    torch.cuda.synchronize()
+    return out.cpu().numpy(), (q.cpu().numpy() if q is not None else None)
+
+
+@pytest.mark.parametrize("name,n", [("deploy_d128x4_bf16_8m", 1000), ("tiny_d32_fp32", 77),
+                                    ("d256x6_bf16_1m", 300), ("deploy_d128x4_bf16_8m", 1),
+                                    ("deploy_d128x4_bf16_8m", 33)])
+def test_decode_matches_oracle_on_the_same_states(tf, name, n):
+    """The oracle's states (rounded to fp32, as the library takes them) and
+    seeds in; the 35 quantiles and the decoded parameters compared."""
+    w = ts.WORKLOADS[name]
+    d = w.d_model
+    print(f"[decode] {name} n={n}", flush=True)
+    hits, offs = ts.make_tracks(w, n_tracks=n)
+    blob = ts.make_weights(w)
+    st = _ref_states(w, hits, offs, blob).astype(np.float32)
+    seeds, _, bad = oracle.seed_tracks(hits, offs, w.b_field, features=False)
+    assert bad == 0
+    hb = ts.make_readout_weights(w)
+    R = tf.Readout(hb, d)
+    g_out, g_q = _decode(tf, R, st, seeds)
+    r_q, r_out = oracle.readout_tracks(st.astype(np.float64), seeds, hb, d)
+    eq = colerr(g_q, r_q)
+    eo = colerr(wrap_phi(g_out, r_out), r_out)
+    print(f"[decode] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
+    assert eq.max() <= quantile_tol(d) and eo.max() <= DECODE_TOL
+    # without the quantile output the decode is the same, bit for bit
+    g2, q2 = _decode(tf, R, st, seeds, quantiles=False)
+    assert q2 is None and np.array_equal(g2, g_out)
+
+
+def test_decode_median_and_decode_rules_on_a_planted_head(tf):
+    """A head whose quantiles are known in closed form: W1 = 0 and W2 = 0, so
+    q = b2 for every track; the seven values of each parameter are planted
+    out of order, the decode then adds their middle value to the seed."""
+    d = 32
+    hb = np.zeros(oracle.readout_blob_size(d), np.float32)
+    hb[: 2 * d] = 1.0
+    b2 = hb[-35:]
+    rng = np.random.default_rng(8)
+    meds = np.array([0.25, -1.5, 3.0, 0.125, -0.75])
+    for p in range(5):
+        v = np.sort(rng.uniform(-4, 4, 7))
+        b2[7 * p:7 * p + 7] = rng.permutation(v)
+        meds[p] = float(np.sort(b2[7 * p:7 * p + 7])[3])   # as stored (float32)
+    R = tf.Readout(hb, d)
+    n = 40
+    states = rng.normal(size=(n, 2 * d)).astype(np.float32)
+    seeds = np.stack([rng.uniform(-1, 1, n), rng.uniform(-50, 50, n), rng.uniform(-np.pi, np.pi, n),
+                      rng.uniform(0.2, 2.9, n), rng.uniform(-1, 1, n)], axis=1)
+    out, q = _decode(tf, R, states, seeds)
+    assert np.array_equal(q, np.tile(b2, (n, 1)))
+    exp = seeds.copy()
+    exp[:, [0, 1, 3]] += meds[[0, 1, 3]]
+    exp[:, 2] = (seeds[:, 2] + meds[2] + np.pi) % (2 * np.pi) - np.pi
+    exp[:, 4] = seeds[:, 4] + meds[4] * (np.abs(seeds[:, 4]) + 0.02)
+    assert np.all(out[:, 2] >= -np.pi) and np.all(out[:, 2] < np.pi)
+    assert np.allclose(out, exp, rtol=1e-12, atol=1e-12)
+
+
+def test_decode_nan_inputs_stay_local(tf):
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    d = w.d_model
+    rng = np.random.default_rng(4)
+    n = 100
+    st = rng.normal(size=(n, 2 * d)).astype(np.float32)
+    seeds = np.stack([rng.uniform(-1, 1, n), rng.uniform(-50, 50, n), rng.uniform(-3, 3, n),
+                      rng.uniform(0.2, 2.9, n), rng.uniform(-1, 1, n)], axis=1)
+    st[7] = np.nan          # a rejected track's states
+    seeds[40] = np.nan      # a track without a seed
+    hb = ts.make_readout_weights(w)
+    R = tf.Readout(hb, d)
+    out, q = _decode(tf, R, st, seeds)
+    assert np.all(np.isnan(out[[7, 40]])) and np.all(np.isnan(q[7]))
+    assert np.all(np.isfinite(q[40]))
+    good = np.ones(n, bool)
+    good[[7, 40]] = False
+    assert np.all(np.isfinite(out[good]))
+    r_q, r_out = oracle.readout_tracks(st[good].astype(np.float64), seeds[good], hb, d)
+    assert colerr(q[good], r_q).max() <= quantile_tol(d)
+    assert colerr(wrap_phi(out[good], r_out), r_out).max() <= DECODE_TOL
+
+
+@pytest.mark.parametrize("name", ["deploy_d128x4_bf16_8m", "d128x4_fp32_65k"])
+def test_seed_states_decode_end_to_end(tf, name):
+    """hits -> (seed, end states) -> readout and decode, all on the GPU, against
+    the oracle's chain; the encoder's tolerance carries through the head."""
+    w = ts.WORKLOADS[name]
+    print(f"[chain] {name}", flush=True)
+    W, blob = _weights(tf, w)
+    hb = ts.make_readout_weights(w)
+    R = tf.Readout(hb, w.d_model)
+    hits, offs = ts.make_tracks(w, n_tracks=1500)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    seeds, _ = tf.seed_tracks(h, o, w.b_field, features=False)
+    states = tf.fit_tracks_states(h, o, W)
+    out, q = tf.decode_tracks(states, seeds, R, quantiles=True)
+    torch.cuda.synchronize()
+    r_seeds, _, _ = oracle.seed_tracks(hits, offs, w.b_field, features=False)
+    r_q, r_out = oracle.readout_tracks(_ref_states(w, hits, offs, blob), r_seeds, hb, w.d_model)
+    eq = colerr(q.cpu().numpy(), r_q)
+    eo = colerr(wrap_phi(out.cpu().numpy(), r_out), r_out)
+    print(f"[chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
+    # the quantiles carry the head's own fp32 rounding on top of the encoder's
+    assert eq.max() <= max(TOL[w.dtype], quantile_tol(w.d_model)) and eo.max() <= TOL[w.dtype]
