@@ -9,6 +9,11 @@ the timed region.  Prints one JSON line.
 
 ``--path seed`` instead times the analytic three-hit seed with its per-hit
 residual features (tf_seed_tracks) over the same tracks, one call per step.
+
+``--path readout`` times the paper's readout path per batch: the seed, the
+encoder up to the last layer's end states (fit_tracks_states), and the
+35-quantile head with its medians and seed-anchored decode (tf_decode_tracks),
+three launches per batch, the step again captured in one HIP graph.
 """
 import argparse
 import json
@@ -200,6 +205,157 @@ def bench_seed(args, w, hits, offs):
     print(json.dumps(res), flush=True)
 
 
+READOUT_METRIC = ("tracks/sec (seed + encoder end states + 35-quantile readout, median, decode) on 1 MI355X; "
+                  "MFMA util vs peak")
+
+
+def states_algorithmic_flops(n_layers, d, n_hits):
+    """Encoder up to the last layer's scans: 8 d^2 per hit for each layer but
+    the last, 4 d^2 per hit for the last (candidate and gate projections; its
+    merge is not evaluated), 6 d per hit for the embedding."""
+    return 8.0 * d * d * (n_layers - 1) * n_hits + 4.0 * d * d * n_hits + 6.0 * d * n_hits
+
+
+def readout_algorithmic_flops(d, n_tracks):
+    """Per track: 2 * d * 2d for W1, 2 * 35 * d for W2."""
+    return (4.0 * d * d + 70.0 * d) * n_tracks
+
+
+def readout_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
+    """Time the oracle's chain (seed, end states, readout and decode) on a
+    bounded, seeded sample of the same tracks."""
+    import oracle
+    n_all = offs.size - 1
+    rng = np.random.default_rng(7)
+
+    def run(sel):
+        L = offs[sel + 1] - offs[sel]
+        h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+        o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+        t0 = time.perf_counter()
+        seeds, _, _ = oracle.seed_tracks(h, o, w.b_field, features=False)
+        st = oracle.track_states(h, o, blob, w.n_layers, w.d_model, n_threads=threads)
+        _, out = oracle.readout_tracks(st, seeds, hb, w.d_model)
+        return out, time.perf_counter() - t0
+
+    idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
+    _, dt = run(idx)
+    n = int(min(n_all, max(256, 256 * seconds / max(dt, 1e-3))))
+    sel = np.sort(rng.choice(n_all, size=n, replace=False))
+    ref, dt = run(sel)
+    g = gpu_out[sel].copy()
+    g[:, 2] -= np.round((g[:, 2] - ref[:, 2]) / (2 * np.pi)) * 2 * np.pi
+    rms = np.sqrt(np.mean(ref ** 2, axis=0))
+    err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), rms)))
+    return {"value": n / dt, "unit": "tracks/s", "cores": oracle.threads(threads), "kind": "oracle",
+            "sample": f"{n} tracks drawn without replacement (seed 7) from the {n_all}-track workload, "
+                      f"fp64 C oracle (seed, end states, readout, decode), {dt:.1f} s wall",
+            "parity_max_col_err_on_sample": err}
+
+
+def bench_readout(args, w, hits, offs, mode, batch):
+    import torch
+    import paper_2609_32479_amd as tf
+    dev = torch.device("cuda:0")
+    h = torch.from_numpy(hits).to(dev)
+    o = torch.from_numpy(offs).to(dev)
+    n_tracks = offs.size - 1
+    n_hits = int(offs[-1] - offs[0])
+    d = w.d_model
+    blob = ts.make_weights(w)
+    hb = ts.make_readout_weights(w)
+    W = tf.Weights(blob, w.n_layers, d, mode, max_hits=args.max_hits or w.len_max)
+    R = tf.Readout(hb, d, mode)
+    seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
+    out = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
+    states = torch.empty((batch, 2 * d), dtype=torch.float32, device=dev)  # reused by every batch
+    starts = list(range(0, n_tracks, batch))
+
+    def one(s0, stream):
+        n = min(batch, n_tracks - s0)
+        tf.seed_tracks(h, o[s0:], w.b_field, features=False, seeds=seeds[s0:], n_tracks=n, stream=stream)
+        tf.fit_tracks_states(h, o[s0:], W, out=states, n_tracks=n, stream=stream)
+        tf.decode_tracks(states[:n], seeds[s0:s0 + n], R, out=out[s0:], stream=stream)
+
+    def step(stream=None):
+        for s0 in starts:
+            one(s0, stream)
+
+    torch.cuda.synchronize()
+    step()
+    torch.cuda.synchronize()
+    # per-launch time of the dominant kernel (the encoder), eager, events on its stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in starts]
+    for (a, b), s0 in zip(ev, starts):
+        a.record()
+        tf.fit_tracks_states(h, o[s0:], W, out=states, n_tracks=min(batch, n_tracks - s0))
+        b.record()
+    torch.cuda.synchronize()
+    launch_ms = np.array([a.elapsed_time(b) for a, b in ev])
+
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            step(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                step(side)
+        torch.cuda.synchronize()
+
+    def run_step():
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        run_step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    flags = tf.device_error(W)
+    gpu_out = out.cpu().numpy()
+    per_launch_flops = states_algorithmic_flops(w.n_layers, d, n_hits) / len(starts)
+    kernel_ms = float(launch_ms.mean())
+    achieved = per_launch_flops / (kernel_ms / 1e3) / 1e12
+    peak = PEAK_TFLOPS[mode]
+    res = {
+        "metric": READOUT_METRIC, "value": n_tracks / (ms_per_step / 1e3), "unit": "tracks/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None,
+        "dtype": {"fp32": "f32", "bf16": "bf16",
+                  "bf16_f16act": "bf16 weights, f16 activations, f32 accumulate"}[mode]
+                 + ("; head f32" if mode == "fp32" else "; head bf16 weights x split-bf16 activations")
+                 + ", seed and decode f64",
+        "data": "synthetic helix tracks (2 T solenoid, seeded), random-init weights",
+        "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
+                   "launches_per_call": 3, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": d, "mode": mode,
+                   "max_hits": W.max_hits, "hip_graph": graph is not None},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None, "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
+                     "flops_per_launch": per_launch_flops},
+        "readout_flops_per_step": readout_algorithmic_flops(d, n_tracks),
+        "host_wall_s": wall,
+        "device_error_flags": flags,
+        "finite_outputs": bool(np.isfinite(gpu_out).all()),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = readout_cpu_baseline(w, blob, hb, hits, offs, args.cpu_seconds, args.cpu_threads,
+                                                   gpu_out)
+    if args.copy_calibration:
+        copy_calibration(dev)
+    print(json.dumps(res), flush=True)
+
+
 def copy_calibration(dev):
     """A plain elementwise device copy of known size, for scaling HBM counters."""
     import torch
@@ -225,8 +381,9 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
-    ap.add_argument("--path", default="encoder", choices=["encoder", "seed"],
-                    help="encoder: fit_tracks (default); seed: tf_seed_tracks with features")
+    ap.add_argument("--path", default="encoder", choices=["encoder", "seed", "readout"],
+                    help="encoder: fit_tracks (default); seed: tf_seed_tracks with features; "
+                         "readout: seed + fit_tracks_states + tf_decode_tracks")
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"after the timed region, run a plain {COPY_MIB} MiB device copy (for counter calibration)")
     args = ap.parse_args()
@@ -252,6 +409,9 @@ def main():
           file=sys.stderr, flush=True)
     if args.path == "seed":
         bench_seed(args, w, hits, offs)
+        return
+    if args.path == "readout":
+        bench_readout(args, w, hits, offs, mode, batch)
         return
     blob = ts.make_weights(w)
 

@@ -225,11 +225,17 @@ typedef struct tf_readout tf_readout;
 size_t tf_readout_blob_size(int32_t d);
 
 /* Copy a readout head blob to the current device.  d: 32, 64, 128 or 256.
+ * dtype (tf_dtype): TF_FP32 runs the head's products in fp32; TF_BF16 and
+ * TF_BF16_F16ACT (the 16-bit models) round W1 diag(g) and W2 to bf16 once
+ * and multiply them with the fp32 activations split into a high and a low
+ * bf16 part (about 16 significant bits), accumulating in fp32.
  * host_blob is only read during the call; *out receives a handle freed with
  * tf_readout_destroy.  Synchronous; allocates device memory.
- * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d)),
- * TF_EUNSUPPORTED (other d), TF_ENOMEM, TF_EHIP.  On error *out is NULL. */
-tf_status tf_readout_create(int32_t d, const float *host_blob, size_t n_floats, tf_readout **out);
+ * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d),
+ * unknown dtype), TF_EUNSUPPORTED (other d), TF_ENOMEM, TF_EHIP.  On error
+ * *out is NULL. */
+tf_status tf_readout_create(int32_t d, int32_t dtype, const float *host_blob, size_t n_floats,
+                            tf_readout **out);
 
 /* Free a handle (NULL is a no-op).  Synchronises the device first. */
 void tf_readout_destroy(tf_readout *h);
@@ -240,7 +246,8 @@ void tf_readout_destroy(tf_readout *h);
  *   q = W2 h + b2,  m_p = median(q[7p .. 7p+6]),
  *   d0, z0, theta: seed + m;  phi: seed + m wrapped to [-pi, pi);
  *   q/p: seed + m * (|seed| + 0.02 / GeV).
- * The head runs in fp32 (matrix cores, fp32 accumulation); the decode in fp64.
+ * The head runs on matrix cores with fp32 accumulation in the handle's number
+ * type; the decode in fp64.
  *
  * states    device, float32 [n_tracks][2d], as written by fit_tracks_states
  *           (d of the handle).  Read only.

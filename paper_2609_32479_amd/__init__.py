@@ -76,7 +76,7 @@ def lib():
         L.tf_readout_blob_size.restype = ctypes.c_size_t
         L.tf_readout_blob_size.argtypes = [ctypes.c_int32]
         L.tf_readout_create.restype = ctypes.c_int
-        L.tf_readout_create.argtypes = [ctypes.c_int32, vp, ctypes.c_size_t, ctypes.POINTER(vp)]
+        L.tf_readout_create.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t, ctypes.POINTER(vp)]
         L.tf_readout_destroy.restype = None
         L.tf_readout_destroy.argtypes = [vp]
         L.tf_decode_tracks.restype = ctypes.c_int
@@ -248,13 +248,15 @@ def readout_blob_size(d: int) -> int:
 class Readout:
     """Device-resident readout head (tf_readout handle) on the current device."""
 
-    def __init__(self, blob, d: int):
+    def __init__(self, blob, d: int, dtype: str = "fp32"):
+        """dtype: "fp32", or "bf16" / "bf16_f16act" for the 16-bit head (include/trackfit.h)."""
         import numpy as np
         arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
         h = ctypes.c_void_p()
-        _check(lib().tf_readout_create(int(d), arr.ctypes.data, arr.size, ctypes.byref(h)), "tf_readout_create")
+        _check(lib().tf_readout_create(int(d), DTYPES[dtype], arr.ctypes.data, arr.size, ctypes.byref(h)),
+               "tf_readout_create")
         self._h = h
-        self.d = int(d)
+        self.d, self.dtype = int(d), dtype
 
     @property
     def handle(self):

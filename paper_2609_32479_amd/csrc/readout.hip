@@ -9,19 +9,25 @@
 // parameter is the median of its seven; it is added to the fp64 seed (phi
 // wrapped to [-pi, pi)), q/p through the seed's scale |q/p_seed| + 0.02/GeV.
 //
-// One wave per 32 tracks, both layers as fp32 matrix-core products with the
+// One wave per 32 tracks, both layers as matrix-core products with the
 // tracks on the 32 columns: hid^T = W1' z^T with W1' = W1 diag(g) (the gain
 // folded in on the host), then the per-track 1/rms scales the columns;
 // q^T = W2 h^T takes the layer-1 accumulators as its B operand as they lie.
 // The reduction order over k is free, so the host packs both weight matrices
 // in the order in which the lanes hold their operands: lane (half s, column
 // t) reads its track's half row z[t][s d ..] as consecutive float4s, and in
-// layer 2 supplies hidden unit 32 m + 8 (q/4) + 4 s + q%4 at k-step (m, q).
-// The weights (d = 128: 160 KiB) are read by every wave and stay in L2.
+// layer 2 supplies the hidden units it holds.  The weights are read by every
+// wave and stay in L2.
+//
+// Two number types: fp32 products (32x32x2) for the fp32 model; for the
+// 16-bit models bf16 weights (W1' rounded once) against fp32 activations
+// split into a high and a low bf16 part (32x32x16, two products per k-step),
+// which keeps the activations to about 16 significant bits.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
 #include <cstdint>
+#include <cstring>
 #include <new>
 #include <vector>
 
@@ -30,6 +36,8 @@
 namespace {
 
 typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(8))) float f32x8;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
 
 constexpr int kNq = 7;          // quantiles per parameter
 constexpr int kNout = 35;       // outputs of the head
@@ -41,6 +49,16 @@ constexpr int kQStride = 37;    // LDS row stride of a track's 35 outputs (float
 
 __device__ __forceinline__ f32x16 mma(float a, float b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ f32x16 mma16(bf16x8 a, bf16x8 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+
+// v = hi + lo + O(2^-16 |v|), both parts bf16 (round to nearest even)
+__device__ __forceinline__ void split16(const f32x8 v, bf16x8 &hi, bf16x8 &lo) {
+    hi = __builtin_convertvector(v, bf16x8);
+    lo = __builtin_convertvector(v - __builtin_convertvector(hi, f32x8), bf16x8);
 }
 
 // Median of seven: the value whose rank (ties broken by position) is 3; NaN if
@@ -60,6 +78,66 @@ __device__ __forceinline__ float median7(const float *v) {
     return nan ? __builtin_nanf("") : med;
 }
 
+// Layer 1 bias and SiLU on the accumulators (lane (s, c) holds unit
+// 32 m + 8 (q/4) + 4 s + q%4 of track c), in place.
+template <int MT>
+__device__ __forceinline__ void bias_silu(f32x16 (&acc)[MT], float inv, const float *__restrict__ b1, int s) {
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const float v = fmaf(inv, acc[m][q], b1[32 * m + 8 * (q >> 2) + 4 * s + (q & 3)]);
+            acc[m][q] = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
+        }
+}
+
+// Outputs to LDS, then medians, decode and the optional quantile rows.  o[rb]
+// holds rows 32 rb + 8 (q/4) + 4 s + q%4 of track c (rows past 34 unused).
+__device__ __forceinline__ void finish(const f32x16 (&o)[2], const float *__restrict__ b2, float (*qs)[kQStride],
+                                       int lane, int t0, int n, const double *__restrict__ seeds,
+                                       float *__restrict__ quant, double *__restrict__ out) {
+    const int s = lane >> 5, c = lane & 31;
+#pragma unroll
+    for (int rb = 0; rb < 2; ++rb)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) {
+            const int row = 32 * rb + 8 * (q >> 2) + 4 * s + (q & 3);
+            if (row < kNout) qs[c][row] = o[rb][q] + b2[row];
+        }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+
+    // medians and decode: lane half 0 takes d0, z0, phi; half 1 theta, q/p
+    const int t = t0 + c;
+    if (t < n) {
+        const float *qt = qs[c];
+        const double *sd = seeds + (size_t)t * 5;
+        double *op = out + (size_t)t * 5;
+        for (int p = s ? 3 : 0; p < (s ? 5 : 3); ++p) {
+            const double med = (double)median7(qt + kNq * p);
+            const double seed = sd[p];
+            double v;
+            if (p == 2) {
+                v = seed + med;
+                v -= 2.0 * kPi * floor((v + kPi) / (2.0 * kPi));
+            } else if (p == 4) {
+                v = seed + med * (fabs(seed) + kQopEps);
+            } else {
+                v = seed + med;
+            }
+            op[p] = v;
+        }
+    }
+    if (quant) {
+        // the wave's block of rows is contiguous: consecutive lanes, consecutive floats
+        const int rows = n - t0 < 32 ? n - t0 : 32;
+        float *qb = quant + (size_t)t0 * kNout;
+        for (int i = lane; i < rows * kNout; i += 64) qb[i] = qs[i / kNout][i % kNout];
+    }
+}
+
+// fp32 head: A1 [d/4][MT][64] float4 (4 consecutive k-steps), A2 [MT][4][2][64] float4.
 template <int D>
 __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__restrict__ states, int n,
                                                                  const double *__restrict__ seeds,
@@ -75,11 +153,10 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__
     if (t0 >= n) return;  // the whole wave
     const int s = lane >> 5, c = lane & 31;
     const int t = t0 + c;
-    const bool valid = t < n;
     // columns past the batch repeat track t0 (in bounds); their results are dropped
-    const float4 *zp = reinterpret_cast<const float4 *>(states + (size_t)(valid ? t : t0) * (2 * D) + s * D);
+    const float4 *zp = reinterpret_cast<const float4 *>(states + (size_t)(t < n ? t : t0) * (2 * D) + s * D);
 
-    // ---- layer 1: acc[m] = rows 32 m .. of W1' z^T, k-step ks of this lane half
+    // layer 1: acc[m] = rows 32 m .. of W1' z^T, k-step ks of this lane half
     // reading z[t][s d + ks]
     f32x16 acc[MT];
 #pragma unroll
@@ -103,18 +180,9 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__
         }
     }
     ss += __shfl_xor(ss, 32);  // both halves of the track's row
-    const float inv = 1.0f / sqrtf(ss * (1.0f / (2 * D)) + kRoEps);
+    bias_silu<MT>(acc, 1.0f / sqrtf(ss * (1.0f / (2 * D)) + kRoEps), b1, s);
 
-    // ---- bias and SiLU: lane (s, c) holds unit 32 m + 8 (q/4) + 4 s + q%4 of track c
-#pragma unroll
-    for (int m = 0; m < MT; ++m)
-#pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const float v = fmaf(inv, acc[m][q], b1[32 * m + 8 * (q >> 2) + 4 * s + (q & 3)]);
-            acc[m][q] = v / (1.0f + expf(-__builtin_amdgcn_fmed3f(v, -80.0f, 80.0f)));
-        }
-
-    // ---- layer 2: o[rb] = rows 32 rb .. of W2 h^T (rows 35 .. 63 are zero weights)
+    // layer 2: o[rb] = rows 32 rb .. of W2 h^T, k-step (m, q) taking the lane's unit of acc[m][q]
     f32x16 o[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
@@ -132,55 +200,113 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__
                 o[rb] = mma(a.z, acc[m][4 * qg + 2], o[rb]);
                 o[rb] = mma(a.w, acc[m][4 * qg + 3], o[rb]);
             }
+    finish(o, b2, qs[wv], lane, t0, n, seeds, quant, out);
+}
+
+// 16-bit head: A1 [d/8][MT][64] bf16x8 (lane (s, i): row 32 m + i, k = s d + 8 ks + e),
+// A2 [MT][2][2][64] bf16x8 (k-step (m, qh): the lane's units of acc[m][8 qh .. 8 qh + 7]).
+template <int D>
+__global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *__restrict__ states, int n,
+                                                                   const double *__restrict__ seeds,
+                                                                   const bf16x8 *__restrict__ A1,
+                                                                   const float *__restrict__ b1,
+                                                                   const bf16x8 *__restrict__ A2,
+                                                                   const float *__restrict__ b2,
+                                                                   float *__restrict__ quant, double *__restrict__ out) {
+    constexpr int MT = D / 32;
+    __shared__ float qs[kWaves][32][kQStride];
+    const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+    const int t0 = (blockIdx.x * kWaves + wv) * 32;
+    if (t0 >= n) return;  // the whole wave
+    const int s = lane >> 5, c = lane & 31;
+    const int t = t0 + c;
+    const float4 *zp = reinterpret_cast<const float4 *>(states + (size_t)(t < n ? t : t0) * (2 * D) + s * D);
+
+    f32x16 acc[MT];
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int q = 0; q < 16; ++q) acc[m][q] = 0.f;
+    float ss = 0.f;
+#pragma unroll 2
+    for (int ks = 0; ks < D / 8; ++ks) {
+        const float4 z0 = zp[2 * ks], z1 = zp[2 * ks + 1];
+        bf16x8 a[MT];
+#pragma unroll
+        for (int m = 0; m < MT; ++m) a[m] = A1[(ks * MT + m) * 64 + lane];
+        ss = fmaf(z0.x, z0.x, fmaf(z0.y, z0.y, fmaf(z0.z, z0.z, fmaf(z0.w, z0.w, ss))));
+        ss = fmaf(z1.x, z1.x, fmaf(z1.y, z1.y, fmaf(z1.z, z1.z, fmaf(z1.w, z1.w, ss))));
+        bf16x8 hi, lo;
+        split16((f32x8){z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w}, hi, lo);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            acc[m] = mma16(a[m], hi, acc[m]);
+            acc[m] = mma16(a[m], lo, acc[m]);
+        }
+    }
+    ss += __shfl_xor(ss, 32);
+    bias_silu<MT>(acc, 1.0f / sqrtf(ss * (1.0f / (2 * D)) + kRoEps), b1, s);
+
+    f32x16 o[2];
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-        for (int q = 0; q < 16; ++q) {
-            const int row = 32 * rb + 8 * (q >> 2) + 4 * s + (q & 3);
-            if (row < kNout) qs[wv][c][row] = o[rb][q] + b2[row];
-        }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-
-    // ---- medians and decode: lane half 0 takes d0, z0, phi; half 1 theta, q/p
-    if (valid) {
-        const float *qt = qs[wv][c];
-        const double *sd = seeds + (size_t)t * 5;
-        double *op = out + (size_t)t * 5;
-        for (int p = s ? 3 : 0; p < (s ? 5 : 3); ++p) {
-            const double med = (double)median7(qt + kNq * p);
-            const double seed = sd[p];
-            double v;
-            if (p == 2) {
-                v = seed + med;
-                v -= 2.0 * kPi * floor((v + kPi) / (2.0 * kPi));
-            } else if (p == 4) {
-                v = seed + med * (fabs(seed) + kQopEps);
-            } else {
-                v = seed + med;
+        for (int q = 0; q < 16; ++q) o[rb][q] = 0.f;
+#pragma unroll
+    for (int m = 0; m < MT; ++m)
+#pragma unroll
+        for (int qh = 0; qh < 2; ++qh) {
+            bf16x8 hi, lo;
+            split16((f32x8){acc[m][8 * qh + 0], acc[m][8 * qh + 1], acc[m][8 * qh + 2], acc[m][8 * qh + 3],
+                            acc[m][8 * qh + 4], acc[m][8 * qh + 5], acc[m][8 * qh + 6], acc[m][8 * qh + 7]},
+                    hi, lo);
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+                const bf16x8 a = A2[((m * 2 + qh) * 2 + rb) * 64 + lane];
+                o[rb] = mma16(a, hi, o[rb]);
+                o[rb] = mma16(a, lo, o[rb]);
             }
-            op[p] = v;
         }
-    }
-    if (quant) {
-        // the wave's block of rows is contiguous: consecutive lanes, consecutive floats
-        const int rows = n - t0 < 32 ? n - t0 : 32;
-        float *qb = quant + (size_t)t0 * kNout;
-        for (int i = lane; i < rows * kNout; i += 64) qb[i] = qs[wv][i / kNout][i % kNout];
-    }
+    finish(o, b2, qs[wv], lane, t0, n, seeds, quant, out);
 }
 
 }  // namespace
 
 struct tf_readout {
     int d = 0;
-    float *dmem = nullptr;
-    const float4 *A1 = nullptr;
+    bool half = false;       // 16-bit head (tf_readout16_kernel)
+    char *dmem = nullptr;
+    const void *A1 = nullptr;
     const float *b1 = nullptr;
-    const float4 *A2 = nullptr;
+    const void *A2 = nullptr;
     const float *b2 = nullptr;
 };
+
+namespace {
+
+// float -> bf16 bits, round to nearest even (NaN stays a quiet NaN)
+uint16_t bf16_bits(float x) {
+    uint32_t u;
+    std::memcpy(&u, &x, 4);
+    if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40);
+    u += 0x7fffu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+template <int D>
+void launch_d(const tf_readout *h, dim3 grid, dim3 block, hipStream_t stream, const float *states, int n,
+              const double *seeds, float *quant, double *out) {
+    if (h->half)
+        hipLaunchKernelGGL(tf_readout16_kernel<D>, grid, block, 0, stream, states, n, seeds,
+                           static_cast<const bf16x8 *>(h->A1), h->b1, static_cast<const bf16x8 *>(h->A2), h->b2,
+                           quant, out);
+    else
+        hipLaunchKernelGGL(tf_readout_kernel<D>, grid, block, 0, stream, states, n, seeds,
+                           static_cast<const float4 *>(h->A1), h->b1, static_cast<const float4 *>(h->A2), h->b2,
+                           quant, out);
+}
+
+}  // namespace
 
 extern "C" size_t tf_readout_blob_size(int32_t d) {
     if (d <= 0) return 0;
@@ -188,58 +314,92 @@ extern "C" size_t tf_readout_blob_size(int32_t d) {
     return 2 * dd + dd * 2 * dd + dd + kNout * dd + kNout;
 }
 
-extern "C" tf_status tf_readout_create(int32_t d, const float *host_blob, size_t n_floats, tf_readout **out) {
+extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *host_blob, size_t n_floats,
+                                       tf_readout **out) {
     if (!out) return TF_EINVAL;
     *out = nullptr;
     if (!host_blob || d <= 0 || n_floats != tf_readout_blob_size(d)) return TF_EINVAL;
+    if (dtype != TF_FP32 && dtype != TF_BF16 && dtype != TF_BF16_F16ACT) return TF_EINVAL;
     if (d != 32 && d != 64 && d != 128 && d != 256) return TF_EUNSUPPORTED;
+    const bool half = dtype != TF_FP32;
     const size_t dd = (size_t)d;
     const int MT = d / 32;
     const float *g = host_blob, *W1 = g + 2 * dd, *b1 = W1 + dd * 2 * dd, *W2 = b1 + dd, *b2 = W2 + kNout * dd;
-    // device layout: A1 [d/4][MT][64][4], b1 [d], A2 [MT][4][2][64][4], b2 [64]
-    const size_t nA1 = dd * 2 * dd, nA2 = (size_t)MT * 4 * 2 * 64 * 4, total = nA1 + dd + nA2 + 64;
-    std::vector<float> h;
+    // W1' (gain folded in) as lane (s, i) holds it: row 32 m + i, column s d + kk, where kk is
+    // the k-step's position in the lane's half row; W2 as lane (s, i) holds it: row 32 rb + i,
+    // the hidden unit that the lane's accumulator slot carries
+    auto w1 = [&](int m, int lane, int kk) {
+        const size_t u = 32 * m + (lane & 31), k = (size_t)(lane >> 5) * dd + kk;
+        return W1[u * 2 * dd + k] * g[k];
+    };
+    auto w2 = [&](int rb, int lane, int m, int q) {
+        const int row = 32 * rb + (lane & 31);
+        const size_t u = 32 * m + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
+        return row < kNout ? W2[(size_t)row * dd + u] : 0.f;
+    };
+    const size_t esz = half ? 2 : 4;
+    const size_t nA1 = dd * 2 * dd, nA2 = (size_t)MT * 2 * 16 * 64;  // elements (A2: 2 row blocks x 16 slots)
+    const size_t oB1 = nA1 * esz, oA2 = oB1 + dd * 4, oB2 = oA2 + nA2 * esz, total = oB2 + 64 * 4;
+    std::vector<char> hbuf;
     try {
-        h.assign(total, 0.f);
+        hbuf.assign(total, 0);
     } catch (const std::bad_alloc &) {
         return TF_ENOMEM;
     }
-    float *hA1 = h.data(), *hb1 = hA1 + nA1, *hA2 = hb1 + dd, *hb2 = hA2 + nA2;
-    for (int grp = 0; grp < d / 4; ++grp)
-        for (int m = 0; m < MT; ++m)
-            for (int lane = 0; lane < 64; ++lane)
-                for (int e = 0; e < 4; ++e) {
-                    const size_t u = 32 * m + (lane & 31), k = (size_t)(lane >> 5) * dd + 4 * grp + e;
-                    hA1[(((size_t)grp * MT + m) * 64 + lane) * 4 + e] = W1[u * 2 * dd + k] * g[k];
-                }
-    for (size_t u = 0; u < dd; ++u) hb1[u] = b1[u];
-    for (int m = 0; m < MT; ++m)
-        for (int qg = 0; qg < 4; ++qg)
-            for (int rb = 0; rb < 2; ++rb)
+    char *hp = hbuf.data();
+    if (half) {
+        // A1 [d/8][MT][64][8]: k-step ks covers kk = 8 ks .. 8 ks + 7
+        uint16_t *A1 = reinterpret_cast<uint16_t *>(hp);
+        for (int ks = 0; ks < d / 8; ++ks)
+            for (int m = 0; m < MT; ++m)
                 for (int lane = 0; lane < 64; ++lane)
-                    for (int e = 0; e < 4; ++e) {
-                        const int row = 32 * rb + (lane & 31);
-                        const size_t u = 32 * m + 8 * qg + 4 * (lane >> 5) + e;
-                        hA2[((((size_t)m * 4 + qg) * 2 + rb) * 64 + lane) * 4 + e] =
-                            row < kNout ? W2[(size_t)row * dd + u] : 0.f;
-                    }
-    for (int r = 0; r < kNout; ++r) hb2[r] = b2[r];
+                    for (int e = 0; e < 8; ++e)
+                        A1[(((size_t)ks * MT + m) * 64 + lane) * 8 + e] = bf16_bits(w1(m, lane, 8 * ks + e));
+        // A2 [MT][2][2][64][8]: k-step (m, qh) takes accumulator slots 8 qh .. 8 qh + 7
+        uint16_t *A2 = reinterpret_cast<uint16_t *>(hp + oA2);
+        for (int m = 0; m < MT; ++m)
+            for (int qh = 0; qh < 2; ++qh)
+                for (int rb = 0; rb < 2; ++rb)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int e = 0; e < 8; ++e)
+                            A2[((((size_t)m * 2 + qh) * 2 + rb) * 64 + lane) * 8 + e] =
+                                bf16_bits(w2(rb, lane, m, 8 * qh + e));
+    } else {
+        // A1 [d/4][MT][64][4]: four consecutive k-steps kk = 4 grp .. 4 grp + 3
+        float *A1 = reinterpret_cast<float *>(hp);
+        for (int grp = 0; grp < d / 4; ++grp)
+            for (int m = 0; m < MT; ++m)
+                for (int lane = 0; lane < 64; ++lane)
+                    for (int e = 0; e < 4; ++e)
+                        A1[(((size_t)grp * MT + m) * 64 + lane) * 4 + e] = w1(m, lane, 4 * grp + e);
+        // A2 [MT][4][2][64][4]: k-steps (m, 4 qg .. 4 qg + 3)
+        float *A2 = reinterpret_cast<float *>(hp + oA2);
+        for (int m = 0; m < MT; ++m)
+            for (int qg = 0; qg < 4; ++qg)
+                for (int rb = 0; rb < 2; ++rb)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int e = 0; e < 4; ++e)
+                            A2[((((size_t)m * 4 + qg) * 2 + rb) * 64 + lane) * 4 + e] = w2(rb, lane, m, 4 * qg + e);
+    }
+    std::memcpy(hp + oB1, b1, dd * 4);
+    std::memcpy(hp + oB2, b2, kNout * 4);
     tf_readout *ro = new (std::nothrow) tf_readout;
     if (!ro) return TF_ENOMEM;
-    if (hipMalloc((void **)&ro->dmem, total * sizeof(float)) != hipSuccess) {
+    if (hipMalloc((void **)&ro->dmem, total) != hipSuccess) {
         delete ro;
         return TF_ENOMEM;
     }
-    if (hipMemcpy(ro->dmem, h.data(), total * sizeof(float), hipMemcpyHostToDevice) != hipSuccess) {
+    if (hipMemcpy(ro->dmem, hp, total, hipMemcpyHostToDevice) != hipSuccess) {
         (void)hipFree(ro->dmem);
         delete ro;
         return TF_EHIP;
     }
     ro->d = d;
-    ro->A1 = reinterpret_cast<const float4 *>(ro->dmem);
-    ro->b1 = ro->dmem + nA1;
-    ro->A2 = reinterpret_cast<const float4 *>(ro->dmem + nA1 + dd);
-    ro->b2 = ro->dmem + nA1 + dd + nA2;
+    ro->half = half;
+    ro->A1 = ro->dmem;
+    ro->b1 = reinterpret_cast<const float *>(ro->dmem + oB1);
+    ro->A2 = ro->dmem + oA2;
+    ro->b2 = reinterpret_cast<const float *>(ro->dmem + oB2);
     *out = ro;
     return TF_OK;
 }
@@ -259,22 +419,10 @@ extern "C" tf_status tf_decode_tracks(const float *states, int32_t n_tracks, con
     const int per_block = 32 * kWaves;
     const dim3 grid((unsigned)((n_tracks + per_block - 1) / per_block)), block(64 * kWaves);
     switch (h->d) {
-        case 32:
-            hipLaunchKernelGGL(tf_readout_kernel<32>, grid, block, 0, stream, states, (int)n_tracks, seeds, h->A1,
-                               h->b1, h->A2, h->b2, quantiles, out);
-            break;
-        case 64:
-            hipLaunchKernelGGL(tf_readout_kernel<64>, grid, block, 0, stream, states, (int)n_tracks, seeds, h->A1,
-                               h->b1, h->A2, h->b2, quantiles, out);
-            break;
-        case 128:
-            hipLaunchKernelGGL(tf_readout_kernel<128>, grid, block, 0, stream, states, (int)n_tracks, seeds, h->A1,
-                               h->b1, h->A2, h->b2, quantiles, out);
-            break;
-        case 256:
-            hipLaunchKernelGGL(tf_readout_kernel<256>, grid, block, 0, stream, states, (int)n_tracks, seeds, h->A1,
-                               h->b1, h->A2, h->b2, quantiles, out);
-            break;
+        case 32: launch_d<32>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
+        case 64: launch_d<64>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
+        case 128: launch_d<128>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
+        case 256: launch_d<256>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
         default: return TF_EINVAL;
     }
     return hipGetLastError() == hipSuccess ? TF_OK : TF_EHIP;

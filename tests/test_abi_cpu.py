@@ -88,10 +88,12 @@ def test_readout_and_states_argument_checks_without_gpu(tf):
     assert L.tf_readout_blob_size(0) == 0
     h = ctypes.c_void_p()
     blob = (ctypes.c_float * 10)()
-    assert L.tf_readout_create(128, blob, 10, ctypes.byref(h)) == tf.TF_EINVAL          # wrong size
-    assert L.tf_readout_create(128, None, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL
-    assert L.tf_readout_create(128, blob, 10, None) == tf.TF_EINVAL
-    assert L.tf_readout_create(96, blob, L.tf_readout_blob_size(96), ctypes.byref(h)) == tf.TF_EUNSUPPORTED
+    fp32 = tf.TF_FP32
+    assert L.tf_readout_create(128, fp32, blob, 10, ctypes.byref(h)) == tf.TF_EINVAL          # wrong size
+    assert L.tf_readout_create(128, fp32, None, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL
+    assert L.tf_readout_create(128, fp32, blob, 10, None) == tf.TF_EINVAL
+    assert L.tf_readout_create(128, 9, blob, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL  # dtype
+    assert L.tf_readout_create(96, fp32, blob, L.tf_readout_blob_size(96), ctypes.byref(h)) == tf.TF_EUNSUPPORTED
     assert h.value is None
     L.tf_readout_destroy(None)   # no-op
     assert L.tf_decode_tracks(None, 0, None, None, None, None, None) == tf.TF_EINVAL    # null handle

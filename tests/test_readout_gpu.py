@@ -35,6 +35,16 @@ def quantile_tol(d):
     return 2.0 ** -24 * (2 * d) * 2
 
 
+# The 16-bit head rounds W1 diag(g) (and W2) to bf16 and keeps the activations
+# to ~16 bits: ~2^-9 per weight, averaged over the dot products, is held to
+# the bf16 model's output tolerance.
+def head_tols(mode, d):
+    """(quantile, decoded) tolerances of a head of this number type."""
+    if mode == "fp32":
+        return quantile_tol(d), DECODE_TOL
+    return TOL["bf16"], TOL["bf16"]
+
+
 @pytest.fixture(scope="module")
 def tf():
     if not torch.cuda.is_available():
@@ -43,8 +53,9 @@ def tf():
     return tf
 
 
-def colerr(g, r):
-    """Per column: max |g - r| / max(|r|, rms of the column); NaN patterns must match."""
+def colerr(g, r, rms=None):
+    """Per column: max |g - r| / max(|r|, rms of the column); NaN patterns must
+    match.  rms: column scales of a larger sample, for a batch of few tracks."""
     g = np.asarray(g, dtype=np.float64)
     r = np.asarray(r, dtype=np.float64)
     assert g.shape == r.shape
@@ -53,7 +64,8 @@ def colerr(g, r):
     g, r = g[ok], r[ok]
     if r.shape[0] == 0:
         return np.zeros(r.shape[1])
-    rms = np.sqrt(np.mean(r ** 2, axis=0))
+    if rms is None:
+        rms = np.sqrt(np.mean(r ** 2, axis=0))
     return np.max(np.abs(g - r) / np.maximum(np.abs(r), np.maximum(rms, 1e-300)), axis=0)
 
 
@@ -183,34 +195,42 @@ def _decode(tf, R, states, seeds, quantiles=True):
     return out.cpu().numpy(), (q.cpu().numpy() if q is not None else None)
 
 
-@pytest.mark.parametrize("name,n", [("deploy_d128x4_bf16_8m", 1000), ("tiny_d32_fp32", 77),
-                                    ("d256x6_bf16_1m", 300), ("deploy_d128x4_bf16_8m", 1),
-                                    ("deploy_d128x4_bf16_8m", 33)])
-def test_decode_matches_oracle_on_the_same_states(tf, name, n):
+@pytest.mark.parametrize("name,n,mode", [("deploy_d128x4_bf16_8m", 1000, "bf16"), ("deploy_d128x4_bf16_8m", 1000, "fp32"),
+                                         ("tiny_d32_fp32", 77, "fp32"), ("tiny_d32_fp32", 77, "bf16"),
+                                         ("d256x6_bf16_1m", 300, "bf16"), ("d256x6_bf16_1m", 300, "fp32"),
+                                         ("d128x4_fp32_65k", 500, "fp32"), ("deploy_d128x4_bf16_8m", 1, "bf16"),
+                                         ("deploy_d128x4_bf16_8m", 33, "bf16"), ("deploy_d128x4_bf16_8m", 33, "fp32")])
+def test_decode_matches_oracle_on_the_same_states(tf, name, n, mode):
     """The oracle's states (rounded to fp32, as the library takes them) and
-    seeds in; the 35 quantiles and the decoded parameters compared."""
+    seeds in; the 35 quantiles and the decoded parameters compared, for both
+    number types of the head."""
     w = ts.WORKLOADS[name]
     d = w.d_model
-    print(f"[decode] {name} n={n}", flush=True)
-    hits, offs = ts.make_tracks(w, n_tracks=n)
+    print(f"[decode] {name} n={n} head {mode}", flush=True)
+    # column scales from at least 300 tracks, the first n of which are decoded
+    hits, offs = ts.make_tracks(w, n_tracks=max(n, 300))
     blob = ts.make_weights(w)
     st = _ref_states(w, hits, offs, blob).astype(np.float32)
     seeds, _, bad = oracle.seed_tracks(hits, offs, w.b_field, features=False)
     assert bad == 0
     hb = ts.make_readout_weights(w)
-    R = tf.Readout(hb, d)
-    g_out, g_q = _decode(tf, R, st, seeds)
+    R = tf.Readout(hb, d, mode)
     r_q, r_out = oracle.readout_tracks(st.astype(np.float64), seeds, hb, d)
-    eq = colerr(g_q, r_q)
-    eo = colerr(wrap_phi(g_out, r_out), r_out)
-    print(f"[decode] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
-    assert eq.max() <= quantile_tol(d) and eo.max() <= DECODE_TOL
+    rms_q, rms_o = (np.sqrt(np.mean(a ** 2, axis=0)) for a in (r_q, r_out))
+    st, seeds, r_q, r_out = st[:n], seeds[:n], r_q[:n], r_out[:n]
+    g_out, g_q = _decode(tf, R, st, seeds)
+    eq = colerr(g_q, r_q, rms_q)
+    eo = colerr(wrap_phi(g_out, r_out), r_out, rms_o)
+    print(f"[decode] {name} head {mode}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
+    tq, to = head_tols(mode, d)
+    assert eq.max() <= tq and eo.max() <= to
     # without the quantile output the decode is the same, bit for bit
     g2, q2 = _decode(tf, R, st, seeds, quantiles=False)
     assert q2 is None and np.array_equal(g2, g_out)
 
 
-def test_decode_median_and_decode_rules_on_a_planted_head(tf):
+@pytest.mark.parametrize("mode", ["fp32", "bf16"])
+def test_decode_median_and_decode_rules_on_a_planted_head(tf, mode):
     """A head whose quantiles are known in closed form: W1 = 0 and W2 = 0, so
     q = b2 for every track; the seven values of each parameter are planted
     out of order, the decode then adds their middle value to the seed."""
@@ -224,7 +244,7 @@ def test_decode_median_and_decode_rules_on_a_planted_head(tf):
         v = np.sort(rng.uniform(-4, 4, 7))
         b2[7 * p:7 * p + 7] = rng.permutation(v)
         meds[p] = float(np.sort(b2[7 * p:7 * p + 7])[3])   # as stored (float32)
-    R = tf.Readout(hb, d)
+    R = tf.Readout(hb, d, mode)
     n = 40
     states = rng.normal(size=(n, 2 * d)).astype(np.float32)
     seeds = np.stack([rng.uniform(-1, 1, n), rng.uniform(-50, 50, n), rng.uniform(-np.pi, np.pi, n),
@@ -239,7 +259,8 @@ def test_decode_median_and_decode_rules_on_a_planted_head(tf):
     assert np.allclose(out, exp, rtol=1e-12, atol=1e-12)
 
 
-def test_decode_nan_inputs_stay_local(tf):
+@pytest.mark.parametrize("mode", ["fp32", "bf16"])
+def test_decode_nan_inputs_stay_local(tf, mode):
     w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
     d = w.d_model
     rng = np.random.default_rng(4)
@@ -250,7 +271,7 @@ def test_decode_nan_inputs_stay_local(tf):
     st[7] = np.nan          # a rejected track's states
     seeds[40] = np.nan      # a track without a seed
     hb = ts.make_readout_weights(w)
-    R = tf.Readout(hb, d)
+    R = tf.Readout(hb, d, mode)
     out, q = _decode(tf, R, st, seeds)
     assert np.all(np.isnan(out[[7, 40]])) and np.all(np.isnan(q[7]))
     assert np.all(np.isfinite(q[40]))
@@ -258,8 +279,9 @@ def test_decode_nan_inputs_stay_local(tf):
     good[[7, 40]] = False
     assert np.all(np.isfinite(out[good]))
     r_q, r_out = oracle.readout_tracks(st[good].astype(np.float64), seeds[good], hb, d)
-    assert colerr(q[good], r_q).max() <= quantile_tol(d)
-    assert colerr(wrap_phi(out[good], r_out), r_out).max() <= DECODE_TOL
+    tq, to = head_tols(mode, d)
+    assert colerr(q[good], r_q).max() <= tq
+    assert colerr(wrap_phi(out[good], r_out), r_out).max() <= to
 
 
 @pytest.mark.parametrize("name", ["deploy_d128x4_bf16_8m", "d128x4_fp32_65k"])
@@ -270,7 +292,8 @@ def test_seed_states_decode_end_to_end(tf, name):
     print(f"[chain] {name}", flush=True)
     W, blob = _weights(tf, w)
     hb = ts.make_readout_weights(w)
-    R = tf.Readout(hb, w.d_model)
+    mode = tf.MODE_FOR_WEIGHTS[w.dtype]
+    R = tf.Readout(hb, w.d_model, mode)
     hits, offs = ts.make_tracks(w, n_tracks=1500)
     h = torch.from_numpy(hits).cuda()
     o = torch.from_numpy(offs).cuda()
@@ -283,5 +306,6 @@ def test_seed_states_decode_end_to_end(tf, name):
     eq = colerr(q.cpu().numpy(), r_q)
     eo = colerr(wrap_phi(out.cpu().numpy(), r_out), r_out)
     print(f"[chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
-    # the quantiles carry the head's own fp32 rounding on top of the encoder's
-    assert eq.max() <= max(TOL[w.dtype], quantile_tol(w.d_model)) and eo.max() <= TOL[w.dtype]
+    # the quantiles carry the head's own rounding on top of the encoder's
+    tq, _ = head_tols(mode, w.d_model)
+    assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]

@@ -314,8 +314,9 @@ def readout_layout(d: int):
 
 
 def make_readout_weights(w, seed: int | None = None) -> np.ndarray:
-    """float32 blob of the readout head for a workload's width (fp32 values,
-    drawn like the encoder's: N(0, 1/fan_in), U(+-fan_in^-1/2), gains U(0.5, 1.5))."""
+    """float32 blob of the readout head for a workload's width, drawn like the
+    encoder's (N(0, 1/fan_in), U(+-fan_in^-1/2), gains U(0.5, 1.5)); rounded
+    to bf16 values for a bf16 workload, as its encoder weights are."""
     w = workload(w)
     rng = np.random.default_rng(w.weight_seed + 100 if seed is None else seed)
     parts = []
@@ -327,4 +328,5 @@ def make_readout_weights(w, seed: int | None = None) -> np.ndarray:
             parts.append(rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n))
         else:
             parts.append(rng.uniform(0.5, 1.5, n))
-    return np.concatenate(parts).astype(np.float32)
+    blob = np.concatenate(parts).astype(np.float32)
+    return round_to_bf16(blob) if w.dtype == "bf16" else blob
