@@ -40,8 +40,10 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # device copy of known size (profiles/ holds the summary).  Valid only for the
 # kernel source whose SHA-256 is recorded; otherwise traffic is reported null.
 TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "batch": 262144, "calls_per_step": 32,
-           "kernel_sha256": "e937ddb7d9793af8b96fadf6ac45ab5be68c89b6f46da6b32a1065cc4612a048",
-           "fetch_bytes": 50702062, "write_bytes": 5538656}
+           "kernel_sha256": "a4ff96fe0aa48cbb064efa363e7d35d1d0b4a334a260b7c6fbbcaf5f98cc9c7d",
+           "fetch_bytes": 50698990, "write_bytes": 5506192}
+# The same for the end-states launch of the readout path (fit_tracks_states).
+STATES_TRAFFIC = dict(TRAFFIC, fetch_bytes=55189391, write_bytes=269221888)
 
 
 def algorithmic_flops(n_layers, d, n_hits, n_tracks):
@@ -85,14 +87,15 @@ def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
             "parity_max_col_err_on_sample": err}
 
 
-def traffic_bytes(w, batch, calls):
+def traffic_bytes(w, batch, calls, rec=None):
     """Counter-derived HBM bytes per launch, when they were taken on this kernel
     source and this launch shape; else None."""
-    if TRAFFIC is None or calls != TRAFFIC["calls_per_step"] or batch != TRAFFIC["batch"]:
+    rec = TRAFFIC if rec is None else rec
+    if calls != rec["calls_per_step"] or batch != rec["batch"]:
         return None
-    if w.name != TRAFFIC["workload"] or kernel_source_sha256() != TRAFFIC["kernel_sha256"]:
+    if w.name != rec["workload"] or kernel_source_sha256() != rec["kernel_sha256"]:
         return None
-    return TRAFFIC["fetch_bytes"] + TRAFFIC["write_bytes"]
+    return rec["fetch_bytes"] + rec["write_bytes"]
 
 
 def kernel_source_sha256():
@@ -341,7 +344,8 @@ def bench_readout(args, w, hits, offs, mode, batch):
                    "launches_per_call": 3, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": d, "mode": mode,
                    "max_hits": W.max_hits, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None, "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
+                     "traffic": traffic_bytes(w, batch, len(starts), STATES_TRAFFIC),
+                     "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "readout_flops_per_step": readout_algorithmic_flops(d, n_tracks),
         "host_wall_s": wall,
