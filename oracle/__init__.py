@@ -39,10 +39,15 @@ def lib():
             fn.restype = None
             fn.argtypes = [dp, dp, ctypes.c_int, ctypes.c_int, dp]
         L.orc_track_forward.restype = ctypes.c_int
-        L.orc_track_forward.argtypes = [fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, dp, dp, dp, dp]
+        L.orc_track_forward.argtypes = [fp, ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int, fp, dp, dp,
+                                        dp, dp]
         L.orc_track_states.restype = ctypes.c_long
-        L.orc_track_states.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp, ctypes.c_size_t, dp,
-                                       ctypes.c_int]
+        L.orc_track_states.argtypes = [fp, ctypes.c_int, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
+                                       ctypes.c_size_t, dp, ctypes.c_int]
+        L.orc_fourier_blob_size.restype = ctypes.c_size_t
+        L.orc_fourier_blob_size.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_fourier_features.restype = None
+        L.orc_fourier_features.argtypes = [fp, ctypes.c_int, fp, fp, dp]
         L.orc_readout_blob_size.restype = ctypes.c_size_t
         L.orc_readout_blob_size.argtypes = [ctypes.c_int]
         L.orc_median_odd.restype = ctypes.c_double
@@ -54,7 +59,7 @@ def lib():
         L.orc_readout_tracks.restype = ctypes.c_long
         L.orc_readout_tracks.argtypes = [dp, ctypes.c_int32, ctypes.c_int, fp, ctypes.c_size_t, dp, dp, dp]
         L.orc_fit_tracks.restype = ctypes.c_long
-        L.orc_fit_tracks.argtypes = [fp, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
+        L.orc_fit_tracks.argtypes = [fp, ctypes.c_int, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
                                      ctypes.c_size_t, dp, ctypes.c_int]
         L.orc_threads.restype = ctypes.c_int
         L.orc_threads.argtypes = [ctypes.c_int]
@@ -131,37 +136,59 @@ def scan_backward(x, a):
     return _scan(lib().orc_scan_backward, x, a)
 
 
-def track_forward(hits, blob, n_layers, d, with_states=False):
+def _model_size(n_layers, d, n_features):
+    return fourier_blob_size(n_layers, d, n_features) if n_features else blob_size(n_layers, d)
+
+
+def track_forward(hits, blob, n_layers, d, with_states=False, n_features=0):
     """One track: returns (out5, pooled [d], residual stream after the last layer [L, d])
     and, if asked, the last layer's end states [2d] (forward at the last hit,
-    reverse at the first hit)."""
-    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    reverse at the first hit).  n_features > 0: hits are [L, F] per-hit
+    features of the Fourier front end."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, n_features or 3))
     blob, pb = _f(blob)
-    assert blob.size == blob_size(n_layers, d)
+    assert blob.size == _model_size(n_layers, d, n_features)
     L = hits.shape[0]
     out = np.empty(5)
     pooled = np.empty(d)
     resid = np.empty((max(L, 1), d))
     states = np.empty(2 * d)
     dp = ctypes.POINTER(ctypes.c_double)
-    rc = lib().orc_track_forward(ph, L, n_layers, d, pb, out.ctypes.data_as(dp),
+    rc = lib().orc_track_forward(ph, L, int(n_features), n_layers, d, pb, out.ctypes.data_as(dp),
                                  pooled.ctypes.data_as(dp), resid.ctypes.data_as(dp),
                                  states.ctypes.data_as(dp) if (with_states and n_layers > 0) else None)
     res = (out, pooled, (resid[:L] if rc == 0 else None))
     return res + (states,) if with_states else res
 
 
-def fit_tracks(hits, offsets, blob, n_layers, d, n_threads=0):
-    """Packed batch: returns out [N, 5] float64 (NaN rows for tracks with no hits)."""
-    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+def fit_tracks(hits, offsets, blob, n_layers, d, n_threads=0, n_features=0):
+    """Packed batch: returns out [N, 5] float64 (NaN rows for tracks with no hits).
+    n_features > 0: hits are [H, F] per-hit features of the Fourier front end."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, n_features or 3))
     offsets = np.ascontiguousarray(offsets, dtype=np.int32)
     blob, pb = _f(blob)
     n = offsets.size - 1
     out = np.empty((max(n, 0), 5))
-    rc = lib().orc_fit_tracks(ph, offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n, n_layers, d,
+    rc = lib().orc_fit_tracks(ph, int(n_features), offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n,
+                              n_layers, d,
                               pb, blob.size, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(n_threads))
     if rc < 0:
         raise ValueError("oracle rejected its arguments")
+    return out
+
+
+def fourier_blob_size(n_layers: int, d: int, n_features: int) -> int:
+    return int(lib().orc_fourier_blob_size(n_layers, d, n_features))
+
+
+def fourier_features(feat, lo, hi):
+    """Fourier features [32 F] of one hit's F features (fp64 values; see oracle.c)."""
+    f, pf = _f(np.asarray(feat).reshape(-1))
+    l, pl = _f(lo)
+    h, ph = _f(hi)
+    assert l.size == f.size == h.size
+    out = np.empty(32 * f.size)
+    lib().orc_fourier_features(pf, f.size, pl, ph, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
     return out
 
 
@@ -213,14 +240,15 @@ def seed_tracks(hits, offsets, b_tesla, features=True):
 # The paper's readout and decode (Sec. Encoder, last paragraph; Sec. Losses).
 # ---------------------------------------------------------------------------
 
-def track_states(hits, offsets, blob, n_layers, d, n_threads=0):
+def track_states(hits, offsets, blob, n_layers, d, n_threads=0, n_features=0):
     """Packed batch: the last layer's end states [N, 2d] (NaN rows for empty tracks)."""
-    hits, ph = _f(np.asarray(hits).reshape(-1, 3))
+    hits, ph = _f(np.asarray(hits).reshape(-1, n_features or 3))
     offsets = np.ascontiguousarray(offsets, dtype=np.int32)
     blob, pb = _f(blob)
     n = offsets.size - 1
     st = np.empty((max(n, 0), 2 * d))
-    rc = lib().orc_track_states(ph, offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n, n_layers, d,
+    rc = lib().orc_track_states(ph, int(n_features), offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n,
+                                n_layers, d,
                                 pb, blob.size, st.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(n_threads))
     if rc < 0:
         raise ValueError("oracle rejected its arguments")

@@ -22,6 +22,10 @@
  *   embed.W[d][3], embed.b[d],
  *   per layer: norm.g[d], in.W[3d][d], in.b[3d], out.W[d][2d], out.b[d],
  *   head.W1[d][d], head.b1[d], head.W2[5][d], head.b2[5].
+ * With the paper's Fourier front end (n_feat = F > 0 per-hit features instead
+ * of (x, y, z)), the first two entries are replaced by
+ *   fe.lo[F], fe.hi[F], fe.W[d][32 F], fe.b[d]
+ * (see orc_fourier_features for the column order of fe.W).
  */
 #include <math.h>
 #include <stdint.h>
@@ -32,6 +36,8 @@
 #endif
 
 #define ORC_EPS 1e-6
+#define ORC_PI 3.14159265358979323846
+#define ORC_NSCALE 16 /* Fourier scales (Sec. Encoder) */
 
 /* Fixed detector bounds used for the min-max normalisation of the hit
  * coordinates (Sec. Encoder: features are min-max normalised to [0, 1]). */
@@ -44,6 +50,39 @@ size_t orc_blob_size(int n_layers, int d) {
     size_t dd = (size_t)d;
     size_t per_layer = dd + 3 * dd * dd + 3 * dd + dd * 2 * dd + dd;
     return 3 * dd + dd + (size_t)n_layers * per_layer + dd * dd + dd + 5 * dd + 5;
+}
+
+/* Floats of the front end: (x, y, z) embedding, or the Fourier front end of F features. */
+static size_t orc_front_size(int d, int n_feat) {
+    size_t dd = (size_t)d, F = (size_t)n_feat;
+    return n_feat > 0 ? 2 * F + dd * 2 * ORC_NSCALE * F + dd : 4 * dd;
+}
+
+/* Blob size of the model with the Fourier front end over n_feat features. */
+size_t orc_fourier_blob_size(int n_layers, int d, int n_feat) {
+    if (n_feat <= 0) return 0;
+    return orc_blob_size(n_layers, d) - 4 * (size_t)d + orc_front_size(d, n_feat);
+}
+
+/* Multi-scale Fourier featurisation of one hit (Sec. Encoder): each of the F
+ * features is min-max normalised with its bounds, u = (x - lo) / (hi - lo),
+ * in float32 (the model's number type: the subtraction, the reciprocal of
+ * the span and the product are each rounded to float32), and expanded at the
+ * 16 scales 2^s, s = 0..15: phi[32 f + s] = sin(pi 2^s u_f) and
+ * phi[32 f + 16 + s] = cos(pi 2^s u_f).  The phase 2^s u_f is exact in
+ * double and reduced modulo 2 exactly before the sine is taken. */
+void orc_fourier_features(const float *feat, int n_feat, const float *lo, const float *hi, double *phi) {
+    for (int f = 0; f < n_feat; ++f) {
+        const float span = hi[f] - lo[f];
+        const float inv = 1.0f / span;
+        const float t = feat[f] - lo[f];
+        const float u = t * inv;
+        for (int sc = 0; sc < ORC_NSCALE; ++sc) {
+            const double x = fmod(ldexp((double)u, sc), 2.0);
+            phi[2 * ORC_NSCALE * f + sc] = sin(ORC_PI * x);
+            phi[2 * ORC_NSCALE * f + ORC_NSCALE + sc] = cos(ORC_PI * x);
+        }
+    }
 }
 
 /* Logistic sigmoid, the gate nonlinearity z_t = sigma(Linear(m_t)) of Sec. Encoder. */
@@ -111,10 +150,11 @@ typedef struct {
     const float *W1, *b1, *W2, *b2;
 } orc_params;
 
-static void orc_resolve(const float *blob, int n_layers, int d, orc_params *p) {
+static void orc_resolve(const float *blob, int n_layers, int d, int n_feat, orc_params *p) {
     size_t dd = (size_t)d, o = 0;
-    p->eW = blob + o; o += dd * 3;
-    p->eb = blob + o; o += dd;
+    p->eW = blob; /* the front end's first array (embed.W, or fe.lo) */
+    p->eb = blob + 3 * dd;
+    o += orc_front_size(d, n_feat);
     p->g = blob + o;
     p->inW = p->g + dd;
     p->inb = p->inW + 3 * dd * dd;
@@ -133,7 +173,8 @@ static void to_double(const float *src, size_t n, double *dst) {
 }
 
 /*
- * One track through the whole model.  hits: [L][3] float (x, y, z) in mm.
+ * One track through the whole model.  hits: [L][3] float (x, y, z) in mm, or
+ * with n_feat = F > 0 the [L][F] per-hit features of the Fourier front end.
  * out5 receives the five head outputs (d0, z0, phi, theta, q/p order).
  * pooled (length d) and resid ([L][d], the residual stream after the last
  * layer) are optional outputs for the tests.  states (length 2d, optional)
@@ -142,7 +183,7 @@ static void to_double(const float *src, size_t n, double *dst) {
  * the reverse state at the first hit.  Returns 0, or -1 if L < 1 (then out5,
  * pooled and states are NaN: the mean over zero hits is undefined).
  */
-int orc_track_forward(const float *hits, int L, int n_layers, int d, const float *blob,
+int orc_track_forward(const float *hits, int L, int n_feat, int n_layers, int d, const float *blob,
                       double *out5, double *pooled, double *resid, double *states) {
     if (L < 1) {
         for (int k = 0; k < 5; ++k) out5[k] = NAN;
@@ -153,26 +194,41 @@ int orc_track_forward(const float *hits, int L, int n_layers, int d, const float
         return -1;
     }
     orc_params P;
-    orc_resolve(blob, n_layers, d, &P);
+    orc_resolve(blob, n_layers, d, n_feat, &P);
     size_t Ld = (size_t)L * d, dd = (size_t)d;
-    double *buf = (double *)malloc(sizeof(double) * (7 * Ld + 3 * (size_t)L + 4 * dd * dd + 8 * dd + 16));
+    const size_t K = 2 * ORC_NSCALE * (size_t)(n_feat > 0 ? n_feat : 0); /* Fourier width */
+    size_t wmax = 4 * dd * dd > dd * K ? 4 * dd * dd : dd * K;
+    double *buf = (double *)malloc(sizeof(double) * (7 * Ld + 3 * (size_t)L + wmax + 8 * dd + K + 16));
     double *r = buf, *y = r + Ld, *x = y + Ld, *gh = x + Ld, *a = gh + Ld, *f = a + Ld, *b = f + Ld;
     double *u = b + Ld;
-    double *Wd = u + 3 * (size_t)L; /* weight staging in double, largest is out.W [d][2d] */
-    double *bd = Wd + 4 * dd * dd;  /* bias staging, up to 3d */
+    double *Wd = u + 3 * (size_t)L; /* weight staging in double: out.W [d][2d] or fe.W [d][32 F] */
+    double *bd = Wd + wmax;         /* bias staging, up to 3d */
     double *fb = bd + 4 * dd;       /* one [f; b] row, 2d */
     double *tmp = fb + 2 * dd;      /* d */
+    double *phi = tmp + dd;         /* one hit's Fourier features, 32 F */
 
-    /* Step 1: min-max normalise the coordinates to [0, 1] (Sec. Encoder). */
-    for (int t = 0; t < L; ++t) {
-        u[3 * t + 0] = ((double)hits[3 * t + 0] - ORC_XY_MIN) / ORC_XY_SPAN;
-        u[3 * t + 1] = ((double)hits[3 * t + 1] - ORC_XY_MIN) / ORC_XY_SPAN;
-        u[3 * t + 2] = ((double)hits[3 * t + 2] - ORC_Z_MIN) / ORC_Z_SPAN;
+    if (n_feat > 0) {
+        /* Steps 1-2, paper front end: Fourier features of each hit, then the
+         * dense projection to the encoder width (Sec. Encoder). */
+        const float *lo = blob, *hi = blob + n_feat, *fW = hi + n_feat, *fbias = fW + dd * K;
+        to_double(fW, dd * K, Wd);
+        to_double(fbias, dd, bd);
+        for (int t = 0; t < L; ++t) {
+            orc_fourier_features(hits + (size_t)t * n_feat, n_feat, lo, hi, phi);
+            orc_linear(Wd, bd, phi, 1, (int)K, d, r + (size_t)t * d);
+        }
+    } else {
+        /* Step 1: min-max normalise the coordinates to [0, 1] (Sec. Encoder). */
+        for (int t = 0; t < L; ++t) {
+            u[3 * t + 0] = ((double)hits[3 * t + 0] - ORC_XY_MIN) / ORC_XY_SPAN;
+            u[3 * t + 1] = ((double)hits[3 * t + 1] - ORC_XY_MIN) / ORC_XY_SPAN;
+            u[3 * t + 2] = ((double)hits[3 * t + 2] - ORC_Z_MIN) / ORC_Z_SPAN;
+        }
+        /* Step 2: dense projection to the encoder width d (Sec. Encoder). */
+        to_double(P.eW, dd * 3, Wd);
+        to_double(P.eb, dd, bd);
+        orc_linear(Wd, bd, u, L, 3, d, r);
     }
-    /* Step 2: dense projection to the encoder width d (Sec. Encoder). */
-    to_double(P.eW, dd * 3, Wd);
-    to_double(P.eb, dd, bd);
-    orc_linear(Wd, bd, u, L, 3, d, r);
 
     /* Step 3: the stacked bidirectional layers. */
     for (int l = 0; l < n_layers; ++l) {
@@ -236,11 +292,17 @@ int orc_track_forward(const float *hits, int L, int n_layers, int d, const float
  * n_threads <= 0 uses the OpenMP default.  Returns the number of tracks whose
  * length was below 1 (their outputs are NaN), or -1 for bad arguments.
  */
-long orc_fit_tracks(const float *hits, const int32_t *offsets, int32_t n_tracks, int n_layers,
+static size_t orc_model_size(int n_layers, int d, int n_feat) {
+    return n_feat > 0 ? orc_fourier_blob_size(n_layers, d, n_feat) : orc_blob_size(n_layers, d);
+}
+
+long orc_fit_tracks(const float *hits, int n_feat, const int32_t *offsets, int32_t n_tracks, int n_layers,
                     int d, const float *blob, size_t n_floats, double *out, int n_threads) {
-    if (n_tracks < 0 || d <= 0 || n_layers < 0 || !blob || (n_tracks > 0 && (!hits || !offsets || !out)))
+    if (n_tracks < 0 || d <= 0 || n_layers < 0 || n_feat < 0 || !blob ||
+        (n_tracks > 0 && (!hits || !offsets || !out)))
         return -1;
-    if (n_floats != orc_blob_size(n_layers, d)) return -1;
+    if (n_floats != orc_model_size(n_layers, d, n_feat)) return -1;
+    const size_t stride = n_feat > 0 ? (size_t)n_feat : 3;
     long bad = 0;
 #ifdef _OPENMP
     int nt = n_threads > 0 ? n_threads : omp_get_max_threads();
@@ -248,8 +310,8 @@ long orc_fit_tracks(const float *hits, const int32_t *offsets, int32_t n_tracks,
 #endif
     for (int32_t i = 0; i < n_tracks; ++i) {
         int L = offsets[i + 1] - offsets[i];
-        if (orc_track_forward(hits + (size_t)offsets[i] * 3, L, n_layers, d, blob, out + (size_t)i * 5,
-                              NULL, NULL, NULL) != 0)
+        if (orc_track_forward(hits + (size_t)offsets[i] * stride, L, n_feat, n_layers, d, blob,
+                              out + (size_t)i * 5, NULL, NULL, NULL) != 0)
             bad += 1;
     }
     (void)n_threads;
@@ -260,11 +322,13 @@ long orc_fit_tracks(const float *hits, const int32_t *offsets, int32_t n_tracks,
  * state at the last hit, reverse state at the first hit, of the last layer).
  * Returns the number of tracks with no hits (NaN rows), or -1 for bad
  * arguments.  With n_layers = 0 there are no states and every row is NaN. */
-long orc_track_states(const float *hits, const int32_t *offsets, int32_t n_tracks, int n_layers, int d,
-                      const float *blob, size_t n_floats, double *states, int n_threads) {
-    if (n_tracks < 0 || d <= 0 || n_layers < 0 || !blob || (n_tracks > 0 && (!hits || !offsets || !states)))
+long orc_track_states(const float *hits, int n_feat, const int32_t *offsets, int32_t n_tracks, int n_layers,
+                      int d, const float *blob, size_t n_floats, double *states, int n_threads) {
+    if (n_tracks < 0 || d <= 0 || n_layers < 0 || n_feat < 0 || !blob ||
+        (n_tracks > 0 && (!hits || !offsets || !states)))
         return -1;
-    if (n_floats != orc_blob_size(n_layers, d)) return -1;
+    if (n_floats != orc_model_size(n_layers, d, n_feat)) return -1;
+    const size_t stride = n_feat > 0 ? (size_t)n_feat : 3;
     long bad = 0;
 #ifdef _OPENMP
     int nt = n_threads > 0 ? n_threads : omp_get_max_threads();
@@ -276,8 +340,8 @@ long orc_track_states(const float *hits, const int32_t *offsets, int32_t n_track
         double *st = states + (size_t)i * 2 * d;
         if (n_layers == 0)
             for (int j = 0; j < 2 * d; ++j) st[j] = NAN;
-        if (orc_track_forward(hits + (size_t)offsets[i] * 3, L, n_layers, d, blob, out5, NULL, NULL,
-                              n_layers > 0 ? st : NULL) != 0)
+        if (orc_track_forward(hits + (size_t)offsets[i] * stride, L, n_feat, n_layers, d, blob, out5, NULL,
+                              NULL, n_layers > 0 ? st : NULL) != 0)
             bad += 1;
     }
     (void)n_threads;

@@ -33,6 +33,8 @@ __all__ = [
     "Workload", "WORKLOADS", "workload", "make_tracks", "make_track_chunk",
     "make_weights", "blob_layout", "blob_size", "round_to_bf16", "TRACK_CHUNK",
     "KAPPA_GEV_PER_T_M", "readout_layout", "make_readout_weights",
+    "FOURIER_WORKLOADS", "N_MEASURED", "measured_features", "feature_bounds", "fourier_layout",
+    "make_fourier_weights", "hit_features",
 ]
 
 # pT [GeV] = KAPPA * B [T] * R [m] for a unit-charge particle.
@@ -61,6 +63,7 @@ class Workload:
     pt_mode: str = "uniform_pt"   # "uniform_pt": pT~U(1,10); "uniform_invpt": 1/pT~U(0.1,1)
     eta_max: float = 1.5
     batch: int = 0        # tracks per fit_tracks call when the workload is streamed
+    n_features: int = 0   # > 0: per-hit features for the Fourier front end (12 measured + 3 seed)
 
     @property
     def data_seed(self) -> int:
@@ -88,6 +91,18 @@ WORKLOADS = {
 }
 
 
+# The same tracks and encoders with the paper's front end: 15 per-hit features
+# (12 measured stand-ins and the 3 seed residual features), Fourier-expanded.
+FOURIER_WORKLOADS = {
+    w.name: w for w in [
+        dataclasses.replace(WORKLOADS["tiny_d32_fp32"], name="fourier15_tiny_d32_fp32", n_features=15),
+        dataclasses.replace(WORKLOADS["d128x4_fp32_65k"], name="fourier15_d128x4_fp32_65k", n_features=15),
+        dataclasses.replace(WORKLOADS["deploy_d128x4_bf16_8m"], name="fourier15_deploy_d128x4_bf16_8m",
+                            n_features=15),
+    ]
+}
+
+
 def workload(name_or_index) -> Workload:
     if isinstance(name_or_index, Workload):
         return name_or_index
@@ -96,6 +111,8 @@ def workload(name_or_index) -> Workload:
             if w.index == name_or_index:
                 return w
         raise KeyError(name_or_index)
+    if name_or_index in FOURIER_WORKLOADS:
+        return FOURIER_WORKLOADS[name_or_index]
     return WORKLOADS[name_or_index]
 
 
@@ -330,3 +347,106 @@ def make_readout_weights(w, seed: int | None = None) -> np.ndarray:
             parts.append(rng.uniform(0.5, 1.5, n))
     blob = np.concatenate(parts).astype(np.float32)
     return round_to_bf16(blob) if w.dtype == "bf16" else blob
+
+
+# ----------------------------------------------------------------------------
+# Per-hit features of the paper's front end (inputs only: no arithmetic of the
+# method).  The paper's hits carry 12 measured features (position, derived
+# angles, detector identifiers) and three seed features; these are seeded
+# stand-ins with the same roles, computed from the generated hit positions.
+# ----------------------------------------------------------------------------
+
+N_MEASURED = 12
+MEASURED_NAMES = ("x", "y", "z", "r", "phi", "cot_theta", "layer", "phi_module", "z_module",
+                  "local_u", "local_v", "eta")
+Z_MODULE_MM = 100.0      # sensor length along z
+
+
+def _phi_modules(layer):
+    """Sensors around the barrel cylinder: more at larger radius."""
+    return 8 * (layer + 2)
+
+
+def measured_features(w, hits, offs) -> np.ndarray:
+    """float32 [H, 12]: x, y, z, r, phi, z/r, layer index, sensor index in phi
+    and in z, the hit's offsets from its sensor's centre (along r phi and z),
+    and asinh(z/r).  Hit t of a track lies on barrel layer t (tracks keep their
+    innermost layers)."""
+    w = workload(w)
+    h = np.asarray(hits, dtype=np.float64)
+    offs = np.asarray(offs, dtype=np.int64)
+    H = h.shape[0]
+    layer = np.arange(H) - np.repeat(offs[:-1] - offs[0], np.diff(offs))
+    x, y, z = h[:, 0], h[:, 1], h[:, 2]
+    r = np.hypot(x, y)
+    phi = np.arctan2(y, x)
+    nmod = _phi_modules(layer)
+    pm = np.floor((phi + np.pi) / (2 * np.pi) * nmod)
+    pm = np.minimum(pm, nmod - 1)
+    phic = -np.pi + (pm + 0.5) * 2 * np.pi / nmod
+    zm = np.floor((z + w.z_max) / Z_MODULE_MM)
+    zc = -w.z_max + (zm + 0.5) * Z_MODULE_MM
+    out = np.stack([x, y, z, r, phi, z / r, layer, pm, zm, r * (phi - phic), z - zc, np.arcsinh(z / r)], axis=1)
+    return np.ascontiguousarray(out, dtype=np.float32)
+
+
+def feature_bounds(w):
+    """(lo, hi) float32 [15]: min-max bounds of the 12 measured and the 3 seed
+    features (asinh dU, asinh dV of the residual in mm, up to ~27 mm on the
+    outer layers of a three-hit seed; helix path length in mm)."""
+    w = workload(w)
+    cot = np.sinh(w.eta_max + 0.1)
+    nmod = _phi_modules(w.n_det_layers - 1)
+    radii = np.linspace(w.r_min, w.r_max, w.n_det_layers)
+    half_u = 1.05 * float(np.max(np.pi * radii / _phi_modules(np.arange(w.n_det_layers))))
+    rb = 1.001 * w.r_max   # float32 rounding of hits on the outermost cylinder
+    lo = [-rb, -rb, -w.z_max, 0.0, -np.pi, -cot, 0.0, 0.0, 0.0, -half_u, -Z_MODULE_MM / 2,
+          -(w.eta_max + 0.1), -4.0, -4.0, 0.0]
+    hi = [rb, rb, w.z_max, rb, np.pi, cot, w.n_det_layers - 1, nmod - 1,
+          2 * w.z_max / Z_MODULE_MM - 1, half_u, Z_MODULE_MM / 2, w.eta_max + 0.1, 4.0, 4.0, 2.5 * w.r_max]
+    return np.array(lo, np.float32), np.array(hi, np.float32)
+
+
+def fourier_layout(n_layers: int, d: int, n_features: int):
+    """Blob of the model with the Fourier front end: the bounds, the dense
+    projection of the 32 F Fourier features (column 32 f + 16 c + s: c = 0
+    sine, 1 cosine, of pi 2^s u_f), then the encoder layers and head of
+    blob_layout."""
+    K = 32 * n_features
+    lay = [("fe.lo", (n_features,), 0, "lo"), ("fe.hi", (n_features,), 0, "hi"),
+           ("fe.W", (d, K), K, "w"), ("fe.b", (d,), K, "b")]
+    return lay + blob_layout(n_layers, d)[2:]
+
+
+def make_fourier_weights(w, seed: int | None = None) -> np.ndarray:
+    """float32 blob for a Fourier workload (bounds from feature_bounds; the rest
+    drawn like make_weights; matrices rounded to bf16 for a bf16 workload)."""
+    w = workload(w)
+    F = w.n_features
+    assert F == 15, "the feature generator provides 15 features"
+    rng = np.random.Generator(np.random.PCG64(w.weight_seed + 200 if seed is None else seed))
+    lo, hi = feature_bounds(w)
+    parts = []
+    for name, shape, fan_in, kind in fourier_layout(w.n_layers, w.d_model, F):
+        n = int(np.prod(shape))
+        if kind == "lo":
+            parts.append(lo.astype(np.float64))
+        elif kind == "hi":
+            parts.append(hi.astype(np.float64))
+        elif kind == "w":
+            parts.append(rng.normal(0.0, fan_in ** -0.5, n))
+        elif kind == "b":
+            parts.append(rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n))
+        else:
+            parts.append(rng.uniform(0.5, 1.5, n))
+    blob = np.concatenate(parts).astype(np.float32)
+    if w.dtype == "bf16":
+        blob[2 * F:] = round_to_bf16(blob[2 * F:])
+    return blob
+
+
+def hit_features(w, hits, offs, seed_features) -> np.ndarray:
+    """float32 [H, 15]: the 12 measured features and the 3 given seed
+    features (from the seed kernel or its oracle), in the blob's order."""
+    sf = np.asarray(seed_features, dtype=np.float32).reshape(-1, 3)
+    return np.ascontiguousarray(np.concatenate([measured_features(w, hits, offs), sf], axis=1))
