@@ -64,6 +64,14 @@ typedef struct {
                          supported (64 for d_model <= 128, 32 for 256).  Up to
                          32 selects the one-tile-per-wave kernel, which is
                          faster; longer tracks then get NaN and an error flag. */
+    int32_t n_features; /* 0: hits are (x, y, z) and the model embeds them
+                           linearly.  1..16: the paper's front end (Sec.
+                           Encoder): hits carry n_features values per hit, each
+                           min-max normalised, u = (x - lo) * (1 / (hi - lo))
+                           with every step rounded to float32, expanded to
+                           sin(pi 2^s u) and cos(pi 2^s u) for s = 0..15, and
+                           the 32 n_features values projected linearly to
+                           d_model.  Supported for d_model 32 and 128. */
 } tf_config;
 
 /* Opaque: device-resident weights in kernel order plus a sticky device error
@@ -80,13 +88,15 @@ typedef struct tf_weights tf_weights;
  * Rows 0..d-1 of in.W give the candidate, rows d..2d-1 the gate
  * pre-activation, rows 2d..3d-1 are unused.  Columns 0..d-1 of out.W read the
  * forward state, d..2d-1 the reverse state.  n_floats must equal
- * tf_blob_size(n_layers, d_model).  In the 16-bit modes the matrix values
- * should already be bf16-representable; others are rounded to nearest even.
+ * tf_blob_size(n_layers, d_model) (tf_fourier_blob_size with a Fourier front
+ * end).  In the 16-bit modes the matrix values should already be
+ * bf16-representable; others are rounded to nearest even.
  *
  * Ownership: host_blob is only read during the call.  *out receives a handle
  * the caller frees with tf_weights_destroy.  Synchronous.
- * Errors: TF_EINVAL (null pointers, bad sizes, max_hits < 0),
- * TF_EUNSUPPORTED (d_model, n_layers or max_hits outside the supported set),
+ * Errors: TF_EINVAL (null pointers, bad sizes, max_hits < 0, n_features < 0),
+ * TF_EUNSUPPORTED (d_model, n_layers, max_hits or n_features outside the
+ * supported set),
  * TF_ENOMEM, TF_EHIP.  On error *out is set to NULL.
  */
 tf_status tf_weights_create(const tf_config *cfg, const float *host_blob, size_t n_floats,
@@ -97,6 +107,14 @@ void tf_weights_destroy(tf_weights *w);
 
 /* Number of floats of the canonical blob for a model shape (0 if invalid). */
 size_t tf_blob_size(int32_t n_layers, int32_t d_model);
+
+/* Number of floats of the blob of a model with the Fourier front end over
+ * n_features (1..16) per-hit features, 0 if invalid.  Its order replaces
+ * embed.W and embed.b of the canonical blob by
+ *   fe.lo[F], fe.hi[F], fe.W[d][32 F], fe.b[d]
+ * where column 32 f + 16 c + s of fe.W reads sin (c = 0) or cos (c = 1) of
+ * pi 2^s u_f, the normalised feature f at scale s. */
+size_t tf_fourier_blob_size(int32_t n_layers, int32_t d_model, int32_t n_features);
 
 /* Longest track (in hits) the kernels accept for this handle: 32 or 64, from
  * tf_config.max_hits.  Longer tracks get NaN outputs and set
@@ -109,7 +127,8 @@ int32_t tf_max_hits(const tf_weights *w);
  * five perigee parameters out).
  *
  * hits     device, float32 [n_hits][3] = (x, y, z) in mm, time-ordered within
- *          each track.  Read only.
+ *          each track; with the Fourier front end [n_hits][n_features], the
+ *          per-hit features in the order of fe.lo / fe.hi.  Read only.
  * n_hits   rows of hits (bounds every read: a track whose rows leave
  *          [0, n_hits) gets NaN outputs and sets TF_DEVERR_BAD_OFFSETS).
  * offsets  device, int32 [n_tracks + 1]: track i owns rows

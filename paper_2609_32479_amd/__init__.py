@@ -28,7 +28,7 @@ MODE_FOR_WEIGHTS = {"fp32": "fp32", "bf16": "bf16_f16act"}
 DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS = 1, 2, 4
 SEED_TOO_SHORT, SEED_NO_CIRCLE, SEED_BAD_OFFSETS = 1, 2, 4
 
-EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_max_hits",
+EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_fourier_blob_size", "tf_max_hits",
             "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks", "fit_tracks_states",
             "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks")
 
@@ -41,7 +41,7 @@ class TrackfitError(RuntimeError):
 
 class Config(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32),
-                ("dtype", ctypes.c_int32), ("max_hits", ctypes.c_int32)]
+                ("dtype", ctypes.c_int32), ("max_hits", ctypes.c_int32), ("n_features", ctypes.c_int32)]
 
 
 _lib = None
@@ -61,6 +61,8 @@ def lib():
         L.tf_weights_destroy.argtypes = [vp]
         L.tf_blob_size.restype = ctypes.c_size_t
         L.tf_blob_size.argtypes = [ctypes.c_int32, ctypes.c_int32]
+        L.tf_fourier_blob_size.restype = ctypes.c_size_t
+        L.tf_fourier_blob_size.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32]
         L.tf_max_hits.restype = ctypes.c_int32
         L.tf_max_hits.argtypes = [vp]
         L.fit_tracks.restype = ctypes.c_int
@@ -97,7 +99,9 @@ def _check(status: int, what: str):
         raise TrackfitError(status, what)
 
 
-def blob_size(n_layers: int, d_model: int) -> int:
+def blob_size(n_layers: int, d_model: int, n_features: int = 0) -> int:
+    if n_features:
+        return int(lib().tf_fourier_blob_size(int(n_layers), int(d_model), int(n_features)))
     return int(lib().tf_blob_size(int(n_layers), int(d_model)))
 
 
@@ -110,17 +114,20 @@ def _stream_handle(stream) -> int:
 class Weights:
     """Device-resident weights (tf_weights handle) on the current device."""
 
-    def __init__(self, blob, n_layers: int, d_model: int, dtype: str = "fp32", max_hits: int = 0):
+    def __init__(self, blob, n_layers: int, d_model: int, dtype: str = "fp32", max_hits: int = 0,
+                 n_features: int = 0):
         """dtype: "fp32", "bf16" or "bf16_f16act" (library modes, include/trackfit.h);
-        max_hits: longest track that will be passed (0: the largest supported)."""
+        max_hits: longest track that will be passed (0: the largest supported);
+        n_features: per-hit features of the Fourier front end (0: hits are x, y, z)."""
         import numpy as np
         arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
-        cfg = Config(int(n_layers), int(d_model), DTYPES[dtype], int(max_hits))
+        cfg = Config(int(n_layers), int(d_model), DTYPES[dtype], int(max_hits), int(n_features))
         h = ctypes.c_void_p()
         _check(lib().tf_weights_create(ctypes.byref(cfg), arr.ctypes.data, arr.size, ctypes.byref(h)),
                "tf_weights_create")
         self._h = h
         self.n_layers, self.d_model, self.dtype = int(n_layers), int(d_model), dtype
+        self.n_features = int(n_features)
         self.max_hits = int(lib().tf_max_hits(h))
 
     @property
@@ -139,7 +146,7 @@ class Weights:
             pass
 
 
-def _batch(hits: torch.Tensor, offsets: torch.Tensor, n_tracks: int | None) -> int:
+def _batch(hits: torch.Tensor, offsets: torch.Tensor, n_tracks: int | None, width: int = 3) -> int:
     """Check a packed batch's tensors; returns the number of tracks."""
     if not (hits.is_cuda and offsets.is_cuda):
         raise ValueError("hits and offsets must be GPU tensors")
@@ -147,8 +154,8 @@ def _batch(hits: torch.Tensor, offsets: torch.Tensor, n_tracks: int | None) -> i
         raise TypeError("hits must be float32 and offsets int32")
     if not (hits.is_contiguous() and offsets.is_contiguous()):
         raise ValueError("hits and offsets must be contiguous")
-    if hits.dim() != 2 or hits.shape[1] != 3:
-        raise ValueError("hits must have shape [H, 3]")
+    if hits.dim() != 2 or hits.shape[1] != width:
+        raise ValueError(f"hits must have shape [H, {width}]")
     n = offsets.numel() - 1 if n_tracks is None else int(n_tracks)
     if n < 0 or n + 1 > offsets.numel():
         raise ValueError("n_tracks does not fit the offsets array")
@@ -172,7 +179,7 @@ def fit_tracks(hits: torch.Tensor, offsets: torch.Tensor, weights: Weights, out:
     defaults to offsets.numel() - 1 (a prefix of a longer offsets array may be
     given instead).
     """
-    n = _batch(hits, offsets, n_tracks)
+    n = _batch(hits, offsets, n_tracks, weights.n_features or 3)
     out = _out(out, n, 5, hits.device)
     _check(lib().fit_tracks(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, weights.handle,
                             out.data_ptr(), _stream_handle(stream)), "fit_tracks")
@@ -184,7 +191,7 @@ def fit_tracks_states(hits: torch.Tensor, offsets: torch.Tensor, weights: Weight
     """Enqueue the encoder up to the last layer's scans; returns float32
     [N, 2d]: the forward state at each track's last hit, then the reverse
     state at its first hit (the paper's readout input)."""
-    n = _batch(hits, offsets, n_tracks)
+    n = _batch(hits, offsets, n_tracks, weights.n_features or 3)
     out = _out(out, n, 2 * weights.d_model, hits.device)
     _check(lib().fit_tracks_states(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, weights.handle,
                                    out.data_ptr(), _stream_handle(stream)), "fit_tracks_states")

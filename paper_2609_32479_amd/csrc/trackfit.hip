@@ -43,6 +43,7 @@
 //    the second head GEMM straight from the accumulators.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdint>
 #include <cstring>
@@ -189,11 +190,18 @@ template <> struct Frag<OP_F32> {
 
 // Device-side weights.
 struct DevParams {
-    const float4 *emb;           // [D] (w_x, w_y, w_z, b) with the min-max map folded in
+    const float4 *emb;           // [D] (w_x, w_y, w_z, b) with the min-max map folded in; with
+                                 // the Fourier front end: bias [D], lo [16], 1 / (hi - lo) [16]
     const unsigned char *stages; // n_stages x STAGE bytes, in the order the kernel walks them
     int n_layers;
-    int n_stages;                // (MERGE ? 1 : 2) * n_layers * NCH + NH1 + 1
+    int n_stages;                // n_fstages + (MERGE ? 1 : 2) * n_layers * NCH + NH1 + 1
+    int n_feat;                  // per-hit features of the Fourier front end (0: x, y, z)
+    int n_fstages;               // stages of the front end's dense projection
+    int kpf;                     // k-steps of that projection per stage
 };
+
+constexpr int kMaxFeat = 16;     // per-hit features of the Fourier front end, at most
+constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
 
 __device__ __forceinline__ void wave_lds_sync() {
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
@@ -319,7 +327,13 @@ __device__ __forceinline__ void wait_vmcnt() {
 // state at the track's last hit in columns 0..d-1 and the reverse state at its
 // first hit in columns d..2d-1.  The last layer's output projection and the
 // head, whose results nothing reads in this form, are skipped.
-template <int D, int OP, int HT_, bool STATES>
+// FOURIER: the paper's front end instead of the (x, y, z) embedding: hits holds
+// n_feat features per hit, each min-max normalised in fp32 and expanded to
+// sin and cos of pi 2^s u, s = 0..15, and the 32 n_feat values are projected
+// to d on the matrix cores (the projection's weights stream through the stage
+// ring ahead of the first layer's).  Column k of that projection is feature
+// k / 32, cosine if bit 4 of k is set, scale k % 16.
+template <int D, int OP, int HT_, bool STATES, bool FOURIER>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
                           amdgpu_waves_per_eu(KCfg<D, OP, HT_>::WAVES / 4, KCfg<D, OP, HT_>::WAVES / 4)))
 void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
@@ -499,6 +513,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             eb1 = unsigned(emask >> SP) & spm;
             wave_lds_sync();  // the track table is written
 
+            if constexpr (!FOURIER) {
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
@@ -519,6 +534,85 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         const float4 e = emb[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
                         r[m][nt][q] = fmaf(e.x, hx, fmaf(e.y, hy, fmaf(e.z, hz, e.w)));
                     }
+            }
+            } else {
+            // Fourier front end, part 1: the normalised features u = (x - lo) * (1 / (hi - lo))
+            // (each step rounded to fp32) of hit slot 32 nt + cc to the wave's scratch, lane half
+            // hh taking features 8 hh .. 8 hh + 7; r starts at the projection's bias
+            const float *fe = reinterpret_cast<const float *>(smem);  // bias [D], lo [16], inv [16]
+            float *us = stage;                                        // [CAP][kUStride]
+            const int nf = P.n_feat;
+#pragma unroll
+            for (int nt = 0; nt < HT; ++nt) {
+                const int sl = 32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31);
+                const int th = slot_to_hit<SP>(sl);
+                const float *hp = nullptr;
+                if (th < n) {
+                    const int j = __builtin_popcountll(smask & ((2ull << th) - 1ull)) - 1;
+                    hp = hits + ((size_t)t_off[j] + (th - t_start[j])) * nf;
+                }
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    const int f = 8 * hh + e;
+                    if (f < nf) us[sl * kUStride + f] = hp ? (hp[f] - fe[D + f]) * fe[D + kMaxFeat + f] : 0.f;
+                }
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) r[m][nt][q] = fe[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+            }
+            wave_lds_sync();  // the features are in the scratch
+            }
+        }
+        if constexpr (FOURIER) {
+            // Fourier front end, part 2: k-step ks of the dense projection takes, for each
+            // hit slot, the KL Fourier features k = ks K + hh KL + e (column k of the
+            // projection), formed in registers: sin or cos of pi 2^s u_f
+            const float *us = stage;
+            const int kf = 32 * P.n_feat / K;  // k-steps of the projection
+            for (int js = 0; js < P.n_fstages; ++js) {
+                if (work) {
+                    const FT *wfr = reinterpret_cast<const FT *>(slot());
+                    const int k0 = js * P.kpf;
+                    const int kn = kf - k0 < P.kpf ? kf - k0 : P.kpf;
+                    __builtin_amdgcn_s_setprio(1);
+                    for (int kl = 0; kl < kn; ++kl) {
+                        const int ks = k0 + kl;
+                        FT bv[HT];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) {
+                            const int sl = 32 * nt + cc;
+                            float v[8];
+                            if constexpr (C::HALF) {
+                                // feature ks / 2, sine (even ks) or cosine, scales 8 hh + e: in
+                                // revolutions, sin(pi 2^s u) = sin(2 pi frac(2^(s - 1) u)); the
+                                // products by powers of two and the fraction are exact
+                                const float u = us[sl * kUStride + (ks >> 1)];
+                                const float w0 = u * (hh ? 128.0f : 0.5f);
+#pragma unroll
+                                for (int e = 0; e < 8; ++e) {
+                                    const float x = __builtin_amdgcn_fractf(w0 * (float)(1 << e));
+                                    v[e] = (ks & 1) ? __builtin_amdgcn_cosf(x) : __builtin_amdgcn_sinf(x);
+                                }
+                            } else {
+                                // one feature per lane and k-step; the library's sinpi/cospi
+                                // reduce the exact argument 2^s u exactly
+                                const int k = ks * K + hh;
+                                const float x = ldexpf(us[sl * kUStride + (k >> 5)], k & 15);
+                                v[0] = ((k >> 4) & 1) ? cospif(x) : sinpif(x);
+                            }
+                            bv[nt] = F::pack(v);
+                        }
+#pragma unroll
+                        for (int m = 0; m < MT; ++m) {
+                            const FT a = wfr[(kl * MT + m) * 64 + lane];
+#pragma unroll
+                            for (int nt = 0; nt < HT; ++nt) r[m][nt] = F::mma(a, bv[nt], r[m][nt]);
+                        }
+                    }
+                    __builtin_amdgcn_s_setprio(0);
+                }
+                advance(false);
             }
         }
 
@@ -1026,7 +1120,7 @@ Geom geom_d(int D, int ht) {
 }  // namespace
 
 struct tf_weights {
-    int n_layers = 0, d = 0, dtype = 0, max_hits = 0, device = 0, cu_count = 0;
+    int n_layers = 0, d = 0, dtype = 0, max_hits = 0, device = 0, cu_count = 0, n_feat = 0;
     void *dmem = nullptr;
     int *err = nullptr;
     DevParams params{};
@@ -1039,6 +1133,14 @@ extern "C" size_t tf_blob_size(int32_t n_layers, int32_t d) {
     return 4 * dd + (size_t)n_layers * per_layer + dd * dd + dd + 5 * dd + 5;
 }
 
+extern "C" size_t tf_fourier_blob_size(int32_t n_layers, int32_t d, int32_t n_features) {
+    if (n_features <= 0 || n_features > kMaxFeat) return 0;
+    const size_t base = tf_blob_size(n_layers, d);
+    if (!base) return 0;
+    const size_t dd = (size_t)d, F = (size_t)n_features;
+    return base - 4 * dd + 2 * F + dd * 32 * F + dd;
+}
+
 extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, size_t n_floats,
                                        tf_weights **out) {
     if (!out) return TF_EINVAL;
@@ -1046,9 +1148,11 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     if (!cfg || !blob || cfg->max_hits < 0) return TF_EINVAL;
     const int L = cfg->n_layers, D = cfg->d_model;
     if (cfg->dtype != TF_FP32 && cfg->dtype != TF_BF16 && cfg->dtype != TF_BF16_F16ACT) return TF_EINVAL;
-    if (L < 0 || D <= 0) return TF_EINVAL;
+    if (L < 0 || D <= 0 || cfg->n_features < 0) return TF_EINVAL;
     if (!(D == 32 || D == 64 || D == 128 || D == 256) || L > 64) return TF_EUNSUPPORTED;
-    if (n_floats != tf_blob_size(L, D)) return TF_EINVAL;
+    const int NFEAT = cfg->n_features;
+    if (NFEAT > kMaxFeat || (NFEAT > 0 && D != 32 && D != 128)) return TF_EUNSUPPORTED;
+    if (n_floats != (NFEAT ? tf_fourier_blob_size(L, D, NFEAT) : tf_blob_size(L, D))) return TF_EINVAL;
     const int op = cfg->dtype == TF_BF16 ? OP_BF16 : cfg->dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32;
     const bool half = op != OP_F32;
     if (!half && D > 128) return TF_EUNSUPPORTED;  // fp32 stages of d = 256 do not fit in LDS
@@ -1061,27 +1165,60 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const int MT = D / 32, NCH = D / 32;
     const double gs = half ? -1.4426950408889634 : 1.0;  // 16-bit modes evaluate exp2
 
-    // blob views
+    // blob views; the front end (x, y, z embedding, or the Fourier front end's
+    // bounds, dense projection and bias) precedes the layers
     const size_t dd = (size_t)D;
     const float *eW = blob, *eb = blob + 3 * dd;
+    const size_t KF32 = 32 * (size_t)NFEAT;  // Fourier features per hit
+    const float *f_lo = blob, *f_hi = blob + NFEAT, *fW = blob + 2 * NFEAT, *fB = fW + dd * KF32;
+    const size_t front = NFEAT ? 2 * (size_t)NFEAT + dd * KF32 + dd : 4 * dd;
     const size_t lstride = dd + 3 * dd * dd + 3 * dd + dd * 2 * dd + dd;
-    auto g_of = [&](int l) { return blob + 4 * dd + (size_t)l * lstride; };
+    auto g_of = [&](int l) { return blob + front + (size_t)l * lstride; };
     auto inW_of = [&](int l) { return g_of(l) + dd; };
     auto inb_of = [&](int l) { return inW_of(l) + 3 * dd * dd; };
     auto outW_of = [&](int l) { return inb_of(l) + 3 * dd; };
     auto outb_of = [&](int l) { return outW_of(l) + dd * 2 * dd; };
-    const float *W1 = blob + 4 * dd + (size_t)L * lstride;
+    const float *W1 = blob + front + (size_t)L * lstride;
     const float *b1 = W1 + dd * dd, *W2 = b1 + dd, *b2 = W2 + 5 * dd;
 
-    const int n_stages = (G.merge ? 1 : 2) * L * NCH + G.nh1 + 1;
+    // the Fourier front end's projection: KF k-steps of MT fragments, KPF per stage
+    const int frag_bytes = 64 * KL * (half ? 2 : 4);
+    const int KF = NFEAT ? (int)(KF32 / K) : 0;
+    const int KPF = NFEAT ? std::min(KF, G.stage / (MT * frag_bytes)) : 1;
+    const int NFS = NFEAT ? (KF + KPF - 1) / KPF : 0;
+    const int n_stages = NFS + (G.merge ? 1 : 2) * L * NCH + G.nh1 + 1;
     const size_t emb_bytes = (size_t)D * 16;
     const size_t emb_off = 0, st_off = (emb_bytes + 255) & ~size_t(255);
     const size_t err_off = st_off + (size_t)n_stages * G.stage;
     const size_t total = err_off + 256;
     std::vector<unsigned char> hb(total, 0);
 
-    // embedding with u = (x - lo) / span folded in: r = (W/span) x + (b - W lo / span)
-    {
+    int s = 0;
+    if (NFEAT) {
+        // bias [D], lo [16], 1 / (hi - lo) [16] (fp32: the divisor and the quotient each
+        // rounded to float32, as the kernel's normalisation takes them)
+        StageWriter w{OP_F32, hb.data() + emb_off};
+        for (int c = 0; c < D; ++c) w.f32(fB[c]);
+        for (int f = 0; f < kMaxFeat; ++f) w.f32(f < NFEAT ? f_lo[f] : 0.0);
+        for (int f = 0; f < kMaxFeat; ++f) {
+            const float span = f < NFEAT ? f_hi[f] - f_lo[f] : 1.0f;
+            const float inv = 1.0f / span;
+            w.f32(inv);
+        }
+        // projection A fragments: lane (g, c) value e of k-step ks, block m holds
+        // fe.W[channel 32 m + c][column ks K + g KL + e]
+        for (int js = 0; js < NFS; ++js) {
+            StageWriter ws{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            for (int kl = 0; kl < KPF && js * KPF + kl < KF; ++kl)
+                for (int m = 0; m < MT; ++m)
+                    for (int lane = 0; lane < 64; ++lane)
+                        for (int e = 0; e < KL; ++e) {
+                            const size_t col = (size_t)(js * KPF + kl) * K + (lane / 32) * KL + e;
+                            ws.elem(fW[(size_t)(32 * m + lane % 32) * KF32 + col]);
+                        }
+        }
+    } else {
+        // embedding with u = (x - lo) / span folded in: r = (W/span) x + (b - W lo / span)
         StageWriter w{OP_F32, hb.data() + emb_off};
         const double lo[3] = {-1000.0, -1000.0, -3000.0}, span[3] = {2000.0, 2000.0, 6000.0};
         for (int c = 0; c < D; ++c) {
@@ -1093,7 +1230,6 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
             w.f32(b);
         }
     }
-    int s = 0;
     for (int l = 0; l < L; ++l) {
         const float *Wi = inW_of(l), *g = g_of(l), *bi = inb_of(l), *Wo = outW_of(l), *bo = outb_of(l);
         for (int ch = 0; ch < NCH; ++ch) {
@@ -1215,8 +1351,12 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     wt->err = reinterpret_cast<int *>(b + err_off);
     wt->params.emb = reinterpret_cast<const float4 *>(b + emb_off);
     wt->params.stages = reinterpret_cast<const unsigned char *>(b + st_off);
+    wt->n_feat = NFEAT;
     wt->params.n_layers = L;
     wt->params.n_stages = n_stages;
+    wt->params.n_feat = NFEAT;
+    wt->params.n_fstages = NFS;
+    wt->params.kpf = KPF;
     (void)KS2;
     *out = wt;
     return TF_OK;
@@ -1232,7 +1372,7 @@ extern "C" void tf_weights_destroy(tf_weights *w) {
 extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
 
 namespace {
-template <int D, int OP, int HT, bool STATES>
+template <int D, int OP, int HT, bool STATES, bool FOURIER>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                   const tf_weights *w, float *out, hipStream_t stream) {
     using C = KCfg<D, OP, HT>;
@@ -1243,28 +1383,32 @@ hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int
     const long long cap = (long long)w->cu_count;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, STATES>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, STATES, FOURIER>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
                        hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, w->err);
     return hipGetLastError();
 }
 
-template <int D, int OP, bool STATES>
+template <int D, int OP, bool STATES, bool FOURIER>
 hipError_t launch_ht(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                      const tf_weights *w, float *out, hipStream_t stream) {
     if constexpr (D <= 128) {
-        if (w->max_hits == 64) return launch<D, OP, 2, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        if (w->max_hits == 64)
+            return launch<D, OP, 2, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
     }
-    return launch<D, OP, 1, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    return launch<D, OP, 1, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
 }
 
-template <int D, bool STATES>
+template <int D, bool STATES, bool FOURIER>
 hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                     const tf_weights *w, float *out, hipStream_t stream) {
     switch (w->dtype) {
-        case TF_BF16: return launch_ht<D, OP_BF16, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
-        case TF_BF16_F16ACT: return launch_ht<D, OP_F16, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16:
+            return launch_ht<D, OP_BF16, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+        case TF_BF16_F16ACT:
+            return launch_ht<D, OP_F16, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
         default:
-            if constexpr (D <= 128) return launch_ht<D, OP_F32, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            if constexpr (D <= 128)
+                return launch_ht<D, OP_F32, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
             return hipErrorNotSupported;
     }
 }
@@ -1273,11 +1417,20 @@ template <bool STATES>
 tf_status launch_any(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                      const tf_weights *w, float *out, hipStream_t stream) {
     hipError_t e;
+    if (w->n_feat > 0) {
+        // the Fourier front end is built for the paper's width (128) and the small test width
+        switch (w->d) {
+            case 32: e = launch_d<32, STATES, true>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+            case 128: e = launch_d<128, STATES, true>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+            default: return TF_EUNSUPPORTED;
+        }
+        return e == hipSuccess ? TF_OK : TF_EHIP;
+    }
     switch (w->d) {
-        case 32: e = launch_d<32, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 64: e = launch_d<64, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 128: e = launch_d<128, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 256: e = launch_d<256, STATES>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 32: e = launch_d<32, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 64: e = launch_d<64, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 128: e = launch_d<128, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+        case 256: e = launch_d<256, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
         default: return TF_EUNSUPPORTED;
     }
     return e == hipSuccess ? TF_OK : TF_EHIP;
