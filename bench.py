@@ -46,16 +46,60 @@ TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "batch": 262144, "calls_per_step
 STATES_TRAFFIC = dict(TRAFFIC, fetch_bytes=55189391, write_bytes=269221888)
 
 
-def algorithmic_flops(n_layers, d, n_hits, n_tracks):
+def front_flops(d, n_hits, n_features=0):
+    """The front end: 6 d per hit for the 3->d embedding, or 2 x 32 F x d per
+    hit for the Fourier front end's dense projection (its sines and cosines
+    are not counted)."""
+    return (64.0 * n_features * d if n_features else 6.0 * d) * n_hits
+
+
+def algorithmic_flops(n_layers, d, n_hits, n_tracks, n_features=0):
     """8 d^2 per hit and layer (candidate + gate projections: 2 * d * 2d, merge:
-    2 * 2d * d), 6 d per hit for the 3->d embedding, 2 d^2 + 10 d per track for
-    the head.  The unused third of the input projection is not counted."""
-    return 8.0 * d * d * n_layers * n_hits + 6.0 * d * n_hits + (2.0 * d * d + 10.0 * d) * n_tracks
+    2 * 2d * d), the front end, 2 d^2 + 10 d per track for the head.  The
+    unused third of the input projection is not counted."""
+    return 8.0 * d * d * n_layers * n_hits + front_flops(d, n_hits, n_features) + (2.0 * d * d + 10.0 * d) * n_tracks
 
 
-def algorithmic_bytes(n_hits, n_tracks):
-    """12 B per hit read, 4 B per track of offsets, 20 B per track written."""
-    return 12.0 * n_hits + 4.0 * (n_tracks + 1) + 20.0 * n_tracks
+def algorithmic_bytes(n_hits, n_tracks, n_features=0):
+    """12 B per hit read (4 F B with the Fourier front end), 4 B per track of
+    offsets, 20 B per track written."""
+    return 4.0 * (n_features or 3) * n_hits + 4.0 * (n_tracks + 1) + 20.0 * n_tracks
+
+
+def model_blob(w):
+    return ts.make_fourier_weights(w) if w.n_features else ts.make_weights(w)
+
+
+def device_features(tf, w, hits, offs, h, o, dev):
+    """The Fourier front end's per-hit feature rows on the device: the 12
+    measured features from the generator (in chunks of tracks), then the
+    GPU seed writes its 3 residual features into columns 12..14."""
+    import torch
+    n = offs.size - 1
+    feats = torch.empty((int(offs[-1] - offs[0]), w.n_features), dtype=torch.float32, device=dev)
+    step = 1 << 20
+    for i0 in range(0, n, step):
+        i1 = min(n, i0 + step)
+        a, b = int(offs[i0] - offs[0]), int(offs[i1] - offs[0])
+        m = ts.measured_features(w, hits[a:b], offs[i0:i1 + 1])
+        feats[a:b, :ts.N_MEASURED] = torch.from_numpy(m).to(dev)
+    seeds = torch.empty((n, 5), dtype=torch.float64, device=dev)
+    tf.seed_tracks(h, o, w.b_field, seeds=seeds, feats=feats[:, ts.N_MEASURED:ts.N_MEASURED + 3])
+    torch.cuda.synchronize()
+    return feats
+
+
+def oracle_inputs(w, hits, offs, sel):
+    """A sample's packed hits (or, with the Fourier front end, its feature rows
+    with the oracle's own seed features) and offsets, for the CPU baseline."""
+    import oracle
+    L = offs[sel + 1] - offs[sel]
+    h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+    o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+    if not w.n_features:
+        return h, o
+    _, sf, _ = oracle.seed_tracks(h, o, w.b_field)
+    return ts.hit_features(w, h, o, np.nan_to_num(sf, nan=0.0)), o
 
 
 def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
@@ -67,11 +111,9 @@ def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
     idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
 
     def run(sel):
-        L = offs[sel + 1] - offs[sel]
-        h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
-        o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
         t0 = time.perf_counter()
-        out = oracle.fit_tracks(h, o, blob, w.n_layers, w.d_model, n_threads=threads)
+        h, o = oracle_inputs(w, hits, offs, sel)   # the oracle's seed features are part of its chain
+        out = oracle.fit_tracks(h, o, blob, w.n_layers, w.d_model, n_threads=threads, n_features=w.n_features)
         return out, time.perf_counter() - t0
 
     _, dt = run(idx)
@@ -212,11 +254,11 @@ READOUT_METRIC = ("tracks/sec (seed + encoder end states + 35-quantile readout, 
                   "MFMA util vs peak")
 
 
-def states_algorithmic_flops(n_layers, d, n_hits):
+def states_algorithmic_flops(n_layers, d, n_hits, n_features=0):
     """Encoder up to the last layer's scans: 8 d^2 per hit for each layer but
     the last, 4 d^2 per hit for the last (candidate and gate projections; its
-    merge is not evaluated), 6 d per hit for the embedding."""
-    return 8.0 * d * d * (n_layers - 1) * n_hits + 4.0 * d * d * n_hits + 6.0 * d * n_hits
+    merge is not evaluated), and the front end."""
+    return 8.0 * d * d * (n_layers - 1) * n_hits + 4.0 * d * d * n_hits + front_flops(d, n_hits, n_features)
 
 
 def readout_algorithmic_flops(d, n_tracks):
@@ -236,8 +278,9 @@ def readout_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
         h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
         o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
         t0 = time.perf_counter()
-        seeds, _, _ = oracle.seed_tracks(h, o, w.b_field, features=False)
-        st = oracle.track_states(h, o, blob, w.n_layers, w.d_model, n_threads=threads)
+        seeds, sf, _ = oracle.seed_tracks(h, o, w.b_field, features=bool(w.n_features))
+        inp = ts.hit_features(w, h, o, np.nan_to_num(sf, nan=0.0)) if w.n_features else h
+        st = oracle.track_states(inp, o, blob, w.n_layers, w.d_model, n_threads=threads, n_features=w.n_features)
         _, out = oracle.readout_tracks(st, seeds, hb, w.d_model)
         return out, time.perf_counter() - t0
 
@@ -265,10 +308,14 @@ def bench_readout(args, w, hits, offs, mode, batch):
     n_tracks = offs.size - 1
     n_hits = int(offs[-1] - offs[0])
     d = w.d_model
-    blob = ts.make_weights(w)
+    blob = model_blob(w)
     hb = ts.make_readout_weights(w)
-    W = tf.Weights(blob, w.n_layers, d, mode, max_hits=args.max_hits or w.len_max)
+    W = tf.Weights(blob, w.n_layers, d, mode, max_hits=args.max_hits or w.len_max, n_features=w.n_features)
     R = tf.Readout(hb, d, mode)
+    # the Fourier front end reads per-hit feature rows: the measured columns are
+    # inputs; the seed fills columns 12..14 of each batch's rows inside the step
+    feats = device_features(tf, w, hits, offs, h, o, dev) if w.n_features else None
+    inp = feats if w.n_features else h
     seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
     out = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
     states = torch.empty((batch, 2 * d), dtype=torch.float32, device=dev)  # reused by every batch
@@ -276,8 +323,13 @@ def bench_readout(args, w, hits, offs, mode, batch):
 
     def one(s0, stream):
         n = min(batch, n_tracks - s0)
-        tf.seed_tracks(h, o[s0:], w.b_field, features=False, seeds=seeds[s0:], n_tracks=n, stream=stream)
-        tf.fit_tracks_states(h, o[s0:], W, out=states, n_tracks=n, stream=stream)
+        if feats is not None:
+            r0 = int(offs[s0] - offs[0])
+            tf.seed_tracks(h, o[s0:], w.b_field, seeds=seeds[s0:], n_tracks=n, stream=stream,
+                           feats=feats[r0:, ts.N_MEASURED:ts.N_MEASURED + 3])
+        else:
+            tf.seed_tracks(h, o[s0:], w.b_field, features=False, seeds=seeds[s0:], n_tracks=n, stream=stream)
+        tf.fit_tracks_states(inp, o[s0:], W, out=states, n_tracks=n, stream=stream)
         tf.decode_tracks(states[:n], seeds[s0:s0 + n], R, out=out[s0:], stream=stream)
 
     def step(stream=None):
@@ -291,7 +343,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in starts]
     for (a, b), s0 in zip(ev, starts):
         a.record()
-        tf.fit_tracks_states(h, o[s0:], W, out=states, n_tracks=min(batch, n_tracks - s0))
+        tf.fit_tracks_states(inp, o[s0:], W, out=states, n_tracks=min(batch, n_tracks - s0))
         b.record()
     torch.cuda.synchronize()
     launch_ms = np.array([a.elapsed_time(b) for a, b in ev])
@@ -327,7 +379,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
     ms_per_step = e0.elapsed_time(e1) / args.steps
     flags = tf.device_error(W)
     gpu_out = out.cpu().numpy()
-    per_launch_flops = states_algorithmic_flops(w.n_layers, d, n_hits) / len(starts)
+    per_launch_flops = states_algorithmic_flops(w.n_layers, d, n_hits, w.n_features) / len(starts)
     kernel_ms = float(launch_ms.mean())
     achieved = per_launch_flops / (kernel_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[mode]
@@ -342,6 +394,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
         "data": "synthetic helix tracks (2 T solenoid, seeded), random-init weights",
         "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
                    "launches_per_call": 3, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": d, "mode": mode,
+                   "n_features": w.n_features,
                    "max_hits": W.max_hits, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": traffic_bytes(w, batch, len(starts), STATES_TRAFFIC),
@@ -375,7 +428,8 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="deploy_d128x4_bf16_8m", choices=list(ts.WORKLOADS))
+    ap.add_argument("--workload", default="deploy_d128x4_bf16_8m",
+                    choices=list(ts.WORKLOADS) + list(ts.FOURIER_WORKLOADS))
     ap.add_argument("--mode", default=None, help="library mode: fp32, bf16 or bf16_f16act")
     ap.add_argument("--n-tracks", type=int, default=None, help="override the workload's track count")
     ap.add_argument("--batch", type=int, default=None, help="tracks per fit_tracks call")
@@ -417,13 +471,16 @@ def main():
     if args.path == "readout":
         bench_readout(args, w, hits, offs, mode, batch)
         return
-    blob = ts.make_weights(w)
+    blob = model_blob(w)
 
     dev = torch.device("cuda:0")
     h = torch.from_numpy(hits).to(dev)
     o = torch.from_numpy(offs).to(dev)
     out = torch.empty((n_tracks, 5), dtype=torch.float32, device=dev)
-    W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=args.max_hits or w.len_max)
+    W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=args.max_hits or w.len_max, n_features=w.n_features)
+    # with the Fourier front end the kernel reads per-hit feature rows (inputs,
+    # resident before the timed region like the hits)
+    h = device_features(tf, w, hits, offs, h, o, dev) if w.n_features else h
     starts = list(range(0, n_tracks, batch))
 
     def step(stream=None):
@@ -478,13 +535,13 @@ def main():
     flags = tf.device_error(W)
     gpu_out = out.cpu().numpy()
     n_hits = int(offs[-1] - offs[0])
-    flops_step = algorithmic_flops(w.n_layers, w.d_model, n_hits, n_tracks)
+    flops_step = algorithmic_flops(w.n_layers, w.d_model, n_hits, n_tracks, w.n_features)
     # dominant (only) kernel: algorithmic flops of one launch / its mean duration
     per_launch_flops = flops_step / len(starts)
     kernel_ms = float(launch_ms.mean())
     achieved_tflops = per_launch_flops / (kernel_ms / 1e3) / 1e12
     peak = PEAK_TFLOPS[mode]
-    bytes_step = algorithmic_bytes(n_hits, n_tracks)
+    bytes_step = algorithmic_bytes(n_hits, n_tracks, w.n_features)
 
     res = {
         "metric": METRIC, "value": value, "unit": "tracks/s", "n_gpus": 1, "steps": args.steps,
@@ -494,7 +551,7 @@ def main():
         "data": "synthetic helix tracks (2 T solenoid, seeded), random-init weights",
         "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
                    "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model, "mode": mode,
-                   "max_hits": W.max_hits,
+                   "max_hits": W.max_hits, "n_features": w.n_features,
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved_tflops / peak, "traffic": traffic_bytes(w, batch, len(starts)),

@@ -205,8 +205,13 @@ tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *
  * b_tesla   host scalar > 0: solenoid field along +z.
  * seeds     device, float64 [n_tracks][5]: d0 [mm], z0 [mm], phi, theta,
  *           q/p [1/GeV].  Every row is written.
- * features  device, float32 [offsets[n_tracks] - offsets[0]][3], or NULL to
- *           skip them: row r belongs to hit row offsets[0] + r.
+ * features  device, float32 rows of feature_stride floats, or NULL to skip
+ *           them: the three features of hit row offsets[0] + r are at
+ *           features[r * feature_stride + 0 .. 2], for r < offsets[n_tracks] -
+ *           offsets[0] (with feature_stride = 15 and features pointing at
+ *           column 12, the seed fills the last three columns of the Fourier
+ *           front end's per-hit feature rows).
+ * feature_stride  host scalar: 0 or 3 for packed rows, else >= 3.
  * flags     device int32 or NULL: OR-ed with TF_SEED_* bits of the tracks that
  *           got NaN seeds (their features are NaN too, unless their offsets
  *           are bad, in which case their rows are not written).
@@ -214,10 +219,12 @@ tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *
  *
  * Asynchronous, allocates nothing (graph-capturable).  Outputs must not
  * overlap the inputs.  Errors: TF_EINVAL (null pointers with n_tracks > 0,
- * negative sizes, b_tesla <= 0), TF_EHIP (launch failure).
+ * negative sizes, b_tesla <= 0, feature_stride 1 or 2 or negative), TF_EHIP
+ * (launch failure).
  */
 tf_status tf_seed_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                         double b_tesla, double *seeds, float *features, int32_t *flags, hipStream_t stream);
+                         double b_tesla, double *seeds, float *features, int32_t feature_stride, int32_t *flags,
+                         hipStream_t stream);
 
 /* Bits of tf_seed_tracks' flags. */
 #define TF_SEED_TOO_SHORT 1    /* fewer than three hits */
@@ -245,9 +252,10 @@ size_t tf_readout_blob_size(int32_t d);
 
 /* Copy a readout head blob to the current device.  d: 32, 64, 128 or 256.
  * dtype (tf_dtype): TF_FP32 runs the head's products in fp32; TF_BF16 and
- * TF_BF16_F16ACT (the 16-bit models) round W1 diag(g) and W2 to bf16 once
- * and multiply them with the fp32 activations split into a high and a low
- * bf16 part (about 16 significant bits), accumulating in fp32.
+ * TF_BF16_F16ACT (the 16-bit models) take W1 and W2 in bf16 (exact for
+ * bf16-valued weights; others are rounded to nearest even) and multiply them
+ * with the fp32 activations (the gain applied in fp32) split into a high and
+ * a low bf16 part (about 16 significant bits), accumulating in fp32.
  * host_blob is only read during the call; *out receives a handle freed with
  * tf_readout_destroy.  Synchronous; allocates device memory.
  * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d),

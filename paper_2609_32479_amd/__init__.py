@@ -74,7 +74,8 @@ def lib():
         L.tf_status_string.restype = ctypes.c_char_p
         L.tf_status_string.argtypes = [ctypes.c_int]
         L.tf_seed_tracks.restype = ctypes.c_int
-        L.tf_seed_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, ctypes.c_double, vp, vp, vp, vp]
+        L.tf_seed_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, ctypes.c_double, vp, vp, ctypes.c_int32,
+                                     vp, vp]
         L.tf_readout_blob_size.restype = ctypes.c_size_t
         L.tf_readout_blob_size.argtypes = [ctypes.c_int32]
         L.tf_readout_create.restype = ctypes.c_int
@@ -214,8 +215,10 @@ def seed_tracks(hits: torch.Tensor, offsets: torch.Tensor, b_tesla: float, featu
 
     hits float32 [H, 3] and offsets int32 [N+1] on the GPU.  Returns
     (seeds float64 [N, 5], features float32 [offsets[N] - offsets[0], 3] or
-    None).  ``flags`` (int32 GPU tensor of one element) is OR-ed with the
-    SEED_* bits of tracks without a seed.
+    None).  ``feats`` may be a row-strided view with three unit-stride columns
+    (e.g. columns 12..14 of the Fourier front end's [H, 15] feature rows),
+    whose row 0 belongs to hit row offsets[0].  ``flags`` (int32 GPU tensor
+    of one element) is OR-ed with the SEED_* bits of tracks without a seed.
     """
     if not (hits.is_cuda and offsets.is_cuda):
         raise ValueError("hits and offsets must be GPU tensors")
@@ -230,20 +233,21 @@ def seed_tracks(hits: torch.Tensor, offsets: torch.Tensor, b_tesla: float, featu
         seeds = torch.empty((n, 5), dtype=torch.float64, device=hits.device)
     elif not (seeds.is_cuda and seeds.dtype == torch.float64 and seeds.is_contiguous() and seeds.numel() >= 5 * n):
         raise ValueError("seeds must be a contiguous float64 GPU tensor with room for [N, 5]")
-    fptr = None
+    fptr, fstride = None, 3
     if features:
         if feats is None:  # sized from the offsets (a device read: pass feats to stay asynchronous)
             rows = int(offsets[n].item() - offsets[0].item()) if n > 0 else 0
             feats = torch.empty((max(rows, 0), 3), dtype=torch.float32, device=hits.device)
-        elif not (feats.is_cuda and feats.dtype == torch.float32 and feats.is_contiguous()):
-            raise ValueError("feats must be a contiguous float32 GPU tensor with a row per hit of the batch")
-        fptr = feats.data_ptr()
+        elif not (feats.is_cuda and feats.dtype == torch.float32 and feats.dim() == 2 and feats.shape[1] == 3
+                  and feats.stride(1) == 1 and feats.stride(0) >= 3):
+            raise ValueError("feats must be a float32 GPU tensor [rows, 3] with unit column stride")
+        fptr, fstride = feats.data_ptr(), feats.stride(0)
     else:
         feats = None
     if flags is not None and not (flags.is_cuda and flags.dtype == torch.int32 and flags.numel() >= 1):
         raise ValueError("flags must be an int32 GPU tensor")
     _check(lib().tf_seed_tracks(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, float(b_tesla),
-                                seeds.data_ptr(), fptr, flags.data_ptr() if flags is not None else None,
+                                seeds.data_ptr(), fptr, fstride, flags.data_ptr() if flags is not None else None,
                                 _stream_handle(stream)), "tf_seed_tracks")
     return seeds, feats
 

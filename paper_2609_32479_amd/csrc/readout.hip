@@ -20,9 +20,11 @@
 // wave and stay in L2.
 //
 // Two number types: fp32 products (32x32x2) for the fp32 model; for the
-// 16-bit models bf16 weights (W1' rounded once) against fp32 activations
-// split into a high and a low bf16 part (32x32x16, two products per k-step),
-// which keeps the activations to about 16 significant bits.
+// 16-bit models bf16 weights (W1 and W2 as given, exact for bf16-valued
+// weights; the gain is applied to the fp32 activations instead of being
+// folded in, which would round the products to 8 bits) against fp32
+// activations split into a high and a low bf16 part (32x32x16, two products
+// per k-step), which keeps the activations to about 16 significant bits.
 #include <hip/hip_runtime.h>
 
 #include <cmath>
@@ -203,12 +205,14 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__
     finish(o, b2, qs[wv], lane, t0, n, seeds, quant, out);
 }
 
-// 16-bit head: A1 [d/8][MT][64] bf16x8 (lane (s, i): row 32 m + i, k = s d + 8 ks + e),
-// A2 [MT][2][2][64] bf16x8 (k-step (m, qh): the lane's units of acc[m][8 qh .. 8 qh + 7]).
+// 16-bit head: A1 [d/8][MT][64] bf16x8 (lane (s, i): W1 row 32 m + i, k = s d + 8 ks + e),
+// A2 [MT][2][2][64] bf16x8 (k-step (m, qh): the lane's units of acc[m][8 qh .. 8 qh + 7]),
+// gain [2d] fp32.
 template <int D>
 __global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *__restrict__ states, int n,
                                                                    const double *__restrict__ seeds,
                                                                    const bf16x8 *__restrict__ A1,
+                                                                   const float *__restrict__ gain,
                                                                    const float *__restrict__ b1,
                                                                    const bf16x8 *__restrict__ A2,
                                                                    const float *__restrict__ b2,
@@ -221,6 +225,7 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *
     const int s = lane >> 5, c = lane & 31;
     const int t = t0 + c;
     const float4 *zp = reinterpret_cast<const float4 *>(states + (size_t)(t < n ? t : t0) * (2 * D) + s * D);
+    const float4 *gp = reinterpret_cast<const float4 *>(gain + s * D);
 
     f32x16 acc[MT];
 #pragma unroll
@@ -231,13 +236,16 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *
 #pragma unroll 2
     for (int ks = 0; ks < D / 8; ++ks) {
         const float4 z0 = zp[2 * ks], z1 = zp[2 * ks + 1];
+        const float4 g0 = gp[2 * ks], g1 = gp[2 * ks + 1];
         bf16x8 a[MT];
 #pragma unroll
         for (int m = 0; m < MT; ++m) a[m] = A1[(ks * MT + m) * 64 + lane];
         ss = fmaf(z0.x, z0.x, fmaf(z0.y, z0.y, fmaf(z0.z, z0.z, fmaf(z0.w, z0.w, ss))));
         ss = fmaf(z1.x, z1.x, fmaf(z1.y, z1.y, fmaf(z1.z, z1.z, fmaf(z1.w, z1.w, ss))));
-        bf16x8 hi, lo;
-        split16((f32x8){z0.x, z0.y, z0.z, z0.w, z1.x, z1.y, z1.z, z1.w}, hi, lo);
+        bf16x8 hi, lo;  // g (.) z, split
+        split16((f32x8){g0.x * z0.x, g0.y * z0.y, g0.z * z0.z, g0.w * z0.w, g1.x * z1.x, g1.y * z1.y, g1.z * z1.z,
+                        g1.w * z1.w},
+                hi, lo);
 #pragma unroll
         for (int m = 0; m < MT; ++m) {
             acc[m] = mma16(a[m], hi, acc[m]);
@@ -280,6 +288,7 @@ struct tf_readout {
     const float *b1 = nullptr;
     const void *A2 = nullptr;
     const float *b2 = nullptr;
+    const float *gain = nullptr;  // [2d], 16-bit head only
 };
 
 namespace {
@@ -298,8 +307,8 @@ void launch_d(const tf_readout *h, dim3 grid, dim3 block, hipStream_t stream, co
               const double *seeds, float *quant, double *out) {
     if (h->half)
         hipLaunchKernelGGL(tf_readout16_kernel<D>, grid, block, 0, stream, states, n, seeds,
-                           static_cast<const bf16x8 *>(h->A1), h->b1, static_cast<const bf16x8 *>(h->A2), h->b2,
-                           quant, out);
+                           static_cast<const bf16x8 *>(h->A1), h->gain, h->b1, static_cast<const bf16x8 *>(h->A2),
+                           h->b2, quant, out);
     else
         hipLaunchKernelGGL(tf_readout_kernel<D>, grid, block, 0, stream, states, n, seeds,
                            static_cast<const float4 *>(h->A1), h->b1, static_cast<const float4 *>(h->A2), h->b2,
@@ -325,12 +334,13 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     const size_t dd = (size_t)d;
     const int MT = d / 32;
     const float *g = host_blob, *W1 = g + 2 * dd, *b1 = W1 + dd * 2 * dd, *W2 = b1 + dd, *b2 = W2 + kNout * dd;
-    // W1' (gain folded in) as lane (s, i) holds it: row 32 m + i, column s d + kk, where kk is
-    // the k-step's position in the lane's half row; W2 as lane (s, i) holds it: row 32 rb + i,
+    // W1 as lane (s, i) holds it: row 32 m + i, column s d + kk, where kk is the k-step's
+    // position in the lane's half row, with the gain folded in for the fp32 head (the
+    // 16-bit head applies it to the activations); W2 as lane (s, i) holds it: row 32 rb + i,
     // the hidden unit that the lane's accumulator slot carries
     auto w1 = [&](int m, int lane, int kk) {
         const size_t u = 32 * m + (lane & 31), k = (size_t)(lane >> 5) * dd + kk;
-        return W1[u * 2 * dd + k] * g[k];
+        return half ? W1[u * 2 * dd + k] : W1[u * 2 * dd + k] * g[k];
     };
     auto w2 = [&](int rb, int lane, int m, int q) {
         const int row = 32 * rb + (lane & 31);
@@ -339,7 +349,8 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     };
     const size_t esz = half ? 2 : 4;
     const size_t nA1 = dd * 2 * dd, nA2 = (size_t)MT * 2 * 16 * 64;  // elements (A2: 2 row blocks x 16 slots)
-    const size_t oB1 = nA1 * esz, oA2 = oB1 + dd * 4, oB2 = oA2 + nA2 * esz, total = oB2 + 64 * 4;
+    const size_t oB1 = nA1 * esz, oA2 = oB1 + dd * 4, oB2 = oA2 + nA2 * esz, oG = oB2 + 64 * 4;
+    const size_t total = oG + 2 * dd * 4;
     std::vector<char> hbuf;
     try {
         hbuf.assign(total, 0);
@@ -383,6 +394,7 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     }
     std::memcpy(hp + oB1, b1, dd * 4);
     std::memcpy(hp + oB2, b2, kNout * 4);
+    std::memcpy(hp + oG, g, 2 * dd * 4);
     tf_readout *ro = new (std::nothrow) tf_readout;
     if (!ro) return TF_ENOMEM;
     if (hipMalloc((void **)&ro->dmem, total) != hipSuccess) {
@@ -400,6 +412,7 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     ro->b1 = reinterpret_cast<const float *>(ro->dmem + oB1);
     ro->A2 = ro->dmem + oA2;
     ro->b2 = reinterpret_cast<const float *>(ro->dmem + oB2);
+    ro->gain = reinterpret_cast<const float *>(ro->dmem + oG);
     *out = ro;
     return TF_OK;
 }

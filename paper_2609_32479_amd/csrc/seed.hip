@@ -55,7 +55,8 @@ __device__ __forceinline__ void hit_features(const float *p, double cx, double c
 __global__ __launch_bounds__(kSeedBlock) void tf_seed_kernel(const float *__restrict__ hits, long long n_hits,
                                                               const int *__restrict__ offsets, int n_tracks,
                                                               double b_tesla, double *__restrict__ seeds,
-                                                              float *__restrict__ features, int *__restrict__ flags) {
+                                                              float *__restrict__ features, int fstride,
+                                                              int *__restrict__ flags) {
     __shared__ double circ[kSeedWaves][7][64];  // cx, cy, R, k, z0, cot(theta), sin(theta) per track
     __shared__ int woff[kSeedWaves][65];        // the wave's track offsets
     __shared__ int wbits[kSeedWaves][64];
@@ -120,7 +121,7 @@ __global__ __launch_bounds__(kSeedBlock) void tf_seed_kernel(const float *__rest
         // its own rows
         if (bits == TF_SEED_BAD_OFFSETS) return;
         for (int h = o; h < e; ++h) {
-            float *f = features + (size_t)(h - o0) * 3;
+            float *f = features + (size_t)(h - o0) * fstride;
             if (bits)
                 f[0] = f[1] = f[2] = (float)nan;
             else
@@ -152,7 +153,7 @@ __global__ __launch_bounds__(kSeedBlock) void tf_seed_kernel(const float *__rest
             else
                 b = m;
         }
-        float *f = features + (size_t)(r - o0) * 3;
+        float *f = features + (size_t)(r - o0) * fstride;
         if (wbits[wv][a])
             f[0] = f[1] = f[2] = (float)nan;
         else
@@ -164,13 +165,15 @@ __global__ __launch_bounds__(kSeedBlock) void tf_seed_kernel(const float *__rest
 }  // namespace
 
 extern "C" tf_status tf_seed_tracks(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                                    double b_tesla, double *seeds, float *features, int32_t *flags,
-                                    hipStream_t stream) {
+                                    double b_tesla, double *seeds, float *features, int32_t feature_stride,
+                                    int32_t *flags, hipStream_t stream) {
     if (n_tracks < 0 || n_hits < 0 || !(b_tesla > 0.0)) return TF_EINVAL;
+    if (feature_stride == 0) feature_stride = 3;
+    if (feature_stride < 3) return TF_EINVAL;
     if (n_tracks == 0) return TF_OK;
     if (!offsets || !seeds || (!hits && n_hits > 0)) return TF_EINVAL;
     const int blocks = (n_tracks + kSeedBlock - 1) / kSeedBlock;  // one wave per 64 tracks
     hipLaunchKernelGGL(tf_seed_kernel, dim3(blocks), dim3(kSeedBlock), 0, stream, hits, (long long)n_hits, offsets,
-                       (int)n_tracks, b_tesla, seeds, features, flags);
+                       (int)n_tracks, b_tesla, seeds, features, (int)feature_stride, flags);
     return hipGetLastError() == hipSuccess ? TF_OK : TF_EHIP;
 }

@@ -72,12 +72,23 @@ def test_argument_checks_without_gpu(tf):
     assert L.tf_get_device_error(None, None, None, 0) == tf.TF_EINVAL
     L.tf_weights_destroy(None)   # no-op
     # tf_seed_tracks: checks made before any launch
-    assert L.tf_seed_tracks(None, 0, None, 0, 2.0, None, None, None, None) == tf.TF_OK      # no tracks
-    assert L.tf_seed_tracks(None, 0, None, -1, 2.0, None, None, None, None) == tf.TF_EINVAL
-    assert L.tf_seed_tracks(None, -1, None, 0, 2.0, None, None, None, None) == tf.TF_EINVAL
-    assert L.tf_seed_tracks(None, 0, None, 0, 0.0, None, None, None, None) == tf.TF_EINVAL  # field
-    assert L.tf_seed_tracks(None, 0, None, 0, float("nan"), None, None, None, None) == tf.TF_EINVAL
-    assert L.tf_seed_tracks(None, 10, None, 5, 2.0, None, None, None, None) == tf.TF_EINVAL  # null pointers
+    assert L.tf_seed_tracks(None, 0, None, 0, 2.0, None, None, 0, None, None) == tf.TF_OK      # no tracks
+    assert L.tf_seed_tracks(None, 0, None, -1, 2.0, None, None, 0, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, -1, None, 0, 2.0, None, None, 0, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, 0, None, 0, 0.0, None, None, 0, None, None) == tf.TF_EINVAL  # field
+    assert L.tf_seed_tracks(None, 0, None, 0, float("nan"), None, None, 0, None, None) == tf.TF_EINVAL
+    assert L.tf_seed_tracks(None, 10, None, 5, 2.0, None, None, 0, None, None) == tf.TF_EINVAL  # null pointers
+    assert L.tf_seed_tracks(None, 0, None, 0, 2.0, None, None, 2, None, None) == tf.TF_EINVAL  # row stride
+    # the Fourier front end: blob size and argument checks
+    assert L.tf_fourier_blob_size(4, 128, 15) == L.tf_blob_size(4, 128) - 4 * 128 + 30 + 128 * 480 + 128
+    assert L.tf_fourier_blob_size(4, 128, 0) == 0 and L.tf_fourier_blob_size(4, 128, 17) == 0
+    cfg = tf.Config(4, 128, tf.TF_BF16, 0, -1)
+    assert L.tf_weights_create(ctypes.byref(cfg), blob, 10, ctypes.byref(h)) == tf.TF_EINVAL
+    cfg = tf.Config(4, 64, tf.TF_BF16, 0, 15)
+    assert L.tf_weights_create(ctypes.byref(cfg), blob, L.tf_fourier_blob_size(4, 64, 15), ctypes.byref(h)) \
+        == tf.TF_EUNSUPPORTED
+    cfg = tf.Config(4, 128, tf.TF_BF16, 0, 15)
+    assert L.tf_weights_create(ctypes.byref(cfg), blob, L.tf_blob_size(4, 128), ctypes.byref(h)) == tf.TF_EINVAL
 
 
 def test_readout_and_states_argument_checks_without_gpu(tf):

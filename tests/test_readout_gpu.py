@@ -35,9 +35,10 @@ def quantile_tol(d):
     return 2.0 ** -24 * (2 * d) * 2
 
 
-# The 16-bit head rounds W1 diag(g) (and W2) to bf16 and keeps the activations
-# to ~16 bits: ~2^-9 per weight, averaged over the dot products, is held to
-# the bf16 model's output tolerance.
+# The 16-bit head takes W1 and W2 in bf16 (exact for a bf16 model's weights,
+# rounded for an fp32 model's: ~2^-9 per weight, averaged over the dot
+# products) and keeps the activations to ~16 bits; it is held to the bf16
+# model's output tolerance.
 def head_tols(mode, d):
     """(quantile, decoded) tolerances of a head of this number type."""
     if mode == "fp32":

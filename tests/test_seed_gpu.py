@@ -147,3 +147,22 @@ def test_full_deployment_batch_sampled(tf):
     gf = np.concatenate([g_feat[offs[i]:offs[i + 1]] for i in sel])
     assert np.all(_colerr(_wrap_phi(g_seed[sel], r_seed), r_seed) <= SEED_TOL)
     assert np.all(_colerr(gf.astype(np.float64), r_feat) <= FEAT_TOL)
+
+
+def test_features_into_strided_rows(tf):
+    """Features written with a row stride into columns 12..14 of [H, 15] rows
+    (the Fourier front end's per-hit feature rows): equal to the packed
+    features, the other columns untouched."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    hits, offs = ts.make_tracks(w, n_tracks=500)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    packed = _run(tf, hits, offs, w.b_field)[1]
+    rows = torch.full((hits.shape[0], 15), -5.0, dtype=torch.float32, device="cuda")
+    # the second half of the tracks alone: row 0 of the view is the first hit of track 250
+    r0 = int(offs[250])
+    tf.seed_tracks(h, o[250:], w.b_field, feats=rows[r0:, 12:15])
+    torch.cuda.synchronize()
+    got = rows.cpu().numpy()
+    assert np.array_equal(got[r0:, 12:15], packed[r0:])
+    assert np.all(got[:, :12] == -5.0) and np.all(got[:r0, 12:] == -5.0)
