@@ -76,3 +76,41 @@ def test_full_size_sampled(tf, name):
     ref = oracle.fit_tracks(sh, so, blob, w.n_layers, w.d_model)
     emax, l2 = assert_parity(out[sel], ref, TOL[w.dtype], f"{name} full size, {sel.size} sampled tracks")
     print(f"[full] {name}: {sel.size} sampled, max col err {emax.max():.3g}", flush=True)
+
+
+def test_fourier_deployment_full_size_sampled(tf):
+    """All 8 388 608 tracks through the Fourier front end in the benchmark's
+    launch configuration: the seed kernel writes the 3 seed features into the
+    feature rows, then 32 captured fit_tracks calls.  A seeded sample is run
+    through the oracle's own chain (its seed features, its encoder)."""
+    w = ts.workload("fourier15_deploy_d128x4_bf16_8m")
+    print(f"[full] {w.name}: {w.n_tracks} tracks", flush=True)
+    hits, offs = ts.make_tracks(w, workers=WORKERS)
+    n = offs.size - 1
+    blob = ts.make_fourier_weights(w)
+    W = tf.Weights(blob, w.n_layers, w.d_model, tf.MODE_FOR_WEIGHTS[w.dtype], max_hits=w.len_max,
+                   n_features=w.n_features)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    feats = torch.empty((hits.shape[0], 15), dtype=torch.float32, device="cuda")
+    step = 1 << 20
+    for i0 in range(0, n, step):
+        i1 = min(n, i0 + step)
+        m = ts.measured_features(w, hits[offs[i0]:offs[i1]], offs[i0:i1 + 1])
+        feats[offs[i0]:offs[i1], :12] = torch.from_numpy(m).cuda()
+    tf.seed_tracks(h, o, w.b_field, feats=feats[:, 12:15])
+    out = _launch(tf, W, feats, o, n, w.batch).cpu().numpy()
+    assert tf.device_error(W) == 0
+    assert np.all(np.isfinite(out))
+    L = np.diff(offs)
+    rng = np.random.default_rng(12)
+    sel = set(rng.choice(n, size=2048, replace=False).tolist()) | {0, n - 1, int(np.argmin(L)), int(np.argmax(L))}
+    sel = np.array(sorted(sel))
+    sh = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+    so = np.concatenate([[0], np.cumsum(L[sel])]).astype(np.int32)
+    _, sf, bad = oracle.seed_tracks(sh, so, w.b_field)
+    assert bad == 0
+    ref = oracle.fit_tracks(ts.hit_features(w, sh, so, sf), so, blob, w.n_layers, w.d_model,
+                            n_features=w.n_features)
+    emax, _ = assert_parity(out[sel], ref, TOL[w.dtype], f"{w.name} full size, {sel.size} sampled tracks")
+    print(f"[full] {w.name}: {sel.size} sampled, max col err {emax.max():.3g}", flush=True)
