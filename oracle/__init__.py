@@ -46,6 +46,11 @@ def lib():
                                        ctypes.c_size_t, dp, ctypes.c_int]
         L.orc_fourier_blob_size.restype = ctypes.c_size_t
         L.orc_fourier_blob_size.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_mingru_blob_size.restype = ctypes.c_size_t
+        L.orc_mingru_blob_size.argtypes = [ctypes.c_int, ctypes.c_int, ctypes.c_int, ctypes.c_int]
+        L.orc_mingru_states.restype = ctypes.c_long
+        L.orc_mingru_states.argtypes = [fp, ctypes.c_int, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int,
+                                        ctypes.c_int, fp, ctypes.c_size_t, dp, ctypes.c_int]
         L.orc_fourier_features.restype = None
         L.orc_fourier_features.argtypes = [fp, ctypes.c_int, fp, fp, dp]
         L.orc_readout_blob_size.restype = ctypes.c_size_t
@@ -286,3 +291,26 @@ def readout_tracks(states, seeds, head_blob, d):
     if rc < 0:
         raise ValueError("oracle rejected its arguments")
     return q, out
+
+
+# ---------------------------------------------------------------------------
+# The paper's bidirectional minGRU backbone (Sec. Encoder).
+# ---------------------------------------------------------------------------
+
+def mingru_blob_size(n_layers, d, H, n_features=0):
+    return int(lib().orc_mingru_blob_size(int(n_layers), int(d), int(H), int(n_features)))
+
+
+def mingru_states(hits, offsets, blob, n_layers, d, H, n_features=0, n_threads=0):
+    """Packed batch: the last layer's end states [N, 2H] (NaN rows for empty tracks)."""
+    hits, ph = _f(np.asarray(hits).reshape(-1, n_features or 3))
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    blob, pb = _f(blob)
+    n = offsets.size - 1
+    st = np.empty((max(n, 0), 2 * H))
+    rc = lib().orc_mingru_states(ph, int(n_features), offsets.ctypes.data_as(ctypes.POINTER(ctypes.c_int32)), n,
+                                 int(n_layers), int(d), int(H), pb, blob.size,
+                                 st.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), int(n_threads))
+    if rc < 0:
+        raise ValueError("oracle rejected its arguments")
+    return st

@@ -8,7 +8,7 @@ LIB = os.path.join(HERE, "liboracle.so")
 
 
 def build(verbose: bool = False) -> str:
-    srcs = [os.path.join(HERE, f) for f in ("oracle.c", "seed.c", "readout.c")]
+    srcs = [os.path.join(HERE, f) for f in ("oracle.c", "seed.c", "readout.c", "mingru.c")]
     tmp = LIB + ".tmp"
     cmd = ["gcc", "-O2", "-std=c11", "-fPIC", "-shared", "-fopenmp", "-Wall", "-Wextra",
            *srcs, "-o", tmp, "-lm"]

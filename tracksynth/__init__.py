@@ -34,7 +34,7 @@ __all__ = [
     "make_weights", "blob_layout", "blob_size", "round_to_bf16", "TRACK_CHUNK",
     "KAPPA_GEV_PER_T_M", "readout_layout", "make_readout_weights",
     "FOURIER_WORKLOADS", "N_MEASURED", "measured_features", "feature_bounds", "fourier_layout",
-    "make_fourier_weights", "hit_features",
+    "make_fourier_weights", "hit_features", "MINGRU_WORKLOADS", "mingru_layout", "make_mingru_weights",
 ]
 
 # pT [GeV] = KAPPA * B [T] * R [m] for a unit-charge particle.
@@ -64,6 +64,8 @@ class Workload:
     eta_max: float = 1.5
     batch: int = 0        # tracks per fit_tracks call when the workload is streamed
     n_features: int = 0   # > 0: per-hit features for the Fourier front end (12 measured + 3 seed)
+    arch: str = "residual"  # "residual": the layers of blob_layout; "mingru": the paper's backbone
+    hidden: int = 0       # minGRU hidden width H (the states are 2H wide)
 
     @property
     def data_seed(self) -> int:
@@ -103,6 +105,21 @@ FOURIER_WORKLOADS = {
 }
 
 
+# The paper's backbone: two bidirectional minGRU layers of hidden width H
+# behind the front end (the deployed model: Fourier front end to d = 128,
+# H = 192), on the same tracks.
+MINGRU_WORKLOADS = {
+    w.name: w for w in [
+        dataclasses.replace(WORKLOADS["tiny_d32_fp32"], name="mingru2_h64_tiny_d32_fp32", n_layers=2,
+                            arch="mingru", hidden=64),
+        dataclasses.replace(WORKLOADS["d128x4_fp32_65k"], name="mingru2_h192_fourier15_d128_fp32_65k",
+                            n_layers=2, arch="mingru", hidden=192, n_features=15),
+        dataclasses.replace(WORKLOADS["deploy_d128x4_bf16_8m"], name="mingru2_h192_fourier15_deploy_bf16_8m",
+                            n_layers=2, arch="mingru", hidden=192, n_features=15),
+    ]
+}
+
+
 def workload(name_or_index) -> Workload:
     if isinstance(name_or_index, Workload):
         return name_or_index
@@ -113,6 +130,8 @@ def workload(name_or_index) -> Workload:
         raise KeyError(name_or_index)
     if name_or_index in FOURIER_WORKLOADS:
         return FOURIER_WORKLOADS[name_or_index]
+    if name_or_index in MINGRU_WORKLOADS:
+        return MINGRU_WORKLOADS[name_or_index]
     return WORKLOADS[name_or_index]
 
 
@@ -450,3 +469,45 @@ def hit_features(w, hits, offs, seed_features) -> np.ndarray:
     features (from the seed kernel or its oracle), in the blob's order."""
     sf = np.asarray(seed_features, dtype=np.float32).reshape(-1, 3)
     return np.ascontiguousarray(np.concatenate([measured_features(w, hits, offs), sf], axis=1))
+
+
+def mingru_layout(n_layers: int, d: int, H: int, n_features: int = 0):
+    """Blob of the paper's backbone: the front end ((x, y, z) embedding, or the
+    Fourier front end), then per layer W[4H][D_l], b[4H] with D_0 = d and
+    D_l = 2H: rows 0..H-1 forward candidate, H..2H-1 forward gate
+    pre-activation, 2H..3H-1 reverse candidate, 3H..4H-1 reverse gate; the
+    input of a later layer is [f; b] of the one before."""
+    if n_features:
+        lay = fourier_layout(0, d, n_features)[:4]
+    else:
+        lay = blob_layout(0, d)[:2]
+    for l in range(n_layers):
+        din = d if l == 0 else 2 * H
+        lay += [(f"mg{l}.W", (4 * H, din), din, "w"), (f"mg{l}.b", (4 * H,), din, "b")]
+    return lay
+
+
+def make_mingru_weights(w, seed: int | None = None) -> np.ndarray:
+    """float32 blob for a minGRU workload, drawn like make_weights (bounds from
+    feature_bounds for the Fourier front end); rounded to bf16 values for a
+    bf16 workload, the bounds excepted."""
+    w = workload(w)
+    assert w.arch == "mingru"
+    F = w.n_features
+    rng = np.random.Generator(np.random.PCG64(w.weight_seed + 300 if seed is None else seed))
+    lo, hi = feature_bounds(w) if F else (None, None)
+    parts = []
+    for name, shape, fan_in, kind in mingru_layout(w.n_layers, w.d_model, w.hidden, F):
+        n = int(np.prod(shape))
+        if kind == "lo":
+            parts.append(lo.astype(np.float64))
+        elif kind == "hi":
+            parts.append(hi.astype(np.float64))
+        elif kind == "w":
+            parts.append(rng.normal(0.0, fan_in ** -0.5, n))
+        else:
+            parts.append(rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n))
+    blob = np.concatenate(parts).astype(np.float32)
+    if w.dtype == "bf16":
+        blob[2 * F:] = round_to_bf16(blob[2 * F:])
+    return blob
