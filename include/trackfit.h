@@ -250,7 +250,8 @@ typedef struct tf_readout tf_readout;
  * order), the quantiles in increasing order of their levels. */
 size_t tf_readout_blob_size(int32_t d);
 
-/* Copy a readout head blob to the current device.  d: 32, 64, 128 or 256.
+/* Copy a readout head blob to the current device.  d: 32, 64, 128, 192 (the
+ * paper's backbone: states of 2 x 192) or 256.
  * dtype (tf_dtype): TF_FP32 runs the head's products in fp32; TF_BF16 and
  * TF_BF16_F16ACT (the 16-bit models) take W1 and W2 in bf16 (exact for
  * bf16-valued weights; others are rounded to nearest even) and multiply them
@@ -293,6 +294,74 @@ void tf_readout_destroy(tf_readout *h);
  */
 tf_status tf_decode_tracks(const float *states, int32_t n_tracks, const double *seeds, const tf_readout *h,
                            float *quantiles, double *out, hipStream_t stream);
+
+/*
+ * The paper's own backbone (Sec. Encoder): a stack of bidirectional minGRU
+ * layers of hidden width H behind the front end.  Each layer projects its
+ * input linearly to the forward and reverse candidates and gates, z =
+ * sigmoid(gate), runs the update of Eq. (2) forward from each track's first
+ * hit and in reverse from its last (zero initial state), and hands [f; b]
+ * (2H values per hit) to the next layer; no normalisation or residual inside.
+ * Number types as for tf_config.dtype: fp32 throughout, or 16-bit matrix
+ * operands (weights bf16, activations bf16 or fp16) with fp32 accumulation,
+ * gates and recurrence.
+ */
+typedef struct {
+    int32_t n_layers;   /* 1..8 */
+    int32_t d_model;    /* front-end width: 32 (with H = 64) or 128 (with H = 192) */
+    int32_t hidden;     /* H */
+    int32_t dtype;      /* tf_dtype */
+    int32_t n_features; /* 0: (x, y, z) front end; 1..16: the Fourier front end */
+} tf_mingru_config;
+
+typedef struct tf_mingru tf_mingru;
+
+/* Floats of the blob (0 if invalid).  Order (float32, row-major [out][in]):
+ * the front end as in tf_weights_create's blob (embed.W[d][3], embed.b[d], or
+ * fe.lo[F], fe.hi[F], fe.W[d][32 F], fe.b[d]), then per layer l: W[4H][D_l],
+ * b[4H] with D_0 = d and D_l = 2H; rows 0..H-1 forward candidate, H..2H-1
+ * forward gate pre-activation, 2H..3H-1 reverse candidate, 3H..4H-1 reverse
+ * gate pre-activation; columns of a later layer read [f; b] of the one
+ * before (forward state first). */
+size_t tf_mingru_blob_size(const tf_mingru_config *cfg);
+
+/* Copy a blob to the current device.  Synchronous; allocates device memory.
+ * Tracks may have up to 32 hits.  Errors: TF_EINVAL (null pointers, bad
+ * sizes or dtype), TF_EUNSUPPORTED (other widths, more than 8 layers, more
+ * than 16 features), TF_ENOMEM, TF_EHIP.  On error *out is NULL. */
+tf_status tf_mingru_create(const tf_mingru_config *cfg, const float *host_blob, size_t n_floats, tf_mingru **out);
+
+/* Free a handle (NULL is a no-op).  Synchronises the device first. */
+void tf_mingru_destroy(tf_mingru *h);
+
+/* Bytes of device workspace tf_mingru_states needs for a batch of n_rows hit
+ * rows (offsets[n_tracks] - offsets[0]): the front end's output and up to two
+ * layer outputs, row-major, in the operand type. */
+size_t tf_mingru_workspace_size(const tf_mingru *h, int64_t n_rows);
+
+/*
+ * End states of the last layer for a packed batch: the readout's input
+ * (Sec. Encoder, last paragraph).
+ *
+ * hits, n_hits, offsets, n_tracks  as for fit_tracks (hits carry n_features
+ *           values per hit with the Fourier front end).
+ * workspace device memory of workspace_bytes (see tf_mingru_workspace_size);
+ *           its contents are scratch.  Tracks whose rows do not fit get NaN.
+ * states    device, float32 [n_tracks][2H]: the forward state at the track's
+ *           last hit, then the reverse state at its first hit.  Every row is
+ *           written; tracks with no hits, more than 32 hits or rows outside
+ *           [0, n_hits) get NaN rows and set the device error word.
+ * Asynchronous, allocates nothing.  One launch for the front end, one per
+ * layer, all on stream.  Errors: TF_EINVAL (null pointers with n_tracks > 0,
+ * negative sizes), TF_EHIP (launch failure).
+ */
+tf_status tf_mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                           const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
+                           hipStream_t stream);
+
+/* Read (and if clear != 0, reset) the handle's sticky device error word
+ * (TF_DEVERR_* bits).  Synchronises stream. */
+tf_status tf_mingru_device_error(const tf_mingru *h, hipStream_t stream, int32_t *flags, int clear);
 
 /* Static description of a status code. */
 const char *tf_status_string(tf_status s);

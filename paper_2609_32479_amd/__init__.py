@@ -15,7 +15,7 @@ import torch  # noqa: F401  -- load torch's HIP runtime before the library (one 
 __all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_size",
            "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS",
            "TrackfitError", "lib", "seed_tracks", "fit_tracks_states", "Readout", "decode_tracks",
-           "readout_blob_size", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
+           "readout_blob_size", "MinGRU", "MinGRUConfig", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtrackfit.so")
 
@@ -30,13 +30,20 @@ SEED_TOO_SHORT, SEED_NO_CIRCLE, SEED_BAD_OFFSETS = 1, 2, 4
 
 EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_fourier_blob_size", "tf_max_hits",
             "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks", "fit_tracks_states",
-            "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks")
+            "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks",
+            "tf_mingru_blob_size", "tf_mingru_create", "tf_mingru_destroy", "tf_mingru_workspace_size",
+            "tf_mingru_states", "tf_mingru_device_error")
 
 
 class TrackfitError(RuntimeError):
     def __init__(self, status: int, what: str):
         super().__init__(f"{what}: {_status_string(status)} ({status})")
         self.status = status
+
+
+class MinGRUConfig(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("d_model", ctypes.c_int32), ("hidden", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("n_features", ctypes.c_int32)]
 
 
 class Config(ctypes.Structure):
@@ -82,6 +89,18 @@ def lib():
         L.tf_readout_create.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t, ctypes.POINTER(vp)]
         L.tf_readout_destroy.restype = None
         L.tf_readout_destroy.argtypes = [vp]
+        L.tf_mingru_blob_size.restype = ctypes.c_size_t
+        L.tf_mingru_blob_size.argtypes = [ctypes.POINTER(MinGRUConfig)]
+        L.tf_mingru_create.restype = ctypes.c_int
+        L.tf_mingru_create.argtypes = [ctypes.POINTER(MinGRUConfig), vp, ctypes.c_size_t, ctypes.POINTER(vp)]
+        L.tf_mingru_destroy.restype = None
+        L.tf_mingru_destroy.argtypes = [vp]
+        L.tf_mingru_workspace_size.restype = ctypes.c_size_t
+        L.tf_mingru_workspace_size.argtypes = [vp, ctypes.c_int64]
+        L.tf_mingru_states.restype = ctypes.c_int
+        L.tf_mingru_states.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, ctypes.c_size_t, vp, vp]
+        L.tf_mingru_device_error.restype = ctypes.c_int
+        L.tf_mingru_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
         L.tf_decode_tracks.restype = ctypes.c_int
         L.tf_decode_tracks.argtypes = [vp, ctypes.c_int32, vp, vp, vp, vp, vp]
         _lib = L
@@ -314,3 +333,67 @@ def decode_tracks(states: torch.Tensor, seeds: torch.Tensor, readout: Readout, q
     _check(lib().tf_decode_tracks(states.data_ptr(), n, seeds.data_ptr(), readout.handle, qptr, out.data_ptr(),
                                   _stream_handle(stream)), "tf_decode_tracks")
     return out, q
+
+
+class MinGRU:
+    """The paper's bidirectional minGRU backbone (tf_mingru handle) on the current device."""
+
+    def __init__(self, blob, n_layers: int, d_model: int, hidden: int, dtype: str = "fp32", n_features: int = 0):
+        import numpy as np
+        arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
+        self.cfg = MinGRUConfig(int(n_layers), int(d_model), int(hidden), DTYPES[dtype], int(n_features))
+        h = ctypes.c_void_p()
+        _check(lib().tf_mingru_create(ctypes.byref(self.cfg), arr.ctypes.data, arr.size, ctypes.byref(h)),
+               "tf_mingru_create")
+        self._h = h
+        self.n_layers, self.d_model, self.hidden, self.dtype = int(n_layers), int(d_model), int(hidden), dtype
+        self.n_features = int(n_features)
+
+    @staticmethod
+    def blob_size(n_layers, d_model, hidden, n_features=0) -> int:
+        c = MinGRUConfig(int(n_layers), int(d_model), int(hidden), 0, int(n_features))
+        return int(lib().tf_mingru_blob_size(ctypes.byref(c)))
+
+    @property
+    def handle(self):
+        return self._h
+
+    def workspace_bytes(self, n_rows: int) -> int:
+        return int(lib().tf_mingru_workspace_size(self._h, int(n_rows)))
+
+    def states(self, hits: torch.Tensor, offsets: torch.Tensor, out: torch.Tensor | None = None,
+               workspace: torch.Tensor | None = None, n_rows: int | None = None, n_tracks: int | None = None,
+               stream=None) -> torch.Tensor:
+        """Enqueue the backbone over a packed batch; returns float32 [N, 2H] end
+        states.  ``workspace`` (a byte tensor of workspace_bytes(n_rows)) is
+        allocated here when not given, sized from the offsets (a device read)
+        unless ``n_rows`` (offsets[N] - offsets[0]) is given."""
+        n = _batch(hits, offsets, n_tracks, self.n_features or 3)
+        out = _out(out, n, 2 * self.hidden, hits.device)
+        if workspace is None:
+            if n_rows is None:
+                n_rows = int(offsets[n].item() - offsets[0].item()) if n > 0 else 0
+            workspace = torch.empty(self.workspace_bytes(n_rows), dtype=torch.uint8, device=hits.device)
+        elif not (workspace.is_cuda and workspace.is_contiguous()):
+            raise ValueError("workspace must be a contiguous GPU tensor")
+        _check(lib().tf_mingru_states(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, self._h,
+                                      workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                      out.data_ptr(), _stream_handle(stream)), "tf_mingru_states")
+        return out
+
+    def device_error(self, stream=None, clear: bool = True) -> int:
+        v = ctypes.c_int32(0)
+        _check(lib().tf_mingru_device_error(self._h, _stream_handle(stream), ctypes.byref(v), int(clear)),
+               "tf_mingru_device_error")
+        return int(v.value)
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().tf_mingru_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

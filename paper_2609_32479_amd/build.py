@@ -6,7 +6,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 LIB = os.path.join(HERE, "libtrackfit.so")
-SRCS = [os.path.join(HERE, "csrc", f) for f in ("trackfit.hip", "seed.hip", "readout.hip")]
+SRCS = [os.path.join(HERE, "csrc", f) for f in ("trackfit.hip", "seed.hip", "readout.hip", "mingru.hip")]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 FLAGS = [

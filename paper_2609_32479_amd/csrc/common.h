@@ -1,0 +1,162 @@
+// Device-side building blocks shared by the library's kernels (gfx950):
+// operand types, matrix-core fragments, wave and workgroup synchronisation,
+// lane masks of the segmented scans, the tile's hit-slot order, and the
+// direct-to-LDS weight-stage copy.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
+typedef __attribute__((ext_vector_type(8))) float f32x8;
+typedef __attribute__((ext_vector_type(16))) float f32x16;
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
+
+// Matrix-core operand types.  OP_F32: fp32 weights and operands
+// (v_mfma_f32_32x32x2_f32).  OP_BF16: bf16 weights and bf16 activation
+// operands (v_mfma_f32_32x32x16_bf16).  OP_F16: bf16-valued weights held
+// exactly in fp16 and fp16 activation operands (v_mfma_f32_32x32x16_f16).
+// Accumulation is fp32 in all three.
+enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
+
+constexpr float kLog2e = 1.4426950408889634f;
+constexpr float kRmsEps = 1e-6f;
+// The fp32 gate clamps |pre-activation| to 80 and the 16-bit head clamps the
+// SiLU exponent to 80 log2(e), so that exp stays finite; the change in the
+// result is below exp(-80).
+constexpr float kGateClamp = 80.0f * kLog2e;
+constexpr int kLdsBytesMax = 160 * 1024;
+constexpr int kCopyBytes = 1024;  // one wave-wide 16-byte-per-lane copy
+
+constexpr int cmax(int a, int b) { return a > b ? a : b; }
+constexpr int round_up(int v, int m) { return (v + m - 1) / m * m; }
+
+template <int OP> struct Frag;
+template <> struct Frag<OP_BF16> {
+    typedef bf16x8 T;
+    typedef __bf16 E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) {
+        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+        return __builtin_convertvector(f, bf16x8);
+    }
+};
+template <> struct Frag<OP_F16> {
+    typedef f16x8 T;
+    typedef _Float16 E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
+        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) {
+        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
+        return __builtin_convertvector(f, f16x8);
+    }
+};
+template <> struct Frag<OP_F32> {
+    typedef float T;
+    typedef float E;
+    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
+        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+    }
+    static __device__ __forceinline__ T pack(const float *v) { return v[0]; }
+};
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+// The lane index, read afresh: values derived from it are formed where they
+// are used instead of being held in registers across the whole kernel.
+__device__ __forceinline__ int fresh_lane() {
+    int l;
+    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
+    return l;
+}
+__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
+
+// Lane mask (wave-uniform, 64 bits) of the lanes whose stream has bit p set:
+// lanes 0-31 follow b0, lanes 32-63 follow b1.
+__device__ __forceinline__ unsigned long long half_mask(unsigned b0, unsigned b1, int p) {
+    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
+    const u32x2 m = {(unsigned)((int)(b0 << (31 - p)) >> 31), (unsigned)((int)(b1 << (31 - p)) >> 31)};
+    return __builtin_bit_cast(unsigned long long, m);
+}
+
+// v in lanes outside m, 0 in lanes of m: one v_cndmask with the mask in SGPRs.
+__device__ __forceinline__ float zero_lanes(float v, unsigned long long m) {
+    float r;
+    asm("v_cndmask_b32_e64 %0, %1, 0, %2" : "=v"(r) : "v"(v), "s"(m));
+    return r;
+}
+
+// Tile hit index held in hit slot s (0 <= s < CAP).  Slot s = 32 n + 8 i + 4 g + j
+// is row 8 i + 4 g + j of hit tile n in the input projection; that row lands
+// in lanes of half g at accumulator register 4 i + j, which is position
+// 16 n + 4 i + j of stream g, i.e. tile hit SP * g + 16 n + 4 i + j.
+template <int SP>
+__device__ __forceinline__ int slot_to_hit(int s) {
+    int n = s >> 5, i = (s >> 3) & 3, g = (s >> 2) & 1, j = s & 3;
+    return SP * g + 16 * n + 4 * i + j;
+}
+
+// Copy of one weight stage from global memory straight into an LDS slot:
+// global_load_lds_dwordx4 moves 16 bytes per lane, 1 KiB per wave
+// instruction, into LDS at M0 + 16 * lane.  Each wave copies the pieces
+// w, w + WAVES, ...; waves with fewer pieces repeat the last one (same bytes to
+// the same place), so every wave issues exactly LPW loads per stage and can
+// wait for an older stage with a constant vmcnt.  The instruction is written
+// out because the compiler, which cannot tell the ring slots apart, would
+// otherwise wait for every such load before each LDS access; the kernel keeps
+// the count itself (wait_vmcnt).  The kernel has no other use of M0.
+__device__ __forceinline__ void lds_dma16(const void *gsrc, unsigned lds_addr) {
+    // one wait state between the M0 write and its use by the load
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gsrc)
+                 : "memory", "m0");
+}
+
+// slot_lds: LDS byte address of the slot.
+template <class C>
+__device__ __forceinline__ void copy_stage(const unsigned char *stages, int s, unsigned slot_lds, int wid, int lane) {
+    const unsigned char *src = stages + (size_t)s * C::STAGE + lane * 16;
+#pragma unroll
+    for (int i = 0; i < C::LPW; ++i) {
+        int piece = wid + i * C::WAVES;
+        piece = piece < C::COPIES ? piece : C::COPIES - 1;
+        lds_dma16(src + piece * kCopyBytes, slot_lds + piece * kCopyBytes);
+    }
+}
+
+// Workgroup barrier that orders LDS only (the kernel shares nothing through
+// global memory within a workgroup).
+__device__ __forceinline__ void lds_barrier() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+    static_assert(N >= 0 && N < 64, "vmcnt range");
+    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
+}
+
+}  // namespace

@@ -329,7 +329,7 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     *out = nullptr;
     if (!host_blob || d <= 0 || n_floats != tf_readout_blob_size(d)) return TF_EINVAL;
     if (dtype != TF_FP32 && dtype != TF_BF16 && dtype != TF_BF16_F16ACT) return TF_EINVAL;
-    if (d != 32 && d != 64 && d != 128 && d != 256) return TF_EUNSUPPORTED;
+    if (d != 32 && d != 64 && d != 128 && d != 192 && d != 256) return TF_EUNSUPPORTED;
     const bool half = dtype != TF_FP32;
     const size_t dd = (size_t)d;
     const int MT = d / 32;
@@ -435,6 +435,7 @@ extern "C" tf_status tf_decode_tracks(const float *states, int32_t n_tracks, con
         case 32: launch_d<32>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
         case 64: launch_d<64>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
         case 128: launch_d<128>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
+        case 192: launch_d<192>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
         case 256: launch_d<256>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
         default: return TF_EINVAL;
     }

@@ -51,35 +51,11 @@
 #include <type_traits>
 #include <vector>
 
+#include "common.h"
+#include "internal.h"
 #include "trackfit.h"
 
 namespace {
-
-typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
-typedef __attribute__((ext_vector_type(8))) _Float16 f16x8;
-typedef __attribute__((ext_vector_type(8))) float f32x8;
-typedef __attribute__((ext_vector_type(16))) float f32x16;
-typedef __attribute__((ext_vector_type(4))) float f32x4;
-typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
-
-// Matrix-core operand types.  OP_F32: fp32 weights and operands
-// (v_mfma_f32_32x32x2_f32).  OP_BF16: bf16 weights and bf16 activation
-// operands (v_mfma_f32_32x32x16_bf16).  OP_F16: bf16-valued weights held
-// exactly in fp16 and fp16 activation operands (v_mfma_f32_32x32x16_f16).
-// Accumulation is fp32 in all three.
-enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
-
-constexpr float kLog2e = 1.4426950408889634f;
-constexpr float kRmsEps = 1e-6f;
-// The fp32 gate clamps |pre-activation| to 80 and the 16-bit head clamps the
-// SiLU exponent to 80 log2(e), so that exp stays finite; the change in the
-// result is below exp(-80).
-constexpr float kGateClamp = 80.0f * kLog2e;
-constexpr int kLdsBytesMax = 160 * 1024;
-constexpr int kCopyBytes = 1024;  // one wave-wide 16-byte-per-lane copy
-
-constexpr int cmax(int a, int b) { return a > b ? a : b; }
-constexpr int round_up(int v, int m) { return (v + m - 1) / m * m; }
 
 // ---------------------------------------------------------------------------
 // Compile-time shape of one kernel instance.
@@ -150,44 +126,6 @@ struct KCfg {
     static_assert(KSPS >= KPB && KS1 % KSPS == 0, "head stage split");
 };
 
-template <int OP> struct Frag;
-template <> struct Frag<OP_BF16> {
-    typedef bf16x8 T;
-    typedef __bf16 E;
-    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ T pack(const float *v) {
-        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-        return __builtin_convertvector(f, bf16x8);
-    }
-};
-template <> struct Frag<OP_F16> {
-    typedef f16x8 T;
-    typedef _Float16 E;
-    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ f32x4 mma16(T a, T b, f32x4 c) {
-        return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ T pack(const float *v) {
-        f32x8 f = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7]};
-        return __builtin_convertvector(f, f16x8);
-    }
-};
-template <> struct Frag<OP_F32> {
-    typedef float T;
-    typedef float E;
-    static __device__ __forceinline__ f32x16 mma(T a, T b, f32x16 c) {
-        return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
-    }
-    static __device__ __forceinline__ T pack(const float *v) { return v[0]; }
-};
-
 // Device-side weights.
 struct DevParams {
     const float4 *emb;           // [D] (w_x, w_y, w_z, b) with the min-max map folded in; with
@@ -201,47 +139,10 @@ struct DevParams {
 };
 
 constexpr int kMaxFeat = 16;     // per-hit features of the Fourier front end, at most
+// What the encoder kernel writes: the pooled head's five outputs, the last
+// layer's end states, or (with no layers) the front end's output per hit.
+enum { OUT_HEAD = 0, OUT_STATES = 1, OUT_FRONT = 2 };
 constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
-
-__device__ __forceinline__ void wave_lds_sync() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-}
-
-// The lane index, read afresh: values derived from it are formed where they
-// are used instead of being held in registers across the whole kernel.
-__device__ __forceinline__ int fresh_lane() {
-    int l;
-    asm volatile("v_mbcnt_lo_u32_b32 %0, -1, 0\n\tv_mbcnt_hi_u32_b32 %0, -1, %0" : "=v"(l));
-    return l;
-}
-__device__ __forceinline__ int uniform(int v) { return __builtin_amdgcn_readfirstlane(v); }
-
-// Lane mask (wave-uniform, 64 bits) of the lanes whose stream has bit p set:
-// lanes 0-31 follow b0, lanes 32-63 follow b1.
-__device__ __forceinline__ unsigned long long half_mask(unsigned b0, unsigned b1, int p) {
-    typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
-    const u32x2 m = {(unsigned)((int)(b0 << (31 - p)) >> 31), (unsigned)((int)(b1 << (31 - p)) >> 31)};
-    return __builtin_bit_cast(unsigned long long, m);
-}
-
-// v in lanes outside m, 0 in lanes of m: one v_cndmask with the mask in SGPRs.
-__device__ __forceinline__ float zero_lanes(float v, unsigned long long m) {
-    float r;
-    asm("v_cndmask_b32_e64 %0, %1, 0, %2" : "=v"(r) : "v"(v), "s"(m));
-    return r;
-}
-
-// Tile hit index held in hit slot s (0 <= s < CAP).  Slot s = 32 n + 8 i + 4 g + j
-// is row 8 i + 4 g + j of hit tile n in the input projection; that row lands
-// in lanes of half g at accumulator register 4 i + j, which is position
-// 16 n + 4 i + j of stream g, i.e. tile hit SP * g + 16 n + 4 i + j.
-template <int SP>
-__device__ __forceinline__ int slot_to_hit(int s) {
-    int n = s >> 5, i = (s >> 3) & 3, g = (s >> 2) & 1, j = s & 3;
-    return SP * g + 16 * n + 4 * i + j;
-}
 
 // The head multiplies fp32 vectors (pooled stream, hidden layer) by the
 // weights: with 16-bit operands each vector is split into a rounded high part
@@ -278,66 +179,27 @@ __device__ __forceinline__ void store_fb_pair(char *ws, int p, float v0, float v
     }
 }
 
-// Copy of one weight stage from global memory straight into an LDS slot:
-// global_load_lds_dwordx4 moves 16 bytes per lane, 1 KiB per wave
-// instruction, into LDS at M0 + 16 * lane.  Each wave copies the pieces
-// w, w + WAVES, ...; waves with fewer pieces repeat the last one (same bytes to
-// the same place), so every wave issues exactly LPW loads per stage and can
-// wait for an older stage with a constant vmcnt.  The instruction is written
-// out because the compiler, which cannot tell the ring slots apart, would
-// otherwise wait for every such load before each LDS access; the kernel keeps
-// the count itself (wait_vmcnt).  The kernel has no other use of M0.
-__device__ __forceinline__ void lds_dma16(const void *gsrc, unsigned lds_addr) {
-    // one wait state between the M0 write and its use by the load
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
-                 :
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gsrc)
-                 : "memory", "m0");
-}
-
-// slot_lds: LDS byte address of the slot.
-template <class C>
-__device__ __forceinline__ void copy_stage(const unsigned char *stages, int s, unsigned slot_lds, int wid, int lane) {
-    const unsigned char *src = stages + (size_t)s * C::STAGE + lane * 16;
-#pragma unroll
-    for (int i = 0; i < C::LPW; ++i) {
-        int piece = wid + i * C::WAVES;
-        piece = piece < C::COPIES ? piece : C::COPIES - 1;
-        lds_dma16(src + piece * kCopyBytes, slot_lds + piece * kCopyBytes);
-    }
-}
-
-// Workgroup barrier that orders LDS only (the kernel shares nothing through
-// global memory within a workgroup).
-__device__ __forceinline__ void lds_barrier() {
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
-}
-
-// s_waitcnt vmcnt(N) with the other counters left alone (gfx9 encoding).
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-    static_assert(N >= 0 && N < 64, "vmcnt range");
-    __builtin_amdgcn_s_waitcnt((N & 15) | (7 << 4) | (15 << 8) | ((N >> 4) << 14));
-}
-
 // STATES: instead of the pooled head, write each track's last-layer end states
 // (the paper's own readout input): out is then [n_tracks][2d], the forward
 // state at the track's last hit in columns 0..d-1 and the reverse state at its
 // first hit in columns d..2d-1.  The last layer's output projection and the
 // head, whose results nothing reads in this form, are skipped.
+// OUT_FRONT (no layers): the front end's output per hit, as the next stage's
+// matrix operand type (FE), row (hit row - offsets[0]) of out [out_rows][d],
+// in channel order; rows of rejected tracks are not written.
 // FOURIER: the paper's front end instead of the (x, y, z) embedding: hits holds
 // n_feat features per hit, each min-max normalised in fp32 and expanded to
 // sin and cos of pi 2^s u, s = 0..15, and the 32 n_feat values are projected
 // to d on the matrix cores (the projection's weights stream through the stage
 // ring ahead of the first layer's).  Column k of that projection is feature
 // k / 32, cosine if bit 4 of k is set, scale k % 16.
-template <int D, int OP, int HT_, bool STATES, bool FOURIER>
+template <int D, int OP, int HT_, int OUTM, bool FOURIER>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
                           amdgpu_waves_per_eu(KCfg<D, OP, HT_>::WAVES / 4, KCfg<D, OP, HT_>::WAVES / 4)))
 void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
-                       int n_tracks, DevParams P, float *__restrict__ out, int *__restrict__ err) {
+                       int n_tracks, DevParams P, float *__restrict__ out, long long out_rows, int *__restrict__ err) {
+    constexpr bool STATES = OUTM == OUT_STATES;
+    constexpr bool FRONT = OUTM == OUT_FRONT;
     using C = KCfg<D, OP, HT_>;
     using F = Frag<OP>;
     using FT = typename F::T;
@@ -345,7 +207,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
     constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK, KPB = C::KPB, NCH = C::NCH;
     constexpr int MAXTR = C::MAXTR;
-    constexpr int OUTW = STATES ? 2 * D : 5;  // floats per output row
+    constexpr int OUTW = STATES ? 2 * D : 5;  // floats per output row (head, states)
 
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
     const int lane = threadIdx.x & 63;
@@ -437,7 +299,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             if (bad_m | empty_m | long_m) {
                 errbits |= (bad_m ? TF_DEVERR_BAD_OFFSETS : 0) | (empty_m ? TF_DEVERR_EMPTY_TRACK : 0) |
                            (long_m ? TF_DEVERR_TOO_LONG : 0);
-                if (fresh && (bad || empty || too_long)) {
+                if (!FRONT && fresh && (bad || empty || too_long)) {
 #pragma unroll
                     for (int e = 0; e < OUTW; ++e) out[(size_t)idx * OUTW + e] = qnan;
                 }
@@ -503,7 +365,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             const unsigned long long vstart = smask | (n < 64 ? (1ull << n) : 0ull);
             const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
             const unsigned int spm = SP >= 32 ? 0xffffffffu : ((1u << SP) - 1);
-            if constexpr (STATES) {
+            if constexpr (STATES || FRONT) {
                 st0 = unsigned(smask) & spm;
                 st1 = unsigned(smask >> SP) & spm;
             }
@@ -860,6 +722,38 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         if constexpr (STATES) {
             for (int l = 0; l + 1 < P.n_layers; ++l) layer(std::false_type{});
             layer(std::true_type{});
+        } else if constexpr (FRONT) {
+            // the front end's output of each hit: lane (hh, cc) holds channels
+            // 32 m + 8 (q/4) + 4 hh + 0..3 of hit slot 32 nt + cc, four consecutive
+            // channels per register quad
+            if (work) {
+                const int row0 = offsets[0];
+                FE *xo = reinterpret_cast<FE *>(out);
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt) {
+                    const int th = slot_to_hit<SP>(32 * nt + cc);
+                    if (th < n) {
+                        // the track of tile row th: the number of track starts up to it, less one
+                        const int j = (th < SP ? __builtin_popcount(st0 & ((2u << th) - 1u))
+                                               : __builtin_popcount(st0) +
+                                                     __builtin_popcount(st1 & ((2u << (th - SP)) - 1u))) - 1;
+                        const long long row = (long long)t_off[j] + (th - t_start[j]) - row0;
+                        if (row >= 0 && row < out_rows) {
+                            FE *dst = xo + (size_t)row * D + 4 * hh;
+#pragma unroll
+                            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                                for (int g = 0; g < 4; ++g) {
+                                    typedef FE e4 __attribute__((ext_vector_type(4)));
+                                    typedef float f4 __attribute__((ext_vector_type(4)));
+                                    const f4 v = {r[m][nt][4 * g], r[m][nt][4 * g + 1], r[m][nt][4 * g + 2],
+                                                  r[m][nt][4 * g + 3]};
+                                    *reinterpret_cast<e4 *>(dst + 32 * m + 8 * g) = __builtin_convertvector(v, e4);
+                                }
+                        }
+                    }
+                }
+            }
         } else {
             for (int l = 0; l < P.n_layers; ++l) layer(std::false_type{});
         }
@@ -887,7 +781,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // unrolled, so that the residual block pooled at each step is a fixed register block
 #pragma unroll
             for (int j = 0; j < C::NH1; ++j) {
-                if (work && !STATES) {
+                if (work && OUTM == OUT_HEAD) {
                     const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
                     for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
@@ -983,7 +877,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
             // operand, output row q of column cc is output q of track cc
             if constexpr (C::HEAD16) {
-              if (work && !STATES) {
+              if (work && OUTM == OUT_HEAD) {
                 // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
                 // stored W2 fragments follow that order); output rows 4 hg + i
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
@@ -1015,7 +909,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     }
                 }
               }
-            } else if (work && !STATES) {
+            } else if (work && OUTM == OUT_HEAD) {
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
                 const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
                 f32x16 o;
@@ -1372,9 +1266,9 @@ extern "C" void tf_weights_destroy(tf_weights *w) {
 extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
 
 namespace {
-template <int D, int OP, int HT, bool STATES, bool FOURIER>
+template <int D, int OP, int HT, int OUTM, bool FOURIER>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                  const tf_weights *w, float *out, hipStream_t stream) {
+                  const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
     using C = KCfg<D, OP, HT>;
     // one workgroup per compute unit (the LDS ring and the register file are
     // sized for it), at least 8 tracks per wave
@@ -1383,57 +1277,69 @@ hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int
     const long long cap = (long long)w->cu_count;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, STATES, FOURIER>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
-                       hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, w->err);
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, OUTM, FOURIER>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+                       hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, out_rows, w->err);
     return hipGetLastError();
 }
 
-template <int D, int OP, bool STATES, bool FOURIER>
+template <int D, int OP, int OUTM, bool FOURIER>
 hipError_t launch_ht(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                     const tf_weights *w, float *out, hipStream_t stream) {
+                     const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
     if constexpr (D <= 128) {
         if (w->max_hits == 64)
-            return launch<D, OP, 2, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            return launch<D, OP, 2, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
     }
-    return launch<D, OP, 1, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    return launch<D, OP, 1, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
 }
 
-template <int D, bool STATES, bool FOURIER>
+template <int D, int OUTM, bool FOURIER>
 hipError_t launch_d(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                    const tf_weights *w, float *out, hipStream_t stream) {
+                    const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
     switch (w->dtype) {
         case TF_BF16:
-            return launch_ht<D, OP_BF16, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            return launch_ht<D, OP_BF16, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
         case TF_BF16_F16ACT:
-            return launch_ht<D, OP_F16, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+            return launch_ht<D, OP_F16, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
         default:
             if constexpr (D <= 128)
-                return launch_ht<D, OP_F32, STATES, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, stream);
+                return launch_ht<D, OP_F32, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows,
+                                                           stream);
             return hipErrorNotSupported;
     }
 }
 
-template <bool STATES>
+template <int OUTM>
 tf_status launch_any(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                     const tf_weights *w, float *out, hipStream_t stream) {
+                     const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
     hipError_t e;
-    if (w->n_feat > 0) {
-        // the Fourier front end is built for the paper's width (128) and the small test width
+    // the Fourier front end and the front-end-only pass are built for the paper's
+    // width (128) and the small test width (32)
+    if (w->n_feat > 0 || OUTM == OUT_FRONT) {
+        const bool four = w->n_feat > 0;
         switch (w->d) {
-            case 32: e = launch_d<32, STATES, true>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-            case 128: e = launch_d<128, STATES, true>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
+            case 32:
+                e = four ? launch_d<32, OUTM, true>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream)
+                         : launch_d<32, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
+                break;
+            case 128:
+                e = four ? launch_d<128, OUTM, true>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream)
+                         : launch_d<128, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
+                break;
             default: return TF_EUNSUPPORTED;
         }
         return e == hipSuccess ? TF_OK : TF_EHIP;
     }
-    switch (w->d) {
-        case 32: e = launch_d<32, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 64: e = launch_d<64, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 128: e = launch_d<128, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        case 256: e = launch_d<256, STATES, false>(hits, n_hits, offsets, n_tracks, w, out, stream); break;
-        default: return TF_EUNSUPPORTED;
+    if constexpr (OUTM != OUT_FRONT) {
+        switch (w->d) {
+            case 32: e = launch_d<32, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream); break;
+            case 64: e = launch_d<64, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream); break;
+            case 128: e = launch_d<128, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream); break;
+            case 256: e = launch_d<256, OUTM, false>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream); break;
+            default: return TF_EUNSUPPORTED;
+        }
+        return e == hipSuccess ? TF_OK : TF_EHIP;
     }
-    return e == hipSuccess ? TF_OK : TF_EHIP;
+    return TF_EUNSUPPORTED;
 }
 }  // namespace
 
@@ -1442,7 +1348,7 @@ extern "C" tf_status fit_tracks(const float *hits, int64_t n_hits, const int32_t
     if (!w || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
     if (n_tracks == 0) return TF_OK;
     if (!offsets || !out || (!hits && n_hits > 0)) return TF_EINVAL;
-    return launch_any<false>(hits, n_hits, offsets, n_tracks, w, out, stream);
+    return launch_any<OUT_HEAD>(hits, n_hits, offsets, n_tracks, w, out, 0, stream);
 }
 
 extern "C" tf_status fit_tracks_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
@@ -1451,7 +1357,15 @@ extern "C" tf_status fit_tracks_states(const float *hits, int64_t n_hits, const 
     if (w->n_layers < 1) return TF_EUNSUPPORTED;  // no scan, no states
     if (n_tracks == 0) return TF_OK;
     if (!offsets || !states || (!hits && n_hits > 0)) return TF_EINVAL;
-    return launch_any<true>(hits, n_hits, offsets, n_tracks, w, states, stream);
+    return launch_any<OUT_STATES>(hits, n_hits, offsets, n_tracks, w, states, 0, stream);
+}
+
+tf_status tf_internal_front_end(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                                const tf_weights *w, void *x0, long long rows, hipStream_t stream) {
+    if (!w || w->n_layers != 0 || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
+    if (n_tracks == 0) return TF_OK;
+    if (!offsets || !x0 || (!hits && n_hits > 0)) return TF_EINVAL;
+    return launch_any<OUT_FRONT>(hits, n_hits, offsets, n_tracks, w, static_cast<float *>(x0), rows, stream);
 }
 
 extern "C" tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear) {

@@ -1,0 +1,155 @@
+"""GPU parity of the paper's bidirectional minGRU backbone (tf_mingru_states)
+against the fp64 oracle, element by element: end states on three workloads
+(the (x, y, z) front end at d = 32, H = 64 and the Fourier front end at the
+paper's d = 128, H = 192), ragged batches, rejected tracks, a workspace too
+small for the batch, tile independence, and the chain into the 35-quantile
+readout and decode.
+"""
+import dataclasses
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import tracksynth as ts
+from tests.parity import TOL
+
+torch = pytest.importorskip("torch")
+pytestmark = pytest.mark.gpu
+
+THREADS = int(os.environ.get("ORACLE_THREADS", "0"))
+N = {"mingru2_h64_tiny_d32_fp32": 256, "mingru2_h192_fourier15_d128_fp32_65k": 1024,
+     "mingru2_h192_fourier15_deploy_bf16_8m": 2048}
+
+
+@pytest.fixture(scope="module")
+def tf():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2609_32479_amd as tf
+    return tf
+
+
+def _inputs(w, n, hits=None, offs=None):
+    if hits is None:
+        hits, offs = ts.make_tracks(w, n_tracks=n)
+    if not w.n_features:
+        return hits, offs
+    _, sf, _ = oracle.seed_tracks(hits, offs, w.b_field)
+    return ts.hit_features(w, hits, offs, np.nan_to_num(sf, nan=0.0)), offs
+
+
+def _model(tf, w):
+    blob = ts.make_mingru_weights(w)
+    M = tf.MinGRU(blob, w.n_layers, w.d_model, w.hidden, tf.MODE_FOR_WEIGHTS[w.dtype], w.n_features)
+    return M, blob
+
+
+def _gpu(M, inp, offs, n_tracks=None, ws_rows=None):
+    h = torch.from_numpy(np.ascontiguousarray(inp, dtype=np.float32)).cuda()
+    o = torch.from_numpy(np.ascontiguousarray(offs, dtype=np.int32)).cuda()
+    n = offs.size - 1 if n_tracks is None else n_tracks
+    rows = int(offs[n] - offs[0]) if ws_rows is None else ws_rows
+    ws = torch.empty(M.workspace_bytes(rows), dtype=torch.uint8, device="cuda")
+    st = M.states(h, o, workspace=ws, n_tracks=n_tracks)
+    torch.cuda.synchronize()
+    return st.cpu().numpy()
+
+
+def _ref(w, inp, offs, blob):
+    return oracle.mingru_states(inp, offs, blob, w.n_layers, w.d_model, w.hidden, n_features=w.n_features,
+                                n_threads=THREADS)
+
+
+def _state_err(g, r):
+    assert np.array_equal(np.isnan(g), np.isnan(r))
+    ok = ~np.isnan(r).any(axis=1)
+    rms = np.sqrt(np.mean(r[ok] ** 2, axis=1, keepdims=True))
+    return float(np.max(np.abs(g[ok] - r[ok]) / rms)) if ok.any() else 0.0
+
+
+@pytest.mark.parametrize("name", list(ts.MINGRU_WORKLOADS))
+def test_mingru_states_match_oracle(tf, name):
+    w = ts.workload(name)
+    print(f"[mingru] {name} n={N[name]}", flush=True)
+    M, blob = _model(tf, w)
+    inp, offs = _inputs(w, N[name])
+    g = _gpu(M, inp, offs)
+    r = _ref(w, inp, offs, blob)
+    assert g.shape == (N[name], 2 * w.hidden)
+    e = _state_err(g, r)
+    print(f"[mingru] {name}: max err {e:.3g} of the track's state rms", flush=True)
+    assert e <= TOL[w.dtype]
+    assert M.device_error() == 0
+
+
+@pytest.mark.parametrize("name", ["mingru2_h192_fourier15_deploy_bf16_8m", "mingru2_h64_tiny_d32_fp32"])
+def test_mingru_ragged_batches_bad_tracks_small_workspace(tf, name):
+    w0 = ts.workload(name)
+    M, blob = _model(tf, w0)
+    w = dataclasses.replace(w0, len_min=1, len_max=32, n_det_layers=32)
+    inp, offs = _inputs(w, 500)
+    r_all = _ref(w, inp, offs, blob)
+    for n in (1, 2, 33, 500):
+        g = _gpu(M, inp, offs[: n + 1], n_tracks=n)
+        assert _state_err(g, r_all[:n]) <= TOL[w.dtype], n
+    assert M.device_error() == 0
+    # track 3 emptied, track 7 longer than 32: NaN rows, the rest unchanged
+    Lk = np.diff(offs)
+    Lk[3], Lk[7] = 0, 33
+    rows = [np.resize(np.arange(offs[i], offs[i + 1]), Lk[i]) if Lk[i] else np.arange(0) for i in range(500)]
+    inp2 = inp[np.concatenate(rows)]
+    o2 = np.concatenate([[0], np.cumsum(Lk)]).astype(np.int32)
+    g = _gpu(M, inp2, o2)
+    assert np.all(np.isnan(g[[3, 7]]))
+    good = np.ones(500, bool)
+    good[[3, 7]] = False
+    assert _state_err(g[good], r_all[good]) <= TOL[w.dtype]
+    assert M.device_error() == (tf.DEVERR_EMPTY_TRACK | tf.DEVERR_TOO_LONG)
+    # a workspace for the first 200 tracks' rows only: the later tracks are refused
+    g = _gpu(M, inp, offs, ws_rows=int(offs[200] - offs[0]))
+    assert _state_err(g[:200], r_all[:200]) <= TOL[w.dtype]
+    assert np.all(np.isnan(g[200:]))
+    assert M.device_error() & tf.DEVERR_BAD_OFFSETS
+
+
+def test_mingru_tile_independence_and_absolute_offsets(tf):
+    w = ts.workload("mingru2_h192_fourier15_deploy_bf16_8m")
+    M, blob = _model(tf, w)
+    inp, offs = _inputs(w, 3000)
+    a = _gpu(M, inp, offs)
+    assert np.array_equal(a, _gpu(M, inp, offs))
+    perm = np.random.default_rng(5).permutation(3000)
+    L = np.diff(offs)
+    ip = np.concatenate([inp[offs[i]:offs[i + 1]] for i in perm])
+    op = np.concatenate([[0], np.cumsum(L[perm])]).astype(np.int32)
+    assert np.array_equal(_gpu(M, ip, op), a[perm])
+    # tracks 1000..1999 through absolute offsets into the whole array
+    g = _gpu(M, inp, offs[1000:], n_tracks=1000)
+    assert np.array_equal(g, a[1000:2000])
+
+
+@pytest.mark.parametrize("name", ["mingru2_h192_fourier15_deploy_bf16_8m", "mingru2_h192_fourier15_d128_fp32_65k"])
+def test_mingru_chain_into_readout_and_decode(tf, name):
+    """hits -> seed (features, seeds), backbone end states, 35-quantile head of
+    hidden width H on the 2H states, median and decode: against the oracle's
+    chain on the same features."""
+    w = ts.workload(name)
+    M, blob = _model(tf, w)
+    hits, offs = ts.make_tracks(w, n_tracks=1500)
+    seeds, sf, _ = oracle.seed_tracks(hits, offs, w.b_field)
+    feats = ts.hit_features(w, hits, offs, sf)
+    mode = tf.MODE_FOR_WEIGHTS[w.dtype]
+    hb = ts.make_readout_weights(dataclasses.replace(w, d_model=w.hidden))
+    R = tf.Readout(hb, w.hidden, mode)
+    st = _gpu(M, feats, offs)
+    out, q = tf.decode_tracks(torch.from_numpy(st).cuda(), torch.from_numpy(seeds).cuda(), R, quantiles=True)
+    torch.cuda.synchronize()
+    r_q, r_out = oracle.readout_tracks(_ref(w, feats, offs, blob), seeds, hb, w.hidden)
+    from tests.test_readout_gpu import colerr, wrap_phi, head_tols
+    eq = colerr(q.cpu().numpy(), r_q)
+    eo = colerr(wrap_phi(out.cpu().numpy(), r_out), r_out)
+    print(f"[mingru-chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
+    tq, _ = head_tols(mode, w.hidden)
+    assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]
