@@ -14,6 +14,12 @@ residual features (tf_seed_tracks) over the same tracks, one call per step.
 encoder up to the last layer's end states (fit_tracks_states), and the
 35-quantile head with its medians and seed-anchored decode (tf_decode_tracks),
 three launches per batch, the step again captured in one HIP graph.
+
+``--path paper`` times the paper's own deployed model per batch (workload
+mingru2_h192_fourier15_deploy_bf16_8m): the seed writing the three seed
+features into the 15-feature rows, the Fourier front end and the two
+bidirectional minGRU layers (tf_mingru_states), and the 35-quantile readout
+with its decode, in one HIP graph.
 """
 import argparse
 import json
@@ -413,6 +419,166 @@ def bench_readout(args, w, hits, offs, mode, batch):
     print(json.dumps(res), flush=True)
 
 
+PAPER_METRIC = ("tracks/sec (the paper's deployed model: fp64 seed + Fourier front end + 2 bidirectional minGRU "
+                "layers + 35-quantile readout and decode) on 1 MI355X; MFMA util vs peak")
+PAPER_H100_TRACKS_PER_S = 5.41e6  # the paper's deployed minGRU on one H100 NVL (context: another device, its data)
+
+
+def mingru_algorithmic_flops(w, n_hits):
+    """Per hit: the front end (2 x 32 F x d, or 6 d) and 2 x D_l x 4H per
+    layer (D_0 = d, then 2H).  The sines and cosines are not counted."""
+    f = front_flops(w.d_model, n_hits, w.n_features)
+    for l in range(w.n_layers):
+        din = w.d_model if l == 0 else 2 * w.hidden
+        f += 2.0 * din * 4 * w.hidden * n_hits
+    return f
+
+
+def paper_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
+    """The oracle's chain for the paper's model (seed and its features, Fourier
+    front end and minGRU layers, readout and decode) on a bounded sample."""
+    import oracle
+    n_all = offs.size - 1
+    rng = np.random.default_rng(7)
+
+    def run(sel):
+        L = offs[sel + 1] - offs[sel]
+        h = np.concatenate([hits[offs[i]:offs[i + 1]] for i in sel])
+        o = np.concatenate([[0], np.cumsum(L)]).astype(np.int32)
+        t0 = time.perf_counter()
+        seeds, sf, _ = oracle.seed_tracks(h, o, w.b_field)
+        feats = ts.hit_features(w, h, o, np.nan_to_num(sf, nan=0.0))
+        st = oracle.mingru_states(feats, o, blob, w.n_layers, w.d_model, w.hidden, n_features=w.n_features,
+                                  n_threads=threads)
+        _, out = oracle.readout_tracks(st, seeds, hb, w.hidden)
+        return out, time.perf_counter() - t0
+
+    idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
+    _, dt = run(idx)
+    n = int(min(n_all, max(256, 256 * seconds / max(dt, 1e-3))))
+    sel = np.sort(rng.choice(n_all, size=n, replace=False))
+    ref, dt = run(sel)
+    g = gpu_out[sel].copy()
+    g[:, 2] -= np.round((g[:, 2] - ref[:, 2]) / (2 * np.pi)) * 2 * np.pi
+    rms = np.sqrt(np.mean(ref ** 2, axis=0))
+    err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), rms)))
+    return {"value": n / dt, "unit": "tracks/s", "cores": oracle.threads(threads), "kind": "oracle",
+            "sample": f"{n} tracks drawn without replacement (seed 7) from the {n_all}-track workload, "
+                      f"fp64 C oracle (seed and features, Fourier front end, minGRU layers, readout, decode), "
+                      f"{dt:.1f} s wall",
+            "parity_max_col_err_on_sample": err}
+
+
+def bench_paper(args, w, hits, offs, mode, batch):
+    import dataclasses
+    import torch
+    import paper_2609_32479_amd as tf
+    assert w.arch == "mingru", "--path paper takes a minGRU workload"
+    dev = torch.device("cuda:0")
+    h = torch.from_numpy(hits).to(dev)
+    o = torch.from_numpy(offs).to(dev)
+    n_tracks = offs.size - 1
+    n_hits = int(offs[-1] - offs[0])
+    H = w.hidden
+    blob = ts.make_mingru_weights(w)
+    hb = ts.make_readout_weights(dataclasses.replace(w, d_model=H))
+    M = tf.MinGRU(blob, w.n_layers, w.d_model, H, mode, w.n_features)
+    R = tf.Readout(hb, H, mode)
+    feats = device_features(tf, w, hits, offs, h, o, dev)
+    seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
+    out = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
+    states = torch.empty((batch, 2 * H), dtype=torch.float32, device=dev)
+    starts = list(range(0, n_tracks, batch))
+    rows_max = max(int(offs[min(s0 + batch, n_tracks)] - offs[s0]) for s0 in starts)
+    ws = torch.empty(M.workspace_bytes(rows_max), dtype=torch.uint8, device=dev)
+
+    def one(s0, stream):
+        n = min(batch, n_tracks - s0)
+        r0 = int(offs[s0] - offs[0])
+        tf.seed_tracks(h, o[s0:], w.b_field, seeds=seeds[s0:], n_tracks=n, stream=stream,
+                       feats=feats[r0:, ts.N_MEASURED:ts.N_MEASURED + 3])
+        M.states(feats, o[s0:], out=states, workspace=ws, n_tracks=n, stream=stream)
+        tf.decode_tracks(states[:n], seeds[s0:s0 + n], R, out=out[s0:], stream=stream)
+
+    def step(stream=None):
+        for s0 in starts:
+            one(s0, stream)
+
+    torch.cuda.synchronize()
+    step()
+    torch.cuda.synchronize()
+    # per-call time of the dominant call (front end + minGRU layers), eager, events on its stream
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in starts]
+    for (a, b), s0 in zip(ev, starts):
+        a.record()
+        M.states(feats, o[s0:], out=states, workspace=ws, n_tracks=min(batch, n_tracks - s0))
+        b.record()
+    torch.cuda.synchronize()
+    call_ms = np.array([a.elapsed_time(b) for a, b in ev])
+
+    graph = None
+    if not args.no_graph:
+        side = torch.cuda.Stream()
+        graph = torch.cuda.CUDAGraph()
+        with torch.cuda.stream(side):
+            step(side)
+            torch.cuda.synchronize()
+            with torch.cuda.graph(graph, stream=side):
+                step(side)
+        torch.cuda.synchronize()
+
+    def run_step():
+        if graph is not None:
+            graph.replay()
+        else:
+            step()
+
+    for _ in range(args.warmup):
+        run_step()
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t_wall = time.perf_counter()
+    e0.record()
+    for _ in range(args.steps):
+        run_step()
+    e1.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_wall
+    ms_per_step = e0.elapsed_time(e1) / args.steps
+    flags = M.device_error()
+    gpu_out = out.cpu().numpy()
+    per_call = mingru_algorithmic_flops(w, n_hits) / len(starts)
+    call_avg = float(call_ms.mean())
+    achieved = per_call / (call_avg / 1e3) / 1e12
+    peak = PEAK_TFLOPS[mode]
+    value = n_tracks / (ms_per_step / 1e3)
+    res = {
+        "metric": PAPER_METRIC, "value": value, "unit": "tracks/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": ms_per_step, "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": {"fp32": "f32", "bf16": "bf16", "bf16_f16act": "bf16 weights, f16 activations, f32 accumulate"}[mode]
+                 + "; seed and decode f64",
+        "data": "synthetic helix tracks (2 T solenoid, seeded), synthetic per-hit features, random-init weights",
+        "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
+                   "launches_per_call": 5, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model,
+                   "hidden": H, "n_features": w.n_features, "mode": mode, "hip_graph": graph is not None},
+        "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
+                     "traffic": None, "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
+                     "kernel_avg_ms": call_avg, "flops_per_launch": per_call},
+        "context": {"paper_h100_nvl_tracks_per_s": PAPER_H100_TRACKS_PER_S,
+                    "ratio_to_paper_h100": value / PAPER_H100_TRACKS_PER_S,
+                    "note": "the paper's deployed model on its own data and device; not the same inputs"},
+        "host_wall_s": wall,
+        "device_error_flags": flags,
+        "finite_outputs": bool(np.isfinite(gpu_out).all()),
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = paper_cpu_baseline(w, blob, hb, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
+    if args.copy_calibration:
+        copy_calibration(dev)
+    print(json.dumps(res), flush=True)
+
+
 def copy_calibration(dev):
     """A plain elementwise device copy of known size, for scaling HBM counters."""
     import torch
@@ -428,8 +594,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="deploy_d128x4_bf16_8m",
-                    choices=list(ts.WORKLOADS) + list(ts.FOURIER_WORKLOADS))
+    ap.add_argument("--workload", default=None,
+                    choices=list(ts.WORKLOADS) + list(ts.FOURIER_WORKLOADS) + list(ts.MINGRU_WORKLOADS),
+                    help="default: deploy_d128x4_bf16_8m (mingru2_h192_fourier15_deploy_bf16_8m for --path paper)")
     ap.add_argument("--mode", default=None, help="library mode: fp32, bf16 or bf16_f16act")
     ap.add_argument("--n-tracks", type=int, default=None, help="override the workload's track count")
     ap.add_argument("--batch", type=int, default=None, help="tracks per fit_tracks call")
@@ -439,9 +606,10 @@ def main():
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true")
-    ap.add_argument("--path", default="encoder", choices=["encoder", "seed", "readout"],
+    ap.add_argument("--path", default="encoder", choices=["encoder", "seed", "readout", "paper"],
                     help="encoder: fit_tracks (default); seed: tf_seed_tracks with features; "
-                         "readout: seed + fit_tracks_states + tf_decode_tracks")
+                         "readout: seed + fit_tracks_states + tf_decode_tracks; "
+                         "paper: seed + tf_mingru_states + tf_decode_tracks")
     ap.add_argument("--copy-calibration", action="store_true",
                     help=f"after the timed region, run a plain {COPY_MIB} MiB device copy (for counter calibration)")
     args = ap.parse_args()
@@ -455,6 +623,8 @@ def main():
     import torch
     import paper_2609_32479_amd as tf
 
+    if args.workload is None:
+        args.workload = "mingru2_h192_fourier15_deploy_bf16_8m" if args.path == "paper" else "deploy_d128x4_bf16_8m"
     w = ts.workload(args.workload)
     mode = args.mode or tf.MODE_FOR_WEIGHTS[w.dtype]
     n_tracks = args.n_tracks or w.n_tracks
@@ -470,6 +640,9 @@ def main():
         return
     if args.path == "readout":
         bench_readout(args, w, hits, offs, mode, batch)
+        return
+    if args.path == "paper":
+        bench_paper(args, w, hits, offs, mode, batch)
         return
     blob = model_blob(w)
 
