@@ -54,7 +54,11 @@ struct MCfg {
     static constexpr int STAGE = round_up(KIN * FRAG + 32 * 4, kCopyBytes);  // one weight block + its bias
     static constexpr int COPIES = STAGE / kCopyBytes;
     static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;
-    static constexpr int WAVE_BYTES = 4 * kMgMaxTr * 4 + kMgCap * 4;  // track table, row map
+    // wave-private LDS: track table and row map, then the output transpose tile
+    // [32 rows][32 channels] (row stride padded by 16 bytes)
+    static constexpr int ROWB = 32 * EB + 16;
+    static constexpr int TB_OFF = 4 * kMgMaxTr * 4 + kMgCap * 4;
+    static constexpr int WAVE_BYTES = TB_OFF + kMgCap * ROWB;
     static constexpr int NSLOT_FIT = (kLdsBytesMax - WAVES * WAVE_BYTES) / STAGE;
     static constexpr int NSLOT = NSLOT_FIT > 4 ? 4 : NSLOT_FIT;
     static_assert(NSLOT >= 2, "stage ring");
@@ -291,9 +295,15 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                                 states[(size_t)t_id[j] * 2 * H + col] = AX[i];
                             }
                     } else {
+                        // through the wave's LDS tile, so that each lane stores 16 bytes
+                        // of one row at a time instead of one value per row
+                        constexpr int ROWE = C::ROWB / (int)sizeof(FE);  // tile row stride (elements)
+                        constexpr int VPP = 16 / (int)sizeof(FE);        // values per 16-byte piece
+                        constexpr int PPR = 32 / VPP;                    // pieces per row
+                        FE *tb = reinterpret_cast<FE *>(smem + C::WAVE0 + wid * C::WAVE_BYTES + C::TB_OFF);
+                        wave_lds_sync();  // the previous block's reads of the tile are done
 #pragma unroll
                         for (int i = 0; i < SP; ++i) {
-                            const int yr = rowmap[SP * hh + i];
                             // the asm keeps the state's last update (rounded to fp32) and its
                             // conversion to the operand type apart: fused into one
                             // mixed-precision fma at some positions, they would round once
@@ -301,7 +311,16 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                             // in the tile it lies
                             float v = AX[i];
                             asm volatile("" : "+v"(v));
-                            if (yr >= 0) Y[(size_t)yr * 2 * H + col] = (FE)v;
+                            tb[(SP * hh + i) * ROWE + cc] = (FE)v;
+                        }
+                        wave_lds_sync();
+#pragma unroll
+                        for (int it = lane; it < 32 * PPR; it += 64) {
+                            const int row = it / PPR, g = it % PPR;
+                            const int yr = rowmap[row];
+                            if (yr >= 0)
+                                *reinterpret_cast<u32x4 *>(Y + (size_t)yr * 2 * H + dir * H + 32 * ch + g * VPP) =
+                                    *reinterpret_cast<const u32x4 *>(tb + row * ROWE + g * VPP);
                         }
                     }
                 }
