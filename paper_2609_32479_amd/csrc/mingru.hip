@@ -51,7 +51,13 @@ struct MCfg {
     // 16-bit operands: two waves per SIMD (256 registers: the input operands
     // take DIN / 4); fp32 operands: one (DIN / 2 of the 512)
     static constexpr int WAVES = HALF ? 8 : 4;
-    static constexpr int STAGE = round_up(KIN * FRAG + 32 * 4, kCopyBytes);  // one weight block + its bias
+    // one weight block: a 32-row slice of the candidate or gate rows, then its 32 biases
+    static constexpr int BLOCK = round_up(KIN * FRAG + 32 * 4, 16);
+    // a stage holds one block, or both blocks of a chunk and direction when two
+    // slots of that size still leave room for a ring of at least three
+    static constexpr bool MERGE = 3 * round_up(2 * BLOCK, kCopyBytes) + WAVES * (4 * kMgMaxTr * 4 + kMgCap * 4 + kMgCap * (32 * EB + 16)) <= kLdsBytesMax;
+    static constexpr int STAGE = round_up((MERGE ? 2 : 1) * BLOCK, kCopyBytes);
+    static constexpr int SPC = MERGE ? 1 : 2;  // stages per chunk and direction
     static constexpr int COPIES = STAGE / kCopyBytes;
     static constexpr int LPW = (COPIES + WAVES - 1) / WAVES;
     // wave-private LDS: track table and row map, then the output transpose tile
@@ -107,7 +113,7 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
     using F = Frag<OP>;
     using FT = typename F::T;
     using FE = typename F::E;
-    constexpr int K = C::K, KL = C::KL, KIN = C::KIN, NCHK = H / 32, S = 4 * NCHK, SP = kMgSP;
+    constexpr int K = C::K, KL = C::KL, KIN = C::KIN, NCHK = H / 32, S = 2 * C::SPC * NCHK, SP = kMgSP;
     static_assert(H % 32 == 0, "hidden width");
 
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
@@ -247,11 +253,13 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                     __builtin_amdgcn_s_setprio(0);
                     ax += reinterpret_cast<const float *>(slot() + KIN * C::FRAG)[cc];
                 }
-                advance(false);
+                if constexpr (!C::MERGE) advance(false);
+                // the gate block: the next stage, or the second block of this one
+                const char *gsl = slot() + (C::MERGE ? C::BLOCK : 0);
                 if (work) {
                     // gate block: rows dir 2H + H + 32 ch + cc; bias pre-scaled by -log2(e)
                     // in the 16-bit modes (exp2 below)
-                    const FT *wf = reinterpret_cast<const FT *>(slot());
+                    const FT *wf = reinterpret_cast<const FT *>(gsl);
                     f32x16 gx;
 #pragma unroll
                     for (int i = 0; i < 16; ++i) gx[i] = 0.f;
@@ -259,7 +267,7 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
 #pragma unroll
                     for (int ks = 0; ks < KIN; ++ks) gx = F::mma(xa[ks], wf[ks * 64 + lane], gx);
                     __builtin_amdgcn_s_setprio(0);
-                    const float bgv = reinterpret_cast<const float *>(slot() + KIN * C::FRAG)[cc];
+                    const float bgv = reinterpret_cast<const float *>(gsl + KIN * C::FRAG)[cc];
                     float AX[SP], CF[SP];
 #pragma unroll
                     for (int i = 0; i < SP; ++i) {
@@ -354,15 +362,19 @@ hipError_t launch_last(bool last, const void *X, long long x_rows, const int32_t
                 : launch_layer<OP, DIN, H, false>(X, x_rows, offsets, n_tracks, stages, Y, states, err, cu_count, stream);
 }
 
-// Stage geometry of a layer for the host: bytes per stage.
+// Stage geometry of a layer for the host: bytes per stage, per block, and
+// whether a chunk's candidate and gate blocks share a stage.
+struct MGeom {
+    int stage, block, merge;
+};
 template <int OP, int DIN>
-int stage_bytes() {
-    return MCfg<OP, DIN>::STAGE;
+MGeom stage_bytes() {
+    return {MCfg<OP, DIN>::STAGE, MCfg<OP, DIN>::BLOCK, MCfg<OP, DIN>::MERGE ? 1 : 0};
 }
 
 int op_of(int32_t dtype) { return dtype == TF_BF16 ? OP_BF16 : dtype == TF_BF16_F16ACT ? OP_F16 : OP_F32; }
 
-int stage_bytes_of(int op, int din) {
+MGeom stage_bytes_of(int op, int din) {
     switch (op) {
         case OP_BF16:
         case OP_F16:
@@ -460,21 +472,25 @@ extern "C" tf_status tf_mingru_create(const tf_mingru_config *cfg, const float *
     for (int l = 0; l < L; ++l) {
         const int din = l == 0 ? d : 2 * H;
         loff[l] = total;
-        total += (size_t)4 * (H / 32) * stage_bytes_of(op, din);
+        const MGeom g = stage_bytes_of(op, din);
+        total += (size_t)(g.merge ? 2 : 4) * (H / 32) * g.stage;
     }
     const size_t err_off = total;
     total += 256;
     std::vector<unsigned char> hb(total, 0);
     const float *lw = blob + front_floats(d, nf);
     for (int l = 0; l < L; ++l) {
-        const int din = l == 0 ? d : 2 * H, SB = stage_bytes_of(op, din), KIN = din / K;
+        const int din = l == 0 ? d : 2 * H, KIN = din / K;
+        const MGeom g = stage_bytes_of(op, din);
         const float *W = lw, *b = lw + (size_t)4 * H * din;
         unsigned char *dst = hb.data() + loff[l];
         for (int ch = 0; ch < H / 32; ++ch)
             for (int dir = 0; dir < 2; ++dir)
                 for (int part = 0; part < 2; ++part) {
+                    // the candidate block starts a stage; the gate block follows it in the
+                    // same stage (merged) or starts the next one
                     unsigned char *sp = dst;
-                    dst += SB;
+                    dst += (g.merge && part == 0) ? g.block : (g.merge ? g.stage - g.block : g.stage);
                     const int rbase = dir * 2 * H + part * H + 32 * ch;
                     size_t o = 0;
                     for (int ks = 0; ks < KIN; ++ks)
