@@ -37,19 +37,52 @@ import tracksynth as ts  # noqa: E402
 METRIC = "tracks/sec (encoder+head forward) on 1 MI355X; MFMA util / HBM GB/s vs peak"
 PEAK_TFLOPS = {"fp32": 157.3, "bf16": 2516.6, "bf16_f16act": 2516.6}  # dense MFMA, MI355X datasheet
 PEAK_HBM_GBS = 8000.0
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc", "trackfit.hip")
+CSRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc")
 COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 
-# HBM bytes per launch of the deployment workload's 262 144-track call, from two
-# rocprofv3 --pmc runs (FETCH_SIZE, then WRITE_SIZE) of this script with
-# --copy-calibration, each scaled by the same counter's reading for a plain
-# device copy of known size (profiles/ holds the summary).  Valid only for the
-# kernel source whose SHA-256 is recorded; otherwise traffic is reported null.
-TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "batch": 262144, "calls_per_step": 32,
-           "kernel_sha256": "a4ff96fe0aa48cbb064efa363e7d35d1d0b4a334a260b7c6fbbcaf5f98cc9c7d",
-           "fetch_bytes": 50698990, "write_bytes": 5506192}
-# The same for the end-states launch of the readout path (fit_tracks_states).
-STATES_TRAFFIC = dict(TRAFFIC, fetch_bytes=55189391, write_bytes=269221888)
+# HBM bytes per launch (per call for the paper's model: its front-end pass and
+# two layer launches added up), from two rocprofv3 --pmc runs of this script
+# with --no-graph --copy-calibration (FETCH_SIZE, then WRITE_SIZE), each scaled
+# by the same counter's reading for a plain device copy of known size
+# (profiles/ holds the summaries).  Keyed by (path, workload); a record is used
+# only while the SHA-256 of the listed kernel sources, concatenated, is the one
+# recorded and the launch shape is the recorded one; otherwise traffic is null.
+ENCODER_SRCS = ("trackfit.hip", "common.h")
+TRAFFIC = {
+    ("encoder", "deploy_d128x4_bf16_8m"): {
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
+        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 50699182, "write_bytes": 5507904},
+    ("readout", "deploy_d128x4_bf16_8m"): {
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
+        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 55204686, "write_bytes": 269221888},
+    ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
+        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 234364122, "write_bytes": 21865104},
+    ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
+        "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
+        "sha256": "f3af1ce1507ec07fec86258f7c8da08eeef7ca427196bbda8d7ce612a441d710",
+        "fetch_bytes": 267332535 + 1075914708 + 2915707119, "write_bytes": 939913936 + 3227833472 + 402653184},
+}
+
+
+def sources_sha256(names):
+    import hashlib
+    h = hashlib.sha256()
+    for n in names:
+        with open(os.path.join(CSRC, n), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def traffic_bytes(path, w, batch, calls):
+    """Counter-derived HBM bytes per launch, when they were taken on these
+    kernel sources and this launch shape; else None."""
+    rec = TRAFFIC.get((path, w.name))
+    if rec is None or calls != rec["calls_per_step"] or batch != rec["batch"]:
+        return None
+    if sources_sha256(rec["srcs"]) != rec["sha256"]:
+        return None
+    return rec["fetch_bytes"] + rec["write_bytes"]
 
 
 def front_flops(d, n_hits, n_features=0):
@@ -135,31 +168,14 @@ def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
             "parity_max_col_err_on_sample": err}
 
 
-def traffic_bytes(w, batch, calls, rec=None):
-    """Counter-derived HBM bytes per launch, when they were taken on this kernel
-    source and this launch shape; else None."""
-    rec = TRAFFIC if rec is None else rec
-    if calls != rec["calls_per_step"] or batch != rec["batch"]:
-        return None
-    if w.name != rec["workload"] or kernel_source_sha256() != rec["kernel_sha256"]:
-        return None
-    return rec["fetch_bytes"] + rec["write_bytes"]
-
-
-def kernel_source_sha256():
-    import hashlib
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
-
-
 SEED_METRIC = "tracks/sec (fp64 three-hit seed + per-hit residual features) on 1 MI355X; HBM GB/s vs peak"
 SEED_SRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc", "seed.hip")
 # HBM bytes of one tf_seed_tracks call over the whole deployment workload, from
 # FETCH_SIZE / WRITE_SIZE runs of this script's seed path with --copy-calibration
 # (scaled as for the encoder); valid only for the recorded source.
 SEED_TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "n_tracks": 8388608,
-                "kernel_sha256": "0c35360525fc4d780d486b8f00cad12a6b0bc32d655328daf811ca9424b4fcab",
-                "fetch_bytes": 2675781353, "write_bytes": 1780067216}
+                "kernel_sha256": "95e15c248fe9e118aec25f0451b9ee525b1ebbdb58a9f7125625fab4e8e6629f",
+                "fetch_bytes": 2672606279, "write_bytes": 1778368704}
 
 
 def seed_algorithmic_bytes(n_hits, n_tracks):
@@ -403,7 +419,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
                    "n_features": w.n_features,
                    "max_hits": W.max_hits, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes(w, batch, len(starts), STATES_TRAFFIC),
+                     "traffic": traffic_bytes("readout", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "readout_flops_per_step": readout_algorithmic_flops(d, n_tracks),
@@ -563,7 +579,7 @@ def bench_paper(args, w, hits, offs, mode, batch):
                    "launches_per_call": 5, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model,
                    "hidden": H, "n_features": w.n_features, "mode": mode, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": None, "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
+                     "traffic": traffic_bytes("paper", w, batch, len(starts)), "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
                      "kernel_avg_ms": call_avg, "flops_per_launch": per_call},
         "context": {"paper_h100_nvl_tracks_per_s": PAPER_H100_TRACKS_PER_S,
                     "ratio_to_paper_h100": value / PAPER_H100_TRACKS_PER_S,
@@ -727,7 +743,7 @@ def main():
                    "max_hits": W.max_hits, "n_features": w.n_features,
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
-                     "frac": achieved_tflops / peak, "traffic": traffic_bytes(w, batch, len(starts)),
+                     "frac": achieved_tflops / peak, "traffic": traffic_bytes("encoder", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
