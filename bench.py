@@ -51,17 +51,17 @@ ENCODER_SRCS = ("trackfit.hip", "common.h")
 TRAFFIC = {
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 50699182, "write_bytes": 5507904},
+        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 52832260, "write_bytes": 5546288},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 55204686, "write_bytes": 269221888},
+        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 57544986, "write_bytes": 269221888},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "c3c5d64eb4f10f20b0ea7b0f0e98ad20de26cbf37bf6bd1d34b42d1a3a6184eb", "fetch_bytes": 234364122, "write_bytes": 21865104},
+        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 236667367, "write_bytes": 22137856},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "f3af1ce1507ec07fec86258f7c8da08eeef7ca427196bbda8d7ce612a441d710",
-        "fetch_bytes": 267332535 + 1075914708 + 2915707119, "write_bytes": 939913936 + 3227833472 + 402653184},
+        "sha256": "3e8e1c15470025fa97de1d760fec5e323caea43cda3b86c8407dc58164a19db0",
+        "fetch_bytes": 266949706 + 998528850 + 3002700821, "write_bytes": 939847712 + 3418877632 + 402653184},
 }
 
 

@@ -143,50 +143,55 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
 
     const long long gw = (long long)blockIdx.x * C::WAVES + wid;
     const long long nw = (long long)gridDim.x * C::WAVES;
-    const int g_begin = int((long long)n_tracks * gw / nw);
-    const int g_end = int((long long)n_tracks * (gw + 1) / nw);
+    const int g_begin = group_begin(offsets, n_tracks, gw, nw, lane);
+    const int g_end = group_begin(offsets, n_tracks, gw + 1, nw, lane);
     const int row0 = offsets[0];
     const float qnan = __builtin_nanf("");
     int errbits = 0;
 
+    // Tiles are packed from a window of the wave's tracks: the first track not
+    // yet fitted (t) and the WIN - 1 after it; bit i of `taken` marks track
+    // t + i as fitted into an earlier tile (or refused).  A track that cannot be
+    // fitted (rows outside the input, no hits, more than 32) is refused: NaN end
+    // states and its error bit.
+    constexpr int WIN = 32;
     int t = g_begin;
+    unsigned taken = 0;
     for (;;) {
-        // ---- tile: the longest run of whole tracks from t that fits; a track that
-        // cannot be fitted (rows outside the input, no hits, more than 32) is
-        // refused on its own
-        int k = 0, n = 0, off = 0, len = 0, incl = 0;
+        int k = 0, n = 0, off = 0, len = 0;
+        unsigned sel = 0;  // window tracks of the tile
         while (t < g_end) {
+            const int sh = taken == ~0u ? WIN : __builtin_ctz(~taken);
+            taken = sh == WIN ? 0u : taken >> sh;
+            t += sh;
+            if (t >= g_end) break;
             const int idx = t + lane;
-            off = (lane <= 32 && idx <= g_end) ? offsets[idx] : 0;
+            off = (lane <= WIN && idx <= g_end) ? offsets[idx] : 0;
             const int nxt = __shfl_down(off, 1);
             len = nxt - off;
-            const bool in_range = lane < 32 && idx < g_end;
+            const bool fresh = lane < WIN && idx < g_end && !((taken >> (lane & 31)) & 1u);
             const bool bad_rows = (long long)off < row0 || nxt < off || (long long)nxt - row0 > x_rows;
             const bool empty = !bad_rows && len == 0;
             const bool too_long = !bad_rows && len > kMgCap;
-            const unsigned long long badm = __ballot(in_range && (bad_rows || empty || too_long));
-            incl = in_range ? len : 0;
-#pragma unroll
-            for (int dd = 1; dd < 32; dd <<= 1) {
-                const int y = __shfl_up(incl, dd);
-                if (lane >= dd) incl += y;
-            }
-            const unsigned long long fitm = __ballot(in_range && incl <= kMgCap && lane < kMgMaxTr);
-            const int first_bad = badm ? __builtin_ctzll(badm) : 64;
-            const int first_nofit = __builtin_ctzll(~fitm);
-            const int kk = first_bad < first_nofit ? first_bad : first_nofit;
-            if (kk == 0) {
-                // track t is refused: NaN end states, and its error bit
-                const int b0 = __builtin_amdgcn_readfirstlane((int)bad_rows), e0 = __builtin_amdgcn_readfirstlane((int)empty);
-                errbits |= b0 ? TF_DEVERR_BAD_OFFSETS : e0 ? TF_DEVERR_EMPTY_TRACK : TF_DEVERR_TOO_LONG;
+            const unsigned bm = unsigned(__ballot(fresh && bad_rows));
+            const unsigned em = unsigned(__ballot(fresh && empty));
+            const unsigned lm = unsigned(__ballot(fresh && too_long));
+            if (bm | em | lm) {
+                errbits |= (bm ? TF_DEVERR_BAD_OFFSETS : 0) | (em ? TF_DEVERR_EMPTY_TRACK : 0) |
+                           (lm ? TF_DEVERR_TOO_LONG : 0);
                 if constexpr (LAST)
-                    for (int e = lane; e < 2 * H; e += 64) states[(size_t)t * 2 * H + e] = qnan;
-                t += 1;
-                continue;
+                    for (unsigned m = bm | em | lm; m; m &= m - 1u)
+                        for (int e = lane; e < 2 * H; e += 64)
+                            states[(size_t)(t + __builtin_ctz(m)) * 2 * H + e] = qnan;
+                taken |= bm | em | lm;
             }
-            k = kk;
-            n = __builtin_amdgcn_readlane(incl, kk - 1);
-            break;
+            const unsigned cand = unsigned(__ballot(fresh && !bad_rows && !empty && !too_long));
+            if (cand) {
+                sel = pack_tile<kMgCap, kMgMaxTr, true>(cand, len, lane, n);
+                k = __builtin_popcount(sel);
+                taken |= sel;
+                break;
+            }
         }
         const bool work = k > 0;
         wait_vmcnt<0>();
@@ -197,14 +202,25 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0, st0 = 0, st1 = 0;
         FT xa[KIN];
         if (work) {
-            if (lane < k) {
-                t_start[lane] = incl - len;
-                t_len[lane] = len;
-                t_off[lane] = off;
-                t_id[lane] = t + lane;
+            // the tile's tracks in window order, on consecutive tile rows
+            const bool mine = lane < WIN && ((sel >> (lane & 31)) & 1u);
+            const int v = mine ? len : 0;
+            int incl = v;  // inclusive prefix sum of the selected lengths over lanes
+#pragma unroll
+            for (int dd = 1; dd < WIN; dd <<= 1) {
+                const int y = __shfl_up(incl, dd);
+                if (lane >= dd) incl += y;
+            }
+            const int rs = incl - v;  // first tile row of this lane's track
+            if (mine) {
+                const int j = __builtin_amdgcn_mbcnt_lo(sel, 0);  // selected tracks before this one
+                t_start[j] = rs;
+                t_len[j] = len;
+                t_off[j] = off;
+                t_id[j] = t + lane;
             }
             unsigned long long smask = 0;  // tile rows that start a track
-            for (int i = 0; i < k; ++i) smask |= 1ull << __builtin_amdgcn_readlane(incl - len, i);
+            for (unsigned m = sel; m; m &= m - 1u) smask |= 1ull << __builtin_amdgcn_readlane(rs, __builtin_ctz(m));
             const unsigned long long valid = (1ull << n) - 1ull;
             const unsigned long long vstart = smask | (1ull << n);
             const unsigned long long emask = ((smask >> 1) | (1ull << (n - 1))) & valid;
@@ -224,7 +240,6 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                 rowmap[lane] = r;
             }
             wave_lds_sync();
-            t += k;
             // A operand: lane (s, i) holds input channels k-step K + s KL .. + KL - 1 of
             // tile row slot_to_hit(i), whose products land in accumulator row i
             const int xr = rowmap[slot_to_hit<SP>(cc)];

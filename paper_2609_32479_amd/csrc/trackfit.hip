@@ -255,20 +255,20 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     };
     auto slot = [&]() -> const char * { return slot_ptr(q); };
 
-    // Contiguous group of tracks for this wave, balanced by track count.
+    // Contiguous group of tracks for this wave, balanced by hit rows.
     const long long gw = (long long)blockIdx.x * C::WAVES + wid;
     const long long nw = (long long)gridDim.x * C::WAVES;
-    const int g_begin = int((long long)n_tracks * gw / nw);
-    const int g_end = int((long long)n_tracks * (gw + 1) / nw);
+    const int g_begin = group_begin(offsets, n_tracks, gw, nw, lane);
+    const int g_end = group_begin(offsets, n_tracks, gw + 1, nw, lane);
 
     int errbits = 0;
     const float qnan = __builtin_nanf("");
 
-    // Tiles are packed first-fit from a window of the wave's tracks: the first
-    // track not yet fitted (t) and the WIN - 1 after it, in track order; bit i
-    // of `taken` marks track t + i as fitted into an earlier tile (or refused).
-    // The first track of the window always fits, so every tile makes progress,
-    // and a track's result does not depend on the tile it lands in.
+    // Tiles are packed from a window of the wave's tracks: the first track not
+    // yet fitted (t) and the WIN - 1 after it, in track order; bit i of `taken`
+    // marks track t + i as fitted into an earlier tile (or refused).  The first
+    // track of the window always goes in, so every tile makes progress, and a
+    // track's result does not depend on the tile it lands in.
     constexpr int WIN = 32;
     int t = g_begin;
     unsigned taken = 0;
@@ -305,21 +305,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 }
                 taken |= unsigned(bad_m | empty_m | long_m);
             }
-            // first-fit in track order
-            unsigned cand = unsigned(__ballot(fresh && !bad && !empty && !too_long));
-            int rows = 0;
-            while (cand) {
-                const int i = __builtin_ctz(cand);
-                cand &= cand - 1u;
-                const int li = __builtin_amdgcn_readlane(len, i);
-                if (rows + li <= CAP) {
-                    sel |= 1u << i;
-                    rows += li;
-                    if (++k == MAXTR || rows == CAP) break;
-                }
-            }
-            if (k > 0) {
-                n = rows;
+            // first-fit in window order (the pair search costs this kernel more per
+            // tile than it saves)
+            const unsigned cand = unsigned(__ballot(fresh && !bad && !empty && !too_long));
+            if (cand) {
+                sel = pack_tile<CAP, MAXTR, false>(cand, len, lane, n);
+                k = __builtin_popcount(sel);
                 taken |= sel;
                 break;
             }
