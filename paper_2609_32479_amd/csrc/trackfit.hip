@@ -423,6 +423,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // projection), formed in registers: sin or cos of pi 2^s u_f
             const float *us = stage;
             const int kf = 32 * P.n_feat / K;  // k-steps of the projection
+            FT cnext[HT];  // 16-bit: the cosines that the k-step after an even one takes
+#pragma unroll
+            for (int nt = 0; nt < HT; ++nt) cnext[nt] = FT{};
             for (int js = 0; js < P.n_fstages; ++js) {
                 if (work) {
                     const FT *wfr = reinterpret_cast<const FT *>(slot());
@@ -437,16 +440,31 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             const int sl = 32 * nt + cc;
                             float v[8];
                             if constexpr (C::HALF) {
-                                // feature ks / 2, sine (even ks) or cosine, scales 8 hh + e: in
-                                // revolutions, sin(pi 2^s u) = sin(2 pi frac(2^(s - 1) u)); the
-                                // products by powers of two and the fraction are exact
-                                const float u = us[sl * kUStride + (ks >> 1)];
-                                const float w0 = u * (hh ? 128.0f : 0.5f);
-#pragma unroll
-                                for (int e = 0; e < 8; ++e) {
-                                    const float x = __builtin_amdgcn_fractf(w0 * (float)(1 << e));
-                                    v[e] = (ks & 1) ? __builtin_amdgcn_cosf(x) : __builtin_amdgcn_sinf(x);
+                                // feature ks / 2, sines (even ks) or cosines (odd ks) of
+                                // pi 2^s u at scales s = 8 hh + e.  The even k-step forms both:
+                                // the lowest scale from the hardware functions, in revolutions
+                                // (sin(pi 2^s u) = sin(2 pi frac(2^(s - 1) u)), the product by a
+                                // power of two and the fraction exact), each next scale by the
+                                // double-angle formulas, i.e. squaring the unit complex number
+                                // c + i s.  An error doubles with each step, so the highest scale
+                                // carries 2^7 times the hardware functions' error, far below the
+                                // 16-bit operand's rounding.
+                                if (ks & 1) {
+                                    bv[nt] = cnext[nt];
+                                    continue;
                                 }
+                                const float u = us[sl * kUStride + (ks >> 1)];
+                                const float x = __builtin_amdgcn_fractf(u * (hh ? 128.0f : 0.5f));
+                                float cv[8];
+                                v[0] = __builtin_amdgcn_sinf(x);
+                                cv[0] = __builtin_amdgcn_cosf(x);
+#pragma unroll
+                                for (int e = 1; e < 8; ++e) {
+                                    const float sp = v[e - 1], cp = cv[e - 1];
+                                    v[e] = (sp + sp) * cp;
+                                    cv[e] = (cp - sp) * (cp + sp);
+                                }
+                                cnext[nt] = F::pack(cv);
                             } else {
                                 // one feature per lane and k-step; the library's sinpi/cospi
                                 // reduce the exact argument 2^s u exactly
