@@ -214,3 +214,80 @@ def test_graph_replay_matches_direct(tf):
         g.replay()
         torch.cuda.synchronize()
         assert np.array_equal(out.cpu().numpy(), ref), f"replay {rep}"
+
+
+def _scrambled_offsets(n_hits, n, seed):
+    """Sorted offsets over the hit rows with about 10 % of the entries replaced by
+    arbitrary values in [-50, n_hits + 50]: tracks around them have negative,
+    reversed, out-of-range, empty or overlong row ranges."""
+    rng = np.random.default_rng(seed)
+    o = np.sort(rng.integers(0, n_hits, n + 1))
+    o[0], o[-1] = 0, n_hits
+    bad = rng.random(n + 1) < 0.1
+    bad[0] = bad[-1] = False
+    o[bad] = rng.integers(-50, n_hits + 50, int(bad.sum()))
+    return o.astype(np.int32)
+
+
+def _valid_tracks(o, n_hits, cap):
+    a, b = o[:-1].astype(np.int64), o[1:].astype(np.int64)
+    return (a >= 0) & (b >= a) & (b <= n_hits) & (b - a >= 1) & (b - a <= cap)
+
+
+@pytest.mark.parametrize("seed", [0, 1])
+def test_scrambled_offsets_every_track_written_once(tf, seed):
+    """Each wave's share of the batch is a group of about equal hit rows, found by
+    a search over the offsets; with offsets that are not monotone every track
+    must still get exactly one result: the oracle's where its rows form a valid
+    track, NaN otherwise."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w, max_hits=32)
+    hits, _ = ts.make_tracks(w, n_tracks=4000)
+    n = 6000
+    o = _scrambled_offsets(hits.shape[0], n, seed)
+    ok = _valid_tracks(o, hits.shape[0], 32)
+    assert 0 < ok.sum() < n
+    h = torch.from_numpy(hits).cuda()
+    out = torch.full((n, 5), 12345.0, device="cuda")
+    tf.fit_tracks(h, torch.from_numpy(o).cuda(), W, out=out, n_tracks=n)
+    torch.cuda.synchronize()
+    g = out.cpu().numpy()
+    assert not np.any(g == 12345.0), "a track was not written"
+    assert np.all(np.isnan(g[~ok])) and np.all(np.isfinite(g[ok]))
+    idx = np.flatnonzero(ok)
+    L = (o[idx + 1] - o[idx]).astype(np.int64)
+    packed = np.concatenate([hits[o[i]:o[i + 1]] for i in idx])
+    r = oracle.fit_tracks(packed, np.concatenate([[0], np.cumsum(L)]).astype(np.int32), blob, w.n_layers,
+                          w.d_model, n_threads=THREADS)
+    assert_parity(g[ok], r, TOL[w.dtype], f"valid tracks among scrambled offsets (seed {seed})")
+    assert tf.device_error(W) & tf.DEVERR_BAD_OFFSETS
+
+
+def test_scrambled_offsets_mingru_every_track_written_once(tf):
+    """The same for the minGRU backbone's end states (its layers split the batch
+    the same way)."""
+    w = ts.workload("mingru2_h192_fourier15_deploy_bf16_8m")
+    blob = ts.make_mingru_weights(w)
+    M = tf.MinGRU(blob, w.n_layers, w.d_model, w.hidden, tf.MODE_FOR_WEIGHTS[w.dtype], w.n_features)
+    hits, offs = ts.make_tracks(w, n_tracks=3000)
+    _, sf, _ = oracle.seed_tracks(hits, offs, w.b_field)
+    feats = ts.hit_features(w, hits, offs, np.nan_to_num(sf, nan=0.0))
+    n = 4000
+    o = _scrambled_offsets(feats.shape[0], n, 7)
+    ok = _valid_tracks(o, feats.shape[0], 32)
+    f = torch.from_numpy(np.ascontiguousarray(feats, dtype=np.float32)).cuda()
+    ws = torch.empty(M.workspace_bytes(feats.shape[0]), dtype=torch.uint8, device="cuda")
+    st = torch.full((n, 2 * w.hidden), 12345.0, device="cuda")
+    M.states(f, torch.from_numpy(o).cuda(), out=st, workspace=ws, n_tracks=n)
+    torch.cuda.synchronize()
+    g = st.cpu().numpy()
+    assert not np.any(g == 12345.0), "a track was not written"
+    assert np.all(np.isnan(g[~ok])) and np.all(np.isfinite(g[ok]))
+    idx = np.flatnonzero(ok)
+    L = (o[idx + 1] - o[idx]).astype(np.int64)
+    packed = np.concatenate([feats[o[i]:o[i + 1]] for i in idx])
+    r = oracle.mingru_states(packed, np.concatenate([[0], np.cumsum(L)]).astype(np.int32), blob, w.n_layers,
+                             w.d_model, w.hidden, n_features=w.n_features, n_threads=THREADS)
+    rms = np.sqrt(np.mean(r ** 2, axis=1, keepdims=True))
+    assert float(np.max(np.abs(g[ok] - r) / rms)) <= TOL[w.dtype]
+    assert M.device_error() & tf.DEVERR_BAD_OFFSETS
