@@ -51,17 +51,17 @@ ENCODER_SRCS = ("trackfit.hip", "common.h")
 TRAFFIC = {
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 52832260, "write_bytes": 5546288},
+        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 52852803, "write_bytes": 5515744},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 57544986, "write_bytes": 269221888},
+        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 57533211, "write_bytes": 269221888},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "0b660c410eca41548636d52e14fdc6145436460f0099e786bed5bff6e8852ea6", "fetch_bytes": 236667367, "write_bytes": 22137856},
+        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 236654760, "write_bytes": 21530640},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "3e8e1c15470025fa97de1d760fec5e323caea43cda3b86c8407dc58164a19db0",
-        "fetch_bytes": 266949706 + 998528850 + 3002700821, "write_bytes": 939847712 + 3418877632 + 402653184},
+        "sha256": "c2aae9079bfd0628df1b1db384e0a8986ec249b88848fc3efed40e1d282e7c87",
+        "fetch_bytes": 264536065 + 997897265 + 3001502736, "write_bytes": 939829296 + 3413465056 + 402653184},
 }
 
 
