@@ -51,7 +51,9 @@ ENCODER_SRCS = ("trackfit.hip", "common.h")
 TRAFFIC = {
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 52852803, "write_bytes": 5515744},
+        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 52852803, "write_bytes": 5515744,
+        # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles), median over launches
+        "mfma_util": 0.329},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
         "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 57533211, "write_bytes": 269221888},
@@ -74,15 +76,27 @@ def sources_sha256(names):
     return h.hexdigest()
 
 
-def traffic_bytes(path, w, batch, calls):
-    """Counter-derived HBM bytes per launch, when they were taken on these
+def counter_record(path, w, batch, calls):
+    """The counter record of this path and workload, when it was taken on these
     kernel sources and this launch shape; else None."""
     rec = TRAFFIC.get((path, w.name))
     if rec is None or calls != rec["calls_per_step"] or batch != rec["batch"]:
         return None
     if sources_sha256(rec["srcs"]) != rec["sha256"]:
         return None
-    return rec["fetch_bytes"] + rec["write_bytes"]
+    return rec
+
+
+def traffic_bytes(path, w, batch, calls):
+    """Counter-derived HBM bytes per launch, or None."""
+    rec = counter_record(path, w, batch, calls)
+    return None if rec is None else rec["fetch_bytes"] + rec["write_bytes"]
+
+
+def mfma_util_counter(path, w, batch, calls):
+    """rocprofv3's MfmaUtil of the dominant kernel, or None."""
+    rec = counter_record(path, w, batch, calls)
+    return None if rec is None else rec.get("mfma_util")
 
 
 def front_flops(d, n_hits, n_features=0):
@@ -744,6 +758,7 @@ def main():
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved_tflops / peak, "traffic": traffic_bytes("encoder", w, batch, len(starts)),
+                     "mfma_util_counter": mfma_util_counter("encoder", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
