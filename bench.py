@@ -52,8 +52,9 @@ TRAFFIC = {
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
         "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 52852803, "write_bytes": 5515744,
-        # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles), median over launches
-        "mfma_util": 0.329},
+        # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
+        # VALUBusy (cycles issuing vector instructions), medians over launches
+        "mfma_util": 0.329, "valu_busy": 0.546},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
         "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 57533211, "write_bytes": 269221888},
@@ -93,10 +94,11 @@ def traffic_bytes(path, w, batch, calls):
     return None if rec is None else rec["fetch_bytes"] + rec["write_bytes"]
 
 
-def mfma_util_counter(path, w, batch, calls):
-    """rocprofv3's MfmaUtil of the dominant kernel, or None."""
+def busy_counter(path, w, batch, calls, key):
+    """rocprofv3's MfmaUtil ("mfma_util") or VALUBusy ("valu_busy") of the
+    dominant kernel, or None."""
     rec = counter_record(path, w, batch, calls)
-    return None if rec is None else rec.get("mfma_util")
+    return None if rec is None else rec.get(key)
 
 
 def front_flops(d, n_hits, n_features=0):
@@ -176,10 +178,19 @@ def cpu_baseline(w, blob, hits, offs, seconds, threads, gpu_out):
     g = gpu_out[sel].astype(np.float64)
     rms = np.sqrt(np.mean(ref ** 2, axis=0))
     err = float(np.max(np.abs(g - ref) / np.maximum(np.abs(ref), rms)))
+    # the same oracle on one host core, on a smaller sample (about a fifth of the time)
+    n1 = int(min(n, max(64, n * seconds / 5.0 / max(dt * oracle.threads(threads), 1e-3))))
+    sel1 = np.sort(rng.choice(n_all, size=n1, replace=False))
+    t0 = time.perf_counter()
+    h1, o1 = oracle_inputs(w, hits, offs, sel1)
+    oracle.fit_tracks(h1, o1, blob, w.n_layers, w.d_model, n_threads=1, n_features=w.n_features)
+    dt1 = time.perf_counter() - t0
     return {"value": n / dt, "unit": "tracks/s", "cores": oracle.threads(threads), "kind": "oracle",
             "sample": f"{n} tracks drawn without replacement (seed 7) from the {n_all}-track workload, "
                       f"fp64 C oracle, {dt:.1f} s wall",
-            "parity_max_col_err_on_sample": err}
+            "parity_max_col_err_on_sample": err,
+            "one_core": {"value": n1 / dt1, "unit": "tracks/s", "cores": 1,
+                         "sample": f"{n1} further tracks drawn the same way, {dt1:.1f} s wall"}}
 
 
 SEED_METRIC = "tracks/sec (fp64 three-hit seed + per-hit residual features) on 1 MI355X; HBM GB/s vs peak"
@@ -758,7 +769,8 @@ def main():
                    "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": achieved_tflops / peak, "traffic": traffic_bytes("encoder", w, batch, len(starts)),
-                     "mfma_util_counter": mfma_util_counter("encoder", w, batch, len(starts)),
+                     "mfma_util_counter": busy_counter("encoder", w, batch, len(starts), "mfma_util"),
+                     "valu_busy_counter": busy_counter("encoder", w, batch, len(starts), "valu_busy"),
                      "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
