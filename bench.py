@@ -51,20 +51,20 @@ ENCODER_SRCS = ("trackfit.hip", "common.h")
 TRAFFIC = {
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 52852803, "write_bytes": 5515744,
+        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 52855939, "write_bytes": 5546560,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.329, "valu_busy": 0.546},
+        "mfma_util": 0.326, "valu_busy": 0.545},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 57533211, "write_bytes": 269221888},
+        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 57532379, "write_bytes": 269221888},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "cea52081b282201ea9cab25637de65841682323f6c6b81b19fdee83a4889a555", "fetch_bytes": 236654760, "write_bytes": 21530640},
+        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 236664040, "write_bytes": 21588592},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "c2aae9079bfd0628df1b1db384e0a8986ec249b88848fc3efed40e1d282e7c87",
-        "fetch_bytes": 264536065 + 997897265 + 3001502736, "write_bytes": 939829296 + 3413465056 + 402653184},
+        "sha256": "8ce150acd7e4ca76414fea62ac26e03373d56c05736fdb3d88291b72f1ceb2fb",
+        "fetch_bytes": 264824499 + 996095115 + 3002571931, "write_bytes": 939887920 + 3411865312 + 402653184},
 }
 
 

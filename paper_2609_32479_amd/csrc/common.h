@@ -167,52 +167,53 @@ __device__ __forceinline__ unsigned pack_tile(unsigned cand, int len, int lane, 
     const unsigned rest = cand & ~sel;
     const int room = CAP - n;
     if constexpr (PAIR) {
-    // bit l - 1 of m1: a length l among the other candidates that fit beside
-    // the first; of m2: one that at least two of them have
-    u64 m1 = 0, m2 = 0;
-    for (unsigned c = rest; c; c &= c - 1u) {
-        const int li = __builtin_amdgcn_readlane(len, __builtin_ctz(c));
-        if (li <= room) {
-            const u64 b = 1ull << (li - 1);
-            m2 |= m1 & b;
-            m1 |= b;
+        // bit l - 1 of m1: a length l among the other candidates that fit beside
+        // the first; of m2: one that at least two of them have
+        u64 m1 = 0, m2 = 0;
+        for (unsigned c = rest; c; c &= c - 1u) {
+            const int li = __builtin_amdgcn_readlane(len, __builtin_ctz(c));
+            if (li <= room) {
+                const u64 b = 1ull << (li - 1);
+                m2 |= m1 & b;
+                m1 |= b;
+            }
         }
-    }
-    auto upto = [](int r) -> u64 { return r <= 0 ? 0ull : r >= 64 ? ~0ull : (1ull << r) - 1ull; };
-    const u64 ms = m1 & upto(room);
-    const int single = ms ? 64 - __builtin_clzll(ms) : 0;
-    // per candidate lane: the longest other length that fits beside it
-    const bool av = lane < 32 && ((rest >> (lane & 31)) & 1u) && len <= room;
-    int pair = 0, partner = 0;
-    if (av) {
-        const int left = room - len;
-        u64 m = m1 & upto(left);
-        if (len <= left && !((m2 >> (len - 1)) & 1ull)) m &= ~(1ull << (len - 1));  // not itself
-        if (m) {
-            partner = 64 - __builtin_clzll(m);
-            pair = len + partner;
+        auto upto = [](int r) -> u64 { return r <= 0 ? 0ull : r >= 64 ? ~0ull : (1ull << r) - 1ull; };
+        const u64 ms = m1 & upto(room);
+        const int single = ms ? 64 - __builtin_clzll(ms) : 0;
+        // per candidate lane: the longest other length that fits beside it
+        const bool av = lane < 32 && ((rest >> (lane & 31)) & 1u) && len <= room;
+        int pair = 0, partner = 0;
+        if (av) {
+            const int left = room - len;
+            u64 m = m1 & upto(left);
+            if (len <= left && !((m2 >> (len - 1)) & 1ull)) m &= ~(1ull << (len - 1));  // not itself
+            if (m) {
+                partner = 64 - __builtin_clzll(m);
+                pair = len + partner;
+            }
         }
-    }
-    // the best pair sum above the best single, counted down from the room left
-    int best = 0;
-    unsigned long long who = 0;
-    for (int sum = room; sum > single; --sum) {
-        who = __ballot(av && pair == sum);
-        if (who) {
-            best = sum;
-            break;
+        // the best pair sum above the best single, counted down from the room left
+        int best = 0;
+        unsigned long long who = 0;
+        for (int sum = room; sum > single; --sum) {
+            who = __ballot(av && pair == sum);
+            if (who) {
+                best = sum;
+                break;
+            }
         }
-    }
-    if (best) {
-        const int i = __builtin_ctzll(who);
-        const int pl = __builtin_amdgcn_readlane(partner, i);
-        const int j = __builtin_ctzll(__ballot(lane < 32 && lane != i && ((rest >> (lane & 31)) & 1u) && len == pl));
-        sel |= (1u << i) | (1u << j);
-        n += best;
-    } else if (single > 0) {
-        sel |= 1u << __builtin_ctzll(__ballot(av && len == single));
-        n += single;
-    }
+        if (best) {
+            const int i = __builtin_ctzll(who);
+            const int pl = __builtin_amdgcn_readlane(partner, i);
+            const bool mate = lane < 32 && lane != i && ((rest >> (lane & 31)) & 1u) && len == pl;
+            const int j = __builtin_ctzll(__ballot(mate));
+            sel |= (1u << i) | (1u << j);
+            n += best;
+        } else if (single > 0) {
+            sel |= 1u << __builtin_ctzll(__ballot(av && len == single));
+            n += single;
+        }
     }
     // first-fit over the rest
     int k = __builtin_popcount(sel);
