@@ -657,8 +657,8 @@ def main():
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py runs on one GPU only: the forward pass has no cross-track exchange, and "
-              "multi-GPU runs are not part of this build (shard the batch by offsets ranges "
-              "across processes instead).", file=sys.stderr)
+              "this library has no multi-GPU path (shard the batch by offsets ranges across "
+              "processes instead).", file=sys.stderr)
         sys.exit(2)
 
     import torch
