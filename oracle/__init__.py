@@ -54,15 +54,14 @@ def lib():
         L.orc_fourier_features.restype = None
         L.orc_fourier_features.argtypes = [fp, ctypes.c_int, fp, fp, dp]
         L.orc_readout_blob_size.restype = ctypes.c_size_t
-        L.orc_readout_blob_size.argtypes = [ctypes.c_int]
-        L.orc_median_odd.restype = ctypes.c_double
-        L.orc_median_odd.argtypes = [dp, ctypes.c_int]
+        L.orc_readout_blob_size.argtypes = [ctypes.c_int, ctypes.c_int]
         L.orc_decode.restype = None
         L.orc_decode.argtypes = [dp, dp, dp]
         L.orc_readout_track.restype = None
-        L.orc_readout_track.argtypes = [dp, ctypes.c_int, fp, dp, dp, dp]
+        L.orc_readout_track.argtypes = [dp, ctypes.c_int, ctypes.c_int, fp, dp, dp, dp]
         L.orc_readout_tracks.restype = ctypes.c_long
-        L.orc_readout_tracks.argtypes = [dp, ctypes.c_int32, ctypes.c_int, fp, ctypes.c_size_t, dp, dp, dp]
+        L.orc_readout_tracks.argtypes = [dp, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp, ctypes.c_size_t, dp,
+                                         dp, dp]
         L.orc_fit_tracks.restype = ctypes.c_long
         L.orc_fit_tracks.argtypes = [fp, ctypes.c_int, ip, ctypes.c_int32, ctypes.c_int, ctypes.c_int, fp,
                                      ctypes.c_size_t, dp, ctypes.c_int]
@@ -260,25 +259,22 @@ def track_states(hits, offsets, blob, n_layers, d, n_threads=0, n_features=0):
     return st
 
 
-def readout_blob_size(d):
-    return int(lib().orc_readout_blob_size(int(d)))
+def readout_blob_size(d, hidden):
+    return int(lib().orc_readout_blob_size(int(d), int(hidden)))
 
 
-def median_odd(v):
-    v, pv = _d(v)
-    return float(lib().orc_median_odd(pv, v.size))
-
-
-def decode(seed, med):
+def decode(seed, est):
+    """Decode the five point estimates against a seed."""
     s, ps = _d(seed)
-    m, pm = _d(med)
+    m, pm = _d(est)
     out = np.empty(5)
     lib().orc_decode(ps, pm, out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)))
     return out
 
 
-def readout_tracks(states, seeds, head_blob, d):
-    """states [N, 2d], seeds [N, 5] -> (quantiles [N, 35], decoded [N, 5])."""
+def readout_tracks(states, seeds, head_blob, d, hidden):
+    """states [N, 2d], seeds [N, 5], a head of hidden width `hidden` ->
+    (quantiles [N, 35], decoded [N, 5])."""
     st, pst = _d(np.asarray(states).reshape(-1, 2 * d))
     sd, psd = _d(np.asarray(seeds).reshape(-1, 5))
     hb, phb = _f(head_blob)
@@ -287,7 +283,8 @@ def readout_tracks(states, seeds, head_blob, d):
     q = np.empty((n, 35))
     out = np.empty((n, 5))
     dp = ctypes.POINTER(ctypes.c_double)
-    rc = lib().orc_readout_tracks(pst, n, d, phb, hb.size, psd, q.ctypes.data_as(dp), out.ctypes.data_as(dp))
+    rc = lib().orc_readout_tracks(pst, n, d, int(hidden), phb, hb.size, psd, q.ctypes.data_as(dp),
+                                  out.ctypes.data_as(dp))
     if rc < 0:
         raise ValueError("oracle rejected its arguments")
     return q, out

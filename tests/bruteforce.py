@@ -67,22 +67,24 @@ def track_forward(hits, blob, n_layers, d, eps=1e-6, states_out=None):
     return h @ P["head.W2"].T + P["head.b2"], pooled, r
 
 
-def readout(states, seed, head_blob, d, eps=1e-6):
+def readout(states, seed, head_blob, d, hidden, eps=1e-6):
     """The paper's readout and decode, restated with numpy: RMSNorm over the 2d
-    end states, SiLU hidden layer, 35 quantiles, per-parameter median of seven,
-    seed-anchored decode (phi wrapped to [-pi, pi), scale-free q/p with
-    epsilon 0.02 / GeV)."""
-    sizes = [2 * d, d * 2 * d, d, 35 * d, 35]
+    end states, SiLU hidden layer of `hidden` units, 35 quantiles, each
+    parameter's median quantile (the middle of its seven outputs) as its point
+    estimate, seed-anchored decode (phi wrapped to [-pi, pi), scale-free q/p
+    with epsilon 0.02 / GeV)."""
+    h_ = hidden
+    sizes = [2 * d, h_ * 2 * d, h_, 35 * h_, 35]
     parts = np.split(np.asarray(head_blob, dtype=np.float64), np.cumsum(sizes)[:-1])
-    g, W1, b1, W2, b2 = parts[0], parts[1].reshape(d, 2 * d), parts[2], parts[3].reshape(35, d), parts[4]
+    g, W1, b1, W2, b2 = parts[0], parts[1].reshape(h_, 2 * d), parts[2], parts[3].reshape(35, h_), parts[4]
     z = np.asarray(states, dtype=np.float64)
     y = g * z / np.sqrt(np.mean(z * z) + eps)
     h = W1 @ y + b1
     h = h * expit(h)
     q = W2 @ h + b2
-    med = np.median(q.reshape(5, 7), axis=1)
+    est = q.reshape(5, 7)[:, 3]
     s = np.asarray(seed, dtype=np.float64)
-    out = s + med
+    out = s + est
     out[2] = (out[2] + np.pi) % (2 * np.pi) - np.pi
-    out[4] = s[4] + med[4] * (abs(s[4]) + 0.02)
+    out[4] = s[4] + est[4] * (abs(s[4]) + 0.02)
     return q, out

@@ -32,7 +32,7 @@ import numpy as np
 __all__ = [
     "Workload", "WORKLOADS", "workload", "make_tracks", "make_track_chunk",
     "make_weights", "blob_layout", "blob_size", "round_to_bf16", "TRACK_CHUNK",
-    "KAPPA_GEV_PER_T_M", "readout_layout", "make_readout_weights",
+    "KAPPA_GEV_PER_T_M", "readout_layout", "readout_dims", "make_readout_weights",
     "FOURIER_WORKLOADS", "N_MEASURED", "measured_features", "feature_bounds", "fourier_layout",
     "make_fourier_weights", "hit_features", "MINGRU_WORKLOADS", "mingru_layout", "make_mingru_weights",
 ]
@@ -66,6 +66,7 @@ class Workload:
     n_features: int = 0   # > 0: per-hit features for the Fourier front end (12 measured + 3 seed)
     arch: str = "residual"  # "residual": the layers of blob_layout; "mingru": the paper's backbone
     hidden: int = 0       # minGRU hidden width H (the states are 2H wide)
+    head_hidden: int = 128  # hidden width of the paper's readout head (Sec. Encoder: 128)
 
     @property
     def data_seed(self) -> int:
@@ -79,7 +80,7 @@ class Workload:
 WORKLOADS = {
     w.name: w for w in [
         Workload("tiny_d32_fp32", 1, n_layers=1, d_model=32, dtype="fp32", n_tracks=256,
-                 len_min=10, len_max=10, n_det_layers=10),
+                 len_min=10, len_max=10, n_det_layers=10, head_hidden=96),
         Workload("d128x4_fp32_65k", 2, n_layers=4, d_model=128, dtype="fp32", n_tracks=65536,
                  len_min=8, len_max=20, n_det_layers=20),
         Workload("d256x6_bf16_1m", 3, n_layers=6, d_model=256, dtype="bf16", n_tracks=1048576,
@@ -111,7 +112,7 @@ FOURIER_WORKLOADS = {
 MINGRU_WORKLOADS = {
     w.name: w for w in [
         dataclasses.replace(WORKLOADS["tiny_d32_fp32"], name="mingru2_h64_tiny_d32_fp32", n_layers=2,
-                            arch="mingru", hidden=64),
+                            arch="mingru", hidden=64, head_hidden=32),
         dataclasses.replace(WORKLOADS["d128x4_fp32_65k"], name="mingru2_h192_fourier15_d128_fp32_65k",
                             n_layers=2, arch="mingru", hidden=192, n_features=15),
         dataclasses.replace(WORKLOADS["deploy_d128x4_bf16_8m"], name="mingru2_h192_fourier15_deploy_bf16_8m",
@@ -341,22 +342,36 @@ def split_blob(blob: np.ndarray, n_layers: int, d: int) -> dict:
     return out
 
 
-def readout_layout(d: int):
+def readout_layout(d: int, hidden: int):
     """Blob of the paper's readout head (Sec. Encoder, last paragraph): RMSNorm
-    gain over the 2d end states, a d-wide hidden layer, 35 quantile outputs
-    (seven per parameter, parameter p owning outputs 7p..7p+6)."""
-    return [("ro.norm.g", (2 * d,), 2 * d, "g"), ("ro.W1", (d, 2 * d), 2 * d, "w"), ("ro.b1", (d,), 2 * d, "b"),
-            ("ro.W2", (35, d), d, "w"), ("ro.b2", (35,), d, "b")]
+    gain over the 2d end states, a hidden layer of `hidden` units, 35 quantile
+    outputs (seven per parameter, parameter p owning outputs 7p..7p+6)."""
+    h = hidden
+    return [("ro.norm.g", (2 * d,), 2 * d, "g"), ("ro.W1", (h, 2 * d), 2 * d, "w"), ("ro.b1", (h,), 2 * d, "b"),
+            ("ro.W2", (35, h), h, "w"), ("ro.b2", (35,), h, "b")]
 
 
-def make_readout_weights(w, seed: int | None = None) -> np.ndarray:
-    """float32 blob of the readout head for a workload's width, drawn like the
-    encoder's (N(0, 1/fan_in), U(+-fan_in^-1/2), gains U(0.5, 1.5)); rounded
-    to bf16 values for a bf16 workload, as its encoder weights are."""
+def readout_dims(w) -> tuple[int, int]:
+    """(d, hidden) of a workload's readout head: the end states are 2d wide
+    (d = the minGRU hidden width H for the paper's backbone, d_model for the
+    residual encoder) and the head has w.head_hidden hidden units."""
     w = workload(w)
+    return (w.hidden if w.arch == "mingru" else w.d_model), w.head_hidden
+
+
+def make_readout_weights(w, seed: int | None = None, d: int | None = None,
+                         hidden: int | None = None) -> np.ndarray:
+    """float32 blob of a workload's readout head (dimensions from readout_dims
+    unless given), drawn like the encoder's (N(0, 1/fan_in),
+    U(+-fan_in^-1/2), gains U(0.5, 1.5)); rounded to bf16 values for a bf16
+    workload, as its encoder weights are."""
+    w = workload(w)
+    d0, h0 = readout_dims(w)
+    d = d0 if d is None else d
+    hidden = h0 if hidden is None else hidden
     rng = np.random.default_rng(w.weight_seed + 100 if seed is None else seed)
     parts = []
-    for _, shape, fan_in, kind in readout_layout(w.d_model):
+    for _, shape, fan_in, kind in readout_layout(d, hidden):
         n = int(np.prod(shape))
         if kind == "w":
             parts.append(rng.normal(0.0, fan_in ** -0.5, n))
