@@ -1,7 +1,8 @@
 """Pins of the fp64 oracle of the analytic three-hit seed and of its per-hit
 residual features (Sec. Method, "Analytic seed"), independent of the oracle's
 own formulas: truth of noise-free helices, a hand-built circle, a brute-force
-circle fit, and symmetries.
+circle fit, symmetries, and the residual features of hits moved off the helix
+by known amounts along the frame's directions.
 """
 import math
 
@@ -53,6 +54,83 @@ def test_features_vanish_on_the_helix_and_give_its_path_length():
             f = oracle.seed_features_hit(s, w.b_field, [x[i, j], y[i, j], z[i, j]])
             assert abs(f[0]) < 1e-8 and abs(f[1]) < 1e-8
             assert abs(f[2] - arc[i, j] / math.sin(truth[i, 3])) < 1e-7
+
+
+def _circle_centre(x, y):
+    """Centre of the circle through three transverse points, from the linear
+    system x^2 + y^2 + a x + b y + c = 0 (a brute-force fit, not the oracle's
+    conformal map)."""
+    A = np.stack([x, y, np.ones(3)], 1)
+    a, b, _ = np.linalg.solve(A, -(x ** 2 + y ** 2))
+    return -a / 2, -b / 2
+
+
+@pytest.mark.parametrize("delta", [0.05, -0.7, 3.0])
+def test_features_of_a_hit_moved_off_the_helix_radially(delta):
+    """A noise-free hit moved by delta along the outward normal of the seed
+    circle (away from its centre, in the transverse plane) keeps its turning
+    angle, so its helix point and path length are unchanged and its residual
+    is delta times that normal.  U = z x T / |z x T| is the transverse tangent
+    turned by +90 degrees: it points to the centre for counter-clockwise motion
+    (negative charge in a field along +z) and away from it for clockwise
+    motion (positive charge).  So dU = q delta and dV = 0: a flipped U, a
+    missing or misplaced asinh, or a residual taken the other way would fail.
+    Both charges occur among the tracks."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    x, y, z, arc, truth = _noise_free(w, 40, seed=11)
+    q = np.sign(truth[:, 4])
+    assert (q > 0).any() and (q < 0).any()
+    for i in range(truth.shape[0]):
+        s = oracle.seed_from_points(np.stack([x[i, :3], y[i, :3], z[i, :3]], 1), w.b_field)
+        cx, cy = _circle_centre(x[i, :3], y[i, :3])
+        for j in (4, 11, 19):
+            nx, ny = x[i, j] - cx, y[i, j] - cy
+            nn = math.hypot(nx, ny)
+            hit = [x[i, j] + delta * nx / nn, y[i, j] + delta * ny / nn, z[i, j]]
+            f = oracle.seed_features_hit(s, w.b_field, hit)
+            assert abs(f[0] - math.asinh(q[i] * delta)) < 1e-7, (i, j, f, q[i])
+            assert abs(f[1]) < 1e-7
+            assert abs(f[2] - arc[i, j] / math.sin(truth[i, 3])) < 1e-7
+
+
+@pytest.mark.parametrize("dz", [0.02, -1.5, 4.0])
+def test_features_of_a_hit_moved_off_the_helix_along_z(dz):
+    """A noise-free hit moved by dz along z keeps its transverse position, so
+    its helix point and path length are unchanged and its residual is
+    (0, 0, dz).  U is transverse, so dU = 0; V = T x U has z component
+    sin(theta), so dV = sin(theta) dz.  A missing sin(theta), or a V built as
+    U x T, would fail."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    x, y, z, arc, truth = _noise_free(w, 40, seed=12)
+    for i in range(truth.shape[0]):
+        s = oracle.seed_from_points(np.stack([x[i, :3], y[i, :3], z[i, :3]], 1), w.b_field)
+        st = math.sin(truth[i, 3])
+        for j in (3, 9, 18):
+            f = oracle.seed_features_hit(s, w.b_field, [x[i, j], y[i, j], z[i, j] + dz])
+            assert abs(f[0]) < 1e-7, (i, j, f)
+            assert abs(f[1] - math.asinh(st * dz)) < 1e-7, (i, j, f, st)
+            assert abs(f[2] - arc[i, j] / st) < 1e-7
+
+
+def test_features_of_a_general_off_helix_move_add_up():
+    """The two moves together: outward by a, along z by b gives dU = q a and
+    dV = sin(theta) b (the frame is orthonormal, so the components of the
+    residual do not mix)."""
+    w = ts.WORKLOADS["d128x4_fp32_65k"]
+    x, y, z, arc, truth = _noise_free(w, 30, seed=13)
+    rng = np.random.default_rng(14)
+    for i in range(truth.shape[0]):
+        s = oracle.seed_from_points(np.stack([x[i, :3], y[i, :3], z[i, :3]], 1), w.b_field)
+        cx, cy = _circle_centre(x[i, :3], y[i, :3])
+        j = int(rng.integers(3, w.n_det_layers))
+        a, b = rng.uniform(-2, 2, 2)
+        nx, ny = x[i, j] - cx, y[i, j] - cy
+        nn = math.hypot(nx, ny)
+        f = oracle.seed_features_hit(s, w.b_field, [x[i, j] + a * nx / nn, y[i, j] + a * ny / nn, z[i, j] + b])
+        st = math.sin(truth[i, 3])
+        assert abs(f[0] - math.asinh(math.copysign(1.0, truth[i, 4]) * a)) < 1e-7
+        assert abs(f[1] - math.asinh(st * b)) < 1e-7
+        assert abs(f[2] - arc[i, j] / st) < 1e-7
 
 
 def test_hand_built_positive_track():
