@@ -12,7 +12,7 @@ residual features (tf_seed_tracks) over the same tracks, one call per step.
 
 ``--path readout`` times the paper's readout path per batch: the seed, the
 encoder up to the last layer's end states (fit_tracks_states), and the
-35-quantile head with its medians and seed-anchored decode (tf_decode_tracks),
+35-quantile head with its point estimates and seed-anchored decode (tf_decode_tracks),
 three launches per batch, the step again captured in one HIP graph.
 
 ``--path paper`` times the paper's own deployed model per batch (workload
@@ -297,7 +297,7 @@ def bench_seed(args, w, hits, offs):
     print(json.dumps(res), flush=True)
 
 
-READOUT_METRIC = ("tracks/sec (seed + encoder end states + 35-quantile readout, median, decode) on 1 MI355X; "
+READOUT_METRIC = ("tracks/sec (seed + encoder end states + 35-quantile readout, point estimate, decode) on 1 MI355X; "
                   "MFMA util vs peak")
 
 
@@ -308,9 +308,9 @@ def states_algorithmic_flops(n_layers, d, n_hits, n_features=0):
     return 8.0 * d * d * (n_layers - 1) * n_hits + 4.0 * d * d * n_hits + front_flops(d, n_hits, n_features)
 
 
-def readout_algorithmic_flops(d, n_tracks):
-    """Per track: 2 * d * 2d for W1, 2 * 35 * d for W2."""
-    return (4.0 * d * d + 70.0 * d) * n_tracks
+def readout_algorithmic_flops(d, nh, n_tracks):
+    """Per track: 2 * nh * 2d for W1 (nh hidden units), 2 * 35 * nh for W2."""
+    return (4.0 * d * nh + 70.0 * nh) * n_tracks
 
 
 def readout_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
@@ -328,7 +328,7 @@ def readout_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
         seeds, sf, _ = oracle.seed_tracks(h, o, w.b_field, features=bool(w.n_features))
         inp = ts.hit_features(w, h, o, np.nan_to_num(sf, nan=0.0)) if w.n_features else h
         st = oracle.track_states(inp, o, blob, w.n_layers, w.d_model, n_threads=threads, n_features=w.n_features)
-        _, out = oracle.readout_tracks(st, seeds, hb, w.d_model)
+        _, out = oracle.readout_tracks(st, seeds, hb, *ts.readout_dims(w))
         return out, time.perf_counter() - t0
 
     idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
@@ -358,7 +358,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
     blob = model_blob(w)
     hb = ts.make_readout_weights(w)
     W = tf.Weights(blob, w.n_layers, d, mode, max_hits=args.max_hits or w.len_max, n_features=w.n_features)
-    R = tf.Readout(hb, d, mode)
+    R = tf.Readout(hb, *ts.readout_dims(w), mode)
     # the Fourier front end reads per-hit feature rows: the measured columns are
     # inputs; the seed fills columns 12..14 of each batch's rows inside the step
     feats = device_features(tf, w, hits, offs, h, o, dev) if w.n_features else None
@@ -447,7 +447,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
                      "traffic": traffic_bytes("readout", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
-        "readout_flops_per_step": readout_algorithmic_flops(d, n_tracks),
+        "readout_flops_per_step": readout_algorithmic_flops(*ts.readout_dims(w), n_tracks),
         "host_wall_s": wall,
         "device_error_flags": flags,
         "finite_outputs": bool(np.isfinite(gpu_out).all()),
@@ -491,7 +491,7 @@ def paper_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
         feats = ts.hit_features(w, h, o, np.nan_to_num(sf, nan=0.0))
         st = oracle.mingru_states(feats, o, blob, w.n_layers, w.d_model, w.hidden, n_features=w.n_features,
                                   n_threads=threads)
-        _, out = oracle.readout_tracks(st, seeds, hb, w.hidden)
+        _, out = oracle.readout_tracks(st, seeds, hb, *ts.readout_dims(w))
         return out, time.perf_counter() - t0
 
     idx = np.sort(rng.choice(n_all, size=min(256, n_all), replace=False))
@@ -511,7 +511,6 @@ def paper_cpu_baseline(w, blob, hb, hits, offs, seconds, threads, gpu_out):
 
 
 def bench_paper(args, w, hits, offs, mode, batch):
-    import dataclasses
     import torch
     import paper_2609_32479_amd as tf
     assert w.arch == "mingru", "--path paper takes a minGRU workload"
@@ -522,9 +521,9 @@ def bench_paper(args, w, hits, offs, mode, batch):
     n_hits = int(offs[-1] - offs[0])
     H = w.hidden
     blob = ts.make_mingru_weights(w)
-    hb = ts.make_readout_weights(dataclasses.replace(w, d_model=H))
+    hb = ts.make_readout_weights(w)
     M = tf.MinGRU(blob, w.n_layers, w.d_model, H, mode, w.n_features)
-    R = tf.Readout(hb, H, mode)
+    R = tf.Readout(hb, *ts.readout_dims(w), mode)
     feats = device_features(tf, w, hits, offs, h, o, dev)
     seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
     out = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)

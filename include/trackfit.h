@@ -50,12 +50,16 @@ typedef enum { TF_FP32 = 0, TF_BF16 = 1, TF_BF16_F16ACT = 2 } tf_dtype;
  * TF_FP32         fp32 weights and activations.
  * TF_BF16         bf16 weights; the normalised activations and the scan
  *                 outputs are rounded to bf16 as GEMM operands.
- * TF_BF16_F16ACT  bf16-valued weights (held exactly in fp16), activations
- *                 rounded to fp16 (the paper's fp16 projections): same speed as
- *                 TF_BF16 with 3 more mantissa bits on the activations.
+ * TF_BF16_F16ACT  weights converted to fp16 operands, activations rounded
+ *                 to fp16 (the paper's fp16 projections): same speed as
+ *                 TF_BF16 with 3 more mantissa bits on the activations.  A
+ *                 bf16 weight converts to fp16 exactly only if its magnitude
+ *                 lies in the fp16 normal range [2^-14, 65504]; smaller ones
+ *                 lose low bits as fp16 subnormals, larger ones overflow.
  * In both 16-bit modes the RMSNorm gain is folded into the input-projection
- * weights (rounded once to the operand type) and the two head layers multiply
- * their fp32 input as a high and a low 16-bit part. */
+ * weights, and the product W_in g is rounded once to the operand type (so it
+ * is not the bf16 weight itself), and the two head layers multiply their fp32
+ * input as a high and a low 16-bit part. */
 typedef struct {
     int32_t n_layers;
     int32_t d_model;
@@ -235,23 +239,27 @@ tf_status tf_seed_tracks(const float *hits, int64_t n_hits, const int32_t *offse
 
 /*
  * The paper's readout and decode (Sec. Encoder, last paragraph: RMSNorm of the
- * end states, a two-layer head with hidden width d and SiLU, 35 outputs;
- * Sec. Losses: seven quantiles per parameter, the median as point estimate;
- * Sec. Method: the prediction is a correction to the analytic seed).
+ * end states and a two-layer head of hidden width 128 with 35 outputs; Sec.
+ * Losses: seven quantiles per parameter, the median quantile as the point
+ * estimate; Sec. Method: the prediction is a correction to the analytic
+ * seed).  The head's activation is SiLU.
  *
  * Opaque: the head's weights in kernel order on the device.  Owned by the
  * library.
  */
 typedef struct tf_readout tf_readout;
 
-/* Number of floats of a readout head blob for width d (0 if invalid):
- * norm.g[2d], W1[d][2d], b1[d], W2[35][d], b2[35] (row-major [out][in]).
- * Output 7 p + i of W2 is quantile i of parameter p (d0, z0, phi, theta, q/p
- * order), the quantiles in increasing order of their levels. */
-size_t tf_readout_blob_size(int32_t d);
+/* Number of floats of a readout head blob for end states of width 2d and a
+ * hidden layer of `hidden` units (0 if invalid):
+ * norm.g[2d], W1[hidden][2d], b1[hidden], W2[35][hidden], b2[35]
+ * (row-major [out][in]).  Output 7 p + i of W2 is quantile i of parameter p
+ * (d0, z0, phi, theta, q/p order), the quantiles in increasing order of their
+ * levels, so that output 7 p + 3 is the median quantile (level 1/2). */
+size_t tf_readout_blob_size(int32_t d, int32_t hidden);
 
-/* Copy a readout head blob to the current device.  d: 32, 64, 128, 192 (the
- * paper's backbone: states of 2 x 192) or 256.
+/* Copy a readout head blob to the current device.  d: a multiple of 32 up to
+ * 256 (192 for the paper's backbone: states of 2 x 192); hidden: a multiple
+ * of 32 up to 256 (the paper's head: 128).
  * dtype (tf_dtype): TF_FP32 runs the head's products in fp32; TF_BF16 and
  * TF_BF16_F16ACT (the 16-bit models) take W1 and W2 in bf16 (exact for
  * bf16-valued weights; others are rounded to nearest even) and multiply them
@@ -259,19 +267,19 @@ size_t tf_readout_blob_size(int32_t d);
  * a low bf16 part (about 16 significant bits), accumulating in fp32.
  * host_blob is only read during the call; *out receives a handle freed with
  * tf_readout_destroy.  Synchronous; allocates device memory.
- * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d),
- * unknown dtype), TF_EUNSUPPORTED (other d), TF_ENOMEM, TF_EHIP.  On error
- * *out is NULL. */
-tf_status tf_readout_create(int32_t d, int32_t dtype, const float *host_blob, size_t n_floats,
+ * Errors: TF_EINVAL (null pointers, n_floats != tf_readout_blob_size(d,
+ * hidden), unknown dtype), TF_EUNSUPPORTED (other d or hidden), TF_ENOMEM,
+ * TF_EHIP.  On error *out is NULL. */
+tf_status tf_readout_create(int32_t d, int32_t hidden, int32_t dtype, const float *host_blob, size_t n_floats,
                             tf_readout **out);
 
 /* Free a handle (NULL is a no-op).  Synchronises the device first. */
 void tf_readout_destroy(tf_readout *h);
 
 /*
- * Readout, median and decode of a batch of tracks:
+ * Readout, point estimates and decode of a batch of tracks:
  *   y = g (.) z / sqrt(mean(z^2) + 1e-6),  h = SiLU(W1 y + b1),
- *   q = W2 h + b2,  m_p = median(q[7p .. 7p+6]),
+ *   q = W2 h + b2,  m_p = q[7p + 3] (parameter p's median quantile),
  *   d0, z0, theta: seed + m;  phi: seed + m wrapped to [-pi, pi);
  *   q/p: seed + m * (|seed| + 0.02 / GeV).
  * The head runs on matrix cores with fp32 accumulation in the handle's number
@@ -296,12 +304,13 @@ tf_status tf_decode_tracks(const float *states, int32_t n_tracks, const double *
                            float *quantiles, double *out, hipStream_t stream);
 
 /*
- * The paper's own backbone (Sec. Encoder): a stack of bidirectional minGRU
- * layers of hidden width H behind the front end.  Each layer projects its
- * input linearly to the forward and reverse candidates and gates, z =
- * sigmoid(gate), runs the update of Eq. (2) forward from each track's first
- * hit and in reverse from its last (zero initial state), and hands [f; b]
- * (2H values per hit) to the next layer; no normalisation or residual inside.
+ * The paper's own backbone (Sec. Encoder, Eq. (2)): a stack of bidirectional
+ * minGRU layers of H channels per direction behind the front end.  Per layer,
+ * four linear maps of the input give the forward and the reverse pass a
+ * candidate and a gate each (z = sigmoid(gate)); the passes run the update of
+ * Eq. (2) from each track's first hit and from its last (zero initial state),
+ * and [f; b] (2H values per hit) feeds the next layer; no normalisation or
+ * residual inside.
  * Number types as for tf_config.dtype: fp32 throughout, or 16-bit matrix
  * operands (weights bf16, activations bf16 or fp16) with fp32 accumulation,
  * gates and recurrence.

@@ -1,9 +1,11 @@
 /*
  * Plain fp64 CPU oracle of the paper's bidirectional minGRU backbone (Sec.
- * Encoder: a stack of bidirectional minGRU layers of hidden width H; each
- * layer projects its input linearly to the forward and reverse gates and
- * candidate states, runs a forward and a reverse scan, and the two
- * directions' states, concatenated (2H values), are the next layer's input).
+ * Encoder, Eq. (2)).  Every layer of the stack carries H channels per
+ * direction: four linear maps of the layer's input give a candidate and a
+ * gate for the left-to-right pass and another pair for the right-to-left
+ * pass; each pass runs the update of Eq. (2) over the track's hits, and at
+ * every hit the 2H states of the two passes, stacked, form the input of the
+ * layer above.
  * TEST INFRASTRUCTURE ONLY: it exists to check the GPU library.  Only the
  * test suite, the smoke check and the benchmark's CPU-baseline leg may load
  * or call it.  It shares no code, header or table with the GPU library.

@@ -84,9 +84,10 @@ def lib():
         L.tf_seed_tracks.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, ctypes.c_double, vp, vp, ctypes.c_int32,
                                      vp, vp]
         L.tf_readout_blob_size.restype = ctypes.c_size_t
-        L.tf_readout_blob_size.argtypes = [ctypes.c_int32]
+        L.tf_readout_blob_size.argtypes = [ctypes.c_int32, ctypes.c_int32]
         L.tf_readout_create.restype = ctypes.c_int
-        L.tf_readout_create.argtypes = [ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t, ctypes.POINTER(vp)]
+        L.tf_readout_create.argtypes = [ctypes.c_int32, ctypes.c_int32, ctypes.c_int32, vp, ctypes.c_size_t,
+                                        ctypes.POINTER(vp)]
         L.tf_readout_destroy.restype = None
         L.tf_readout_destroy.argtypes = [vp]
         L.tf_mingru_blob_size.restype = ctypes.c_size_t
@@ -271,22 +272,23 @@ def seed_tracks(hits: torch.Tensor, offsets: torch.Tensor, b_tesla: float, featu
     return seeds, feats
 
 
-def readout_blob_size(d: int) -> int:
-    return int(lib().tf_readout_blob_size(int(d)))
+def readout_blob_size(d: int, hidden: int) -> int:
+    return int(lib().tf_readout_blob_size(int(d), int(hidden)))
 
 
 class Readout:
-    """Device-resident readout head (tf_readout handle) on the current device."""
+    """Device-resident readout head (tf_readout handle) on the current device:
+    end states of width 2d, a hidden layer of `hidden` units, 35 outputs."""
 
-    def __init__(self, blob, d: int, dtype: str = "fp32"):
+    def __init__(self, blob, d: int, hidden: int, dtype: str = "fp32"):
         """dtype: "fp32", or "bf16" / "bf16_f16act" for the 16-bit head (include/trackfit.h)."""
         import numpy as np
         arr = np.ascontiguousarray(np.asarray(blob, dtype=np.float32).reshape(-1))
         h = ctypes.c_void_p()
-        _check(lib().tf_readout_create(int(d), DTYPES[dtype], arr.ctypes.data, arr.size, ctypes.byref(h)),
-               "tf_readout_create")
+        _check(lib().tf_readout_create(int(d), int(hidden), DTYPES[dtype], arr.ctypes.data, arr.size,
+                                       ctypes.byref(h)), "tf_readout_create")
         self._h = h
-        self.d, self.dtype = int(d), dtype
+        self.d, self.hidden, self.dtype = int(d), int(hidden), dtype
 
     @property
     def handle(self):
@@ -306,7 +308,8 @@ class Readout:
 
 def decode_tracks(states: torch.Tensor, seeds: torch.Tensor, readout: Readout, quantiles: bool = False,
                   out: torch.Tensor | None = None, q: torch.Tensor | None = None, stream=None):
-    """Enqueue the readout head, the medians and the seed-anchored decode.
+    """Enqueue the readout head, the point estimates (each parameter's median
+    quantile) and the seed-anchored decode.
 
     states float32 [N, 2d] (fit_tracks_states), seeds float64 [N, 5]
     (seed_tracks), both on the GPU.  Returns (out float64 [N, 5], quantiles

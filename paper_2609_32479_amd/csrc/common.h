@@ -20,8 +20,9 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4;
 
 // Matrix-core operand types.  OP_F32: fp32 weights and operands
 // (v_mfma_f32_32x32x2_f32).  OP_BF16: bf16 weights and bf16 activation
-// operands (v_mfma_f32_32x32x16_bf16).  OP_F16: bf16-valued weights held
-// exactly in fp16 and fp16 activation operands (v_mfma_f32_32x32x16_f16).
+// operands (v_mfma_f32_32x32x16_bf16).  OP_F16: weights converted to fp16
+// (exact for bf16 values in the fp16 normal range) and fp16 activation
+// operands (v_mfma_f32_32x32x16_f16).
 // Accumulation is fp32 in all three.
 enum { OP_F32 = 0, OP_BF16 = 1, OP_F16 = 2 };
 

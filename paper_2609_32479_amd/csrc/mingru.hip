@@ -1,8 +1,9 @@
-// The paper's bidirectional minGRU backbone on gfx950 (Sec. Encoder): each
-// layer projects its input linearly to forward and reverse candidates and
-// gates, z = sigmoid(gate), runs the update of Eq. (2) forward from each
-// track's first hit and in reverse from its last, and hands the two
-// directions' states, concatenated (2H values per hit), to the next layer.
+// The paper's bidirectional minGRU backbone on gfx950 (Sec. Encoder, Eq. (2)):
+// per layer, four linear maps of the input give the left-to-right and the
+// right-to-left pass a candidate and a gate each (z = sigmoid(gate)); the
+// passes run the update of Eq. (2) from each track's first hit and from its
+// last, and the 2H states of the two passes at a hit, stacked, feed the
+// layer above.
 // The last layer's forward state at a track's last hit and reverse state at
 // its first hit are the readout's input.
 //

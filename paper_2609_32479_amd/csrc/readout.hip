@@ -4,10 +4,12 @@
 //
 // Per track, with z = [f; b] the last layer's forward state at the last hit
 // and reverse state at the first hit (2d floats, from fit_tracks_states):
-// y = g (.) z / rms(z); h = SiLU(W1 y + b1); q = W2 h + b2 (35 values, seven
-// quantiles for each of d0, z0, phi, theta, q/p); the point estimate of each
-// parameter is the median of its seven; it is added to the fp64 seed (phi
-// wrapped to [-pi, pi)), q/p through the seed's scale |q/p_seed| + 0.02/GeV.
+// y = g (.) z / rms(z); h = SiLU(W1 y + b1) with NH hidden units (the paper's
+// head has 128); q = W2 h + b2 (35 values, seven quantiles at ascending levels
+// for each of d0, z0, phi, theta, q/p); the point estimate of each parameter
+// is its median quantile, the middle output q[7p + 3]; it is added to the
+// fp64 seed (phi wrapped to [-pi, pi)), q/p through the seed's scale
+// |q/p_seed| + 0.02/GeV.
 //
 // One wave per 32 tracks, both layers as matrix-core products with the
 // tracks on the 32 columns: hid^T = W1' z^T with W1' = W1 diag(g) (the gain
@@ -48,6 +50,7 @@ constexpr double kQopEps = 0.02;  // 1/GeV, scale floor of the q/p decode
 constexpr double kPi = 3.14159265358979323846;
 constexpr int kWaves = 4;
 constexpr int kQStride = 37;    // LDS row stride of a track's 35 outputs (floats)
+constexpr int kMaxHidden = 256; // hidden units of the head, at most (a multiple of 32)
 
 __device__ __forceinline__ f32x16 mma(float a, float b, f32x16 c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
@@ -63,23 +66,6 @@ __device__ __forceinline__ void split16(const f32x8 v, bf16x8 &hi, bf16x8 &lo) {
     lo = __builtin_convertvector(v - __builtin_convertvector(hi, f32x8), bf16x8);
 }
 
-// Median of seven: the value whose rank (ties broken by position) is 3; NaN if
-// any of the seven is NaN.
-__device__ __forceinline__ float median7(const float *v) {
-    float med = 0.f;
-    bool nan = false;
-#pragma unroll
-    for (int i = 0; i < kNq; ++i) {
-        int rank = 0;
-#pragma unroll
-        for (int j = 0; j < kNq; ++j)
-            if (j != i) rank += (v[j] < v[i] || (v[j] == v[i] && j < i)) ? 1 : 0;
-        if (rank == kNq / 2) med = v[i];
-        nan |= v[i] != v[i];
-    }
-    return nan ? __builtin_nanf("") : med;
-}
-
 // Layer 1 bias and SiLU on the accumulators (lane (s, c) holds unit
 // 32 m + 8 (q/4) + 4 s + q%4 of track c), in place.
 template <int MT>
@@ -93,7 +79,7 @@ __device__ __forceinline__ void bias_silu(f32x16 (&acc)[MT], float inv, const fl
         }
 }
 
-// Outputs to LDS, then medians, decode and the optional quantile rows.  o[rb]
+// Outputs to LDS, then the point estimates, decode and the optional quantile rows.  o[rb]
 // holds rows 32 rb + 8 (q/4) + 4 s + q%4 of track c (rows past 34 unused).
 __device__ __forceinline__ void finish(const f32x16 (&o)[2], const float *__restrict__ b2, float (*qs)[kQStride],
                                        int lane, int t0, int n, const double *__restrict__ seeds,
@@ -110,14 +96,15 @@ __device__ __forceinline__ void finish(const f32x16 (&o)[2], const float *__rest
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 
-    // medians and decode: lane half 0 takes d0, z0, phi; half 1 theta, q/p
+    // point estimates (each parameter's median quantile, its middle output) and
+    // decode: lane half 0 takes d0, z0, phi; half 1 theta, q/p
     const int t = t0 + c;
     if (t < n) {
         const float *qt = qs[c];
         const double *sd = seeds + (size_t)t * 5;
         double *op = out + (size_t)t * 5;
         for (int p = s ? 3 : 0; p < (s ? 5 : 3); ++p) {
-            const double med = (double)median7(qt + kNq * p);
+            const double med = (double)qt[kNq * p + kNq / 2];
             const double seed = sd[p];
             double v;
             if (p == 2) {
@@ -140,15 +127,15 @@ __device__ __forceinline__ void finish(const f32x16 (&o)[2], const float *__rest
 }
 
 // fp32 head: A1 [d/4][MT][64] float4 (4 consecutive k-steps), A2 [MT][4][2][64] float4.
-template <int D>
-__global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__restrict__ states, int n,
+// MT: 32-unit blocks of the hidden layer; D: half the state width (a multiple of 8).
+template <int MT>
+__global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__restrict__ states, int n, int D,
                                                                  const double *__restrict__ seeds,
                                                                  const float4 *__restrict__ A1,
                                                                  const float *__restrict__ b1,
                                                                  const float4 *__restrict__ A2,
                                                                  const float *__restrict__ b2,
                                                                  float *__restrict__ quant, double *__restrict__ out) {
-    constexpr int MT = D / 32;  // 32-unit blocks of the hidden layer
     __shared__ float qs[kWaves][32][kQStride];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int t0 = (blockIdx.x * kWaves + wv) * 32;
@@ -208,8 +195,8 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout_kernel(const float *__
 // 16-bit head: A1 [d/8][MT][64] bf16x8 (lane (s, i): W1 row 32 m + i, k = s d + 8 ks + e),
 // A2 [MT][2][2][64] bf16x8 (k-step (m, qh): the lane's units of acc[m][8 qh .. 8 qh + 7]),
 // gain [2d] fp32.
-template <int D>
-__global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *__restrict__ states, int n,
+template <int MT>
+__global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *__restrict__ states, int n, int D,
                                                                    const double *__restrict__ seeds,
                                                                    const bf16x8 *__restrict__ A1,
                                                                    const float *__restrict__ gain,
@@ -217,7 +204,6 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *
                                                                    const bf16x8 *__restrict__ A2,
                                                                    const float *__restrict__ b2,
                                                                    float *__restrict__ quant, double *__restrict__ out) {
-    constexpr int MT = D / 32;
     __shared__ float qs[kWaves][32][kQStride];
     const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
     const int t0 = (blockIdx.x * kWaves + wv) * 32;
@@ -282,6 +268,7 @@ __global__ __launch_bounds__(64 * kWaves) void tf_readout16_kernel(const float *
 
 struct tf_readout {
     int d = 0;
+    int hidden = 0;
     bool half = false;       // 16-bit head (tf_readout16_kernel)
     char *dmem = nullptr;
     const void *A1 = nullptr;
@@ -302,38 +289,42 @@ uint16_t bf16_bits(float x) {
     return (uint16_t)(u >> 16);
 }
 
-template <int D>
-void launch_d(const tf_readout *h, dim3 grid, dim3 block, hipStream_t stream, const float *states, int n,
-              const double *seeds, float *quant, double *out) {
+template <int MT>
+void launch_mt(const tf_readout *h, dim3 grid, dim3 block, hipStream_t stream, const float *states, int n,
+               const double *seeds, float *quant, double *out) {
     if (h->half)
-        hipLaunchKernelGGL(tf_readout16_kernel<D>, grid, block, 0, stream, states, n, seeds,
+        hipLaunchKernelGGL(tf_readout16_kernel<MT>, grid, block, 0, stream, states, n, h->d, seeds,
                            static_cast<const bf16x8 *>(h->A1), h->gain, h->b1, static_cast<const bf16x8 *>(h->A2),
                            h->b2, quant, out);
     else
-        hipLaunchKernelGGL(tf_readout_kernel<D>, grid, block, 0, stream, states, n, seeds,
+        hipLaunchKernelGGL(tf_readout_kernel<MT>, grid, block, 0, stream, states, n, h->d, seeds,
                            static_cast<const float4 *>(h->A1), h->b1, static_cast<const float4 *>(h->A2), h->b2,
                            quant, out);
 }
 
-}  // namespace
-
-extern "C" size_t tf_readout_blob_size(int32_t d) {
-    if (d <= 0) return 0;
-    const size_t dd = (size_t)d;
-    return 2 * dd + dd * 2 * dd + dd + kNout * dd + kNout;
+bool valid_dims(int d, int hidden) {
+    return d >= 32 && d <= 256 && d % 32 == 0 && hidden >= 32 && hidden <= kMaxHidden && hidden % 32 == 0;
 }
 
-extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *host_blob, size_t n_floats,
-                                       tf_readout **out) {
+}  // namespace
+
+extern "C" size_t tf_readout_blob_size(int32_t d, int32_t hidden) {
+    if (d <= 0 || hidden <= 0) return 0;
+    const size_t dd = (size_t)d, nh = (size_t)hidden;
+    return 2 * dd + nh * 2 * dd + nh + kNout * nh + kNout;
+}
+
+extern "C" tf_status tf_readout_create(int32_t d, int32_t hidden, int32_t dtype, const float *host_blob,
+                                       size_t n_floats, tf_readout **out) {
     if (!out) return TF_EINVAL;
     *out = nullptr;
-    if (!host_blob || d <= 0 || n_floats != tf_readout_blob_size(d)) return TF_EINVAL;
+    if (!host_blob || d <= 0 || hidden <= 0 || n_floats != tf_readout_blob_size(d, hidden)) return TF_EINVAL;
     if (dtype != TF_FP32 && dtype != TF_BF16 && dtype != TF_BF16_F16ACT) return TF_EINVAL;
-    if (d != 32 && d != 64 && d != 128 && d != 192 && d != 256) return TF_EUNSUPPORTED;
+    if (!valid_dims(d, hidden)) return TF_EUNSUPPORTED;
     const bool half = dtype != TF_FP32;
-    const size_t dd = (size_t)d;
-    const int MT = d / 32;
-    const float *g = host_blob, *W1 = g + 2 * dd, *b1 = W1 + dd * 2 * dd, *W2 = b1 + dd, *b2 = W2 + kNout * dd;
+    const size_t dd = (size_t)d, nh = (size_t)hidden;
+    const int MT = hidden / 32;
+    const float *g = host_blob, *W1 = g + 2 * dd, *b1 = W1 + nh * 2 * dd, *W2 = b1 + nh, *b2 = W2 + kNout * nh;
     // W1 as lane (s, i) holds it: row 32 m + i, column s d + kk, where kk is the k-step's
     // position in the lane's half row, with the gain folded in for the fp32 head (the
     // 16-bit head applies it to the activations); W2 as lane (s, i) holds it: row 32 rb + i,
@@ -345,11 +336,11 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
     auto w2 = [&](int rb, int lane, int m, int q) {
         const int row = 32 * rb + (lane & 31);
         const size_t u = 32 * m + 8 * (q >> 2) + 4 * (lane >> 5) + (q & 3);
-        return row < kNout ? W2[(size_t)row * dd + u] : 0.f;
+        return row < kNout ? W2[(size_t)row * nh + u] : 0.f;
     };
     const size_t esz = half ? 2 : 4;
-    const size_t nA1 = dd * 2 * dd, nA2 = (size_t)MT * 2 * 16 * 64;  // elements (A2: 2 row blocks x 16 slots)
-    const size_t oB1 = nA1 * esz, oA2 = oB1 + dd * 4, oB2 = oA2 + nA2 * esz, oG = oB2 + 64 * 4;
+    const size_t nA1 = nh * 2 * dd, nA2 = (size_t)MT * 2 * 16 * 64;  // elements (A2: 2 row blocks x 16 slots)
+    const size_t oB1 = nA1 * esz, oA2 = oB1 + nh * 4, oB2 = oA2 + nA2 * esz, oG = oB2 + 64 * 4;
     const size_t total = oG + 2 * dd * 4;
     std::vector<char> hbuf;
     try {
@@ -392,7 +383,7 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
                         for (int e = 0; e < 4; ++e)
                             A2[((((size_t)m * 4 + qg) * 2 + rb) * 64 + lane) * 4 + e] = w2(rb, lane, m, 4 * qg + e);
     }
-    std::memcpy(hp + oB1, b1, dd * 4);
+    std::memcpy(hp + oB1, b1, nh * 4);
     std::memcpy(hp + oB2, b2, kNout * 4);
     std::memcpy(hp + oG, g, 2 * dd * 4);
     tf_readout *ro = new (std::nothrow) tf_readout;
@@ -407,6 +398,7 @@ extern "C" tf_status tf_readout_create(int32_t d, int32_t dtype, const float *ho
         return TF_EHIP;
     }
     ro->d = d;
+    ro->hidden = hidden;
     ro->half = half;
     ro->A1 = ro->dmem;
     ro->b1 = reinterpret_cast<const float *>(ro->dmem + oB1);
@@ -431,12 +423,17 @@ extern "C" tf_status tf_decode_tracks(const float *states, int32_t n_tracks, con
     if (!states || !seeds || !out) return TF_EINVAL;
     const int per_block = 32 * kWaves;
     const dim3 grid((unsigned)((n_tracks + per_block - 1) / per_block)), block(64 * kWaves);
-    switch (h->d) {
-        case 32: launch_d<32>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
-        case 64: launch_d<64>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
-        case 128: launch_d<128>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
-        case 192: launch_d<192>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
-        case 256: launch_d<256>(h, grid, block, stream, states, (int)n_tracks, seeds, quantiles, out); break;
+    if (!valid_dims(h->d, h->hidden)) return TF_EINVAL;
+    const int nt = (int)n_tracks;
+    switch (h->hidden / 32) {
+        case 1: launch_mt<1>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 2: launch_mt<2>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 3: launch_mt<3>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 4: launch_mt<4>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 5: launch_mt<5>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 6: launch_mt<6>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 7: launch_mt<7>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
+        case 8: launch_mt<8>(h, grid, block, stream, states, nt, seeds, quantiles, out); break;
         default: return TF_EINVAL;
     }
     return hipGetLastError() == hipSuccess ? TF_OK : TF_EHIP;

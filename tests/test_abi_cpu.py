@@ -94,17 +94,20 @@ def test_argument_checks_without_gpu(tf):
 def test_readout_and_states_argument_checks_without_gpu(tf):
     import oracle
     L = tf.lib()
-    for d in (32, 64, 128, 256):
-        assert L.tf_readout_blob_size(d) == oracle.readout_blob_size(d) == 2 * d + 2 * d * d + d + 35 * d + 35
-    assert L.tf_readout_blob_size(0) == 0
+    for d, nh in ((32, 32), (64, 96), (128, 128), (192, 128), (256, 64)):
+        n = 2 * d + nh * 2 * d + nh + 35 * nh + 35
+        assert L.tf_readout_blob_size(d, nh) == oracle.readout_blob_size(d, nh) == n
+    assert L.tf_readout_blob_size(0, 128) == 0 and L.tf_readout_blob_size(128, 0) == 0
     h = ctypes.c_void_p()
     blob = (ctypes.c_float * 10)()
     fp32 = tf.TF_FP32
-    assert L.tf_readout_create(128, fp32, blob, 10, ctypes.byref(h)) == tf.TF_EINVAL          # wrong size
-    assert L.tf_readout_create(128, fp32, None, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL
-    assert L.tf_readout_create(128, fp32, blob, 10, None) == tf.TF_EINVAL
-    assert L.tf_readout_create(128, 9, blob, L.tf_readout_blob_size(128), ctypes.byref(h)) == tf.TF_EINVAL  # dtype
-    assert L.tf_readout_create(96, fp32, blob, L.tf_readout_blob_size(96), ctypes.byref(h)) == tf.TF_EUNSUPPORTED
+    size = L.tf_readout_blob_size
+    assert L.tf_readout_create(128, 128, fp32, blob, 10, ctypes.byref(h)) == tf.TF_EINVAL     # wrong size
+    assert L.tf_readout_create(128, 128, fp32, None, size(128, 128), ctypes.byref(h)) == tf.TF_EINVAL
+    assert L.tf_readout_create(128, 128, fp32, blob, 10, None) == tf.TF_EINVAL
+    assert L.tf_readout_create(128, 128, 9, blob, size(128, 128), ctypes.byref(h)) == tf.TF_EINVAL  # dtype
+    for d, nh in ((40, 128), (288, 128), (128, 48), (128, 288)):   # widths not multiples of 32, or too wide
+        assert L.tf_readout_create(d, nh, fp32, blob, size(d, nh), ctypes.byref(h)) == tf.TF_EUNSUPPORTED
     assert h.value is None
     L.tf_readout_destroy(None)   # no-op
     assert L.tf_decode_tracks(None, 0, None, None, None, None, None) == tf.TF_EINVAL    # null handle

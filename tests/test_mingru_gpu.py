@@ -132,24 +132,26 @@ def test_mingru_tile_independence_and_absolute_offsets(tf):
 
 @pytest.mark.parametrize("name", ["mingru2_h192_fourier15_deploy_bf16_8m", "mingru2_h192_fourier15_d128_fp32_65k"])
 def test_mingru_chain_into_readout_and_decode(tf, name):
-    """hits -> seed (features, seeds), backbone end states, 35-quantile head of
-    hidden width H on the 2H states, median and decode: against the oracle's
-    chain on the same features."""
+    """hits -> seed (features, seeds), backbone end states, the paper's
+    35-quantile head (hidden width 128 on the 2H = 384 states; 32 on the tiny
+    model's 128), point estimates and decode: against the oracle's chain on
+    the same features."""
     w = ts.workload(name)
     M, blob = _model(tf, w)
     hits, offs = ts.make_tracks(w, n_tracks=1500)
     seeds, sf, _ = oracle.seed_tracks(hits, offs, w.b_field)
     feats = ts.hit_features(w, hits, offs, sf)
     mode = tf.MODE_FOR_WEIGHTS[w.dtype]
-    hb = ts.make_readout_weights(dataclasses.replace(w, d_model=w.hidden))
-    R = tf.Readout(hb, w.hidden, mode)
+    hb = ts.make_readout_weights(w)
+    d, nh = ts.readout_dims(w)
+    R = tf.Readout(hb, d, nh, mode)
     st = _gpu(M, feats, offs)
     out, q = tf.decode_tracks(torch.from_numpy(st).cuda(), torch.from_numpy(seeds).cuda(), R, quantiles=True)
     torch.cuda.synchronize()
-    r_q, r_out = oracle.readout_tracks(_ref(w, feats, offs, blob), seeds, hb, w.hidden)
+    r_q, r_out = oracle.readout_tracks(_ref(w, feats, offs, blob), seeds, hb, d, nh)
     from tests.test_readout_gpu import colerr, wrap_phi, head_tols
     eq = colerr(q.cpu().numpy(), r_q)
     eo = colerr(wrap_phi(out.cpu().numpy(), r_out), r_out)
     print(f"[mingru-chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
-    tq, _ = head_tols(mode, w.hidden)
+    tq, _ = head_tols(mode, d, nh)
     assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]

@@ -176,7 +176,7 @@ def test_readout_path_full_size_sampled(tf):
     blob = ts.make_weights(w)
     hb = ts.make_readout_weights(w)
     W = tf.Weights(blob, w.n_layers, w.d_model, mode, max_hits=w.len_max)
-    R = tf.Readout(hb, w.d_model, mode)
+    R = tf.Readout(hb, *ts.readout_dims(w), mode)
     h = torch.from_numpy(hits).cuda()
     o = torch.from_numpy(offs).cuda()
     seeds = torch.empty((n, 5), dtype=torch.float64, device="cuda")
@@ -198,7 +198,7 @@ def test_readout_path_full_size_sampled(tf):
     so = np.concatenate([[0], np.cumsum(L[sel])]).astype(np.int32)
     r_seed, _, _ = oracle.seed_tracks(sh, so, w.b_field, features=False)
     r_st = oracle.track_states(sh, so, blob, w.n_layers, w.d_model)
-    _, r_out = oracle.readout_tracks(r_st, r_seed, hb, w.d_model)
+    _, r_out = oracle.readout_tracks(r_st, r_seed, hb, *ts.readout_dims(w))
     err = _decoded_err(g[sel], r_out)
     print(f"[full] readout path: {sel.size} sampled, max decoded column error {err:.3g}", flush=True)
     assert err <= TOL[w.dtype]
@@ -209,16 +209,15 @@ def test_paper_model_full_size_sampled(tf):
     minGRU layers, readout, decode) over all deployment tracks in 32
     graph-captured batches (the benchmark's configuration); a sample against
     the oracle's chain (its own seed features)."""
-    import dataclasses
     w = ts.workload("mingru2_h192_fourier15_deploy_bf16_8m")
     print(f"[full] paper model {w.name}: {w.n_tracks} tracks", flush=True)
     hits, offs = ts.make_tracks(w, workers=WORKERS)
     n = offs.size - 1
     mode = tf.MODE_FOR_WEIGHTS[w.dtype]
     blob = ts.make_mingru_weights(w)
-    hb = ts.make_readout_weights(dataclasses.replace(w, d_model=w.hidden))
+    hb = ts.make_readout_weights(w)
     M = tf.MinGRU(blob, w.n_layers, w.d_model, w.hidden, mode, w.n_features)
-    R = tf.Readout(hb, w.hidden, mode)
+    R = tf.Readout(hb, *ts.readout_dims(w), mode)
     h = torch.from_numpy(hits).cuda()
     o = torch.from_numpy(offs).cuda()
     feats = _device_feature_rows(tf, w, hits, offs, h, o)
@@ -246,7 +245,7 @@ def test_paper_model_full_size_sampled(tf):
     r_seed, sf, _ = oracle.seed_tracks(sh, so, w.b_field)
     r_st = oracle.mingru_states(ts.hit_features(w, sh, so, sf), so, blob, w.n_layers, w.d_model, w.hidden,
                                 n_features=w.n_features)
-    _, r_out = oracle.readout_tracks(r_st, r_seed, hb, w.hidden)
+    _, r_out = oracle.readout_tracks(r_st, r_seed, hb, *ts.readout_dims(w))
     err = _decoded_err(g[sel], r_out)
     print(f"[full] paper model: {sel.size} sampled, max decoded column error {err:.3g}", flush=True)
     assert err <= TOL[w.dtype]

@@ -1,6 +1,6 @@
 """GPU parity of the paper's readout path against the fp64 oracle, element by
 element: the encoder's last-layer end states (fit_tracks_states), the readout
-head with its medians and seed-anchored decode (tf_decode_tracks) on the
+head with its point estimates and seed-anchored decode (tf_decode_tracks) on the
 oracle's own states, and the chain seed -> states -> decode end to end, plus
 the edge cases (length 1 and maximum, ragged batches, rejected tracks, NaN
 inputs, tile independence).
@@ -23,26 +23,34 @@ N_STATES = {"tiny_d32_fp32": 256, "d128x4_fp32_65k": 2048, "d256x6_bf16_1m": 512
             "long64_d128x4_bf16_200k": 512, "deploy_d128x4_bf16_8m": 2048}
 # The head and the decode run in fp32 on fp32 states; against the fp64 oracle
 # on the same (fp32-valued) states the differences are fp32 roundings.  A
-# quantile is the end of two dot products (2d terms, then d), so its rounding
-# is bounded by about u * (2d + d) relative to the sum of the terms' magnitudes
-# (u = 2^-24), which for these random heads is a few times the column's scale:
-# the quantiles are held to u * 2d * 2 per column.  The decoded parameters are
+# quantile is the end of two dot products (2d terms, then nh, the hidden
+# width), so its rounding is bounded by about u * (2d + nh) relative to the sum
+# of the terms' magnitudes (u = 2^-24), which for these random heads is a few
+# times the column's scale: the quantiles are held to u * (2d + nh) * 4/3 per
+# column.  The decoded parameters are
 # held to the fp32 model's output tolerance.
 DECODE_TOL = 1e-5
 
 
-def quantile_tol(d):
-    return 2.0 ** -24 * (2 * d) * 2
+def quantile_tol(d, nh):
+    return 2.0 ** -24 * (2 * d + nh) * 4 / 3
 
 
-# The 16-bit head takes W1 and W2 in bf16 (exact for a bf16 model's weights,
-# rounded for an fp32 model's: ~2^-9 per weight, averaged over the dot
-# products) and keeps the activations to ~16 bits; it is held to the bf16
-# model's output tolerance.
-def head_tols(mode, d):
+# The 16-bit head takes W1 and W2 in bf16 and keeps the activations to ~16
+# bits; it is held to the bf16 model's output tolerance.  Its weights are
+# bf16 values, as a bf16 model's are (an fp32 model's head blob is rounded
+# to bf16 first, for the oracle as well, so that both sides see the same
+# weights: `head_blob`).
+def head_blob(w, mode, **kw):
+    """The workload's readout head blob, rounded to bf16 values for a 16-bit head."""
+    hb = ts.make_readout_weights(w, **kw)
+    return hb if mode == "fp32" else ts.round_to_bf16(hb)
+
+
+def head_tols(mode, d, nh):
     """(quantile, decoded) tolerances of a head of this number type."""
     if mode == "fp32":
-        return quantile_tol(d), DECODE_TOL
+        return quantile_tol(d, nh), DECODE_TOL
     return TOL["bf16"], TOL["bf16"]
 
 
@@ -196,34 +204,43 @@ def _decode(tf, R, states, seeds, quantiles=True):
     return out.cpu().numpy(), (q.cpu().numpy() if q is not None else None)
 
 
-@pytest.mark.parametrize("name,n,mode", [("deploy_d128x4_bf16_8m", 1000, "bf16"), ("deploy_d128x4_bf16_8m", 1000, "fp32"),
-                                         ("tiny_d32_fp32", 77, "fp32"), ("tiny_d32_fp32", 77, "bf16"),
-                                         ("d256x6_bf16_1m", 300, "bf16"), ("d256x6_bf16_1m", 300, "fp32"),
-                                         ("d128x4_fp32_65k", 500, "fp32"), ("deploy_d128x4_bf16_8m", 1, "bf16"),
-                                         ("deploy_d128x4_bf16_8m", 33, "bf16"), ("deploy_d128x4_bf16_8m", 33, "fp32")])
-def test_decode_matches_oracle_on_the_same_states(tf, name, n, mode):
+@pytest.mark.parametrize("name,n,mode,nh", [("deploy_d128x4_bf16_8m", 1000, "bf16", None),
+                                            ("deploy_d128x4_bf16_8m", 1000, "fp32", None),
+                                            ("tiny_d32_fp32", 77, "fp32", None), ("tiny_d32_fp32", 77, "bf16", None),
+                                            ("d256x6_bf16_1m", 300, "bf16", None), ("d256x6_bf16_1m", 300, "fp32", None),
+                                            ("d128x4_fp32_65k", 500, "fp32", None),
+                                            ("deploy_d128x4_bf16_8m", 1, "bf16", None),
+                                            ("deploy_d128x4_bf16_8m", 33, "bf16", None),
+                                            ("deploy_d128x4_bf16_8m", 33, "fp32", None),
+                                            ("deploy_d128x4_bf16_8m", 500, "bf16", 32),
+                                            ("deploy_d128x4_bf16_8m", 500, "fp32", 224),
+                                            ("d128x4_fp32_65k", 300, "fp32", 64),
+                                            ("d256x6_bf16_1m", 300, "bf16", 256)])
+def test_decode_matches_oracle_on_the_same_states(tf, name, n, mode, nh):
     """The oracle's states (rounded to fp32, as the library takes them) and
     seeds in; the 35 quantiles and the decoded parameters compared, for both
-    number types of the head."""
+    number types of the head, with hidden widths equal to and different from
+    the state width (nh: None takes the workload's head, 128 or 96)."""
     w = ts.WORKLOADS[name]
-    d = w.d_model
-    print(f"[decode] {name} n={n} head {mode}", flush=True)
+    d, nh0 = ts.readout_dims(w)
+    nh = nh0 if nh is None else nh
+    print(f"[decode] {name} n={n} head {mode} hidden {nh}", flush=True)
     # column scales from at least 300 tracks, the first n of which are decoded
     hits, offs = ts.make_tracks(w, n_tracks=max(n, 300))
     blob = ts.make_weights(w)
     st = _ref_states(w, hits, offs, blob).astype(np.float32)
     seeds, _, bad = oracle.seed_tracks(hits, offs, w.b_field, features=False)
     assert bad == 0
-    hb = ts.make_readout_weights(w)
-    R = tf.Readout(hb, d, mode)
-    r_q, r_out = oracle.readout_tracks(st.astype(np.float64), seeds, hb, d)
+    hb = head_blob(w, mode, hidden=nh)
+    R = tf.Readout(hb, d, nh, mode)
+    r_q, r_out = oracle.readout_tracks(st.astype(np.float64), seeds, hb, d, nh)
     rms_q, rms_o = (np.sqrt(np.mean(a ** 2, axis=0)) for a in (r_q, r_out))
     st, seeds, r_q, r_out = st[:n], seeds[:n], r_q[:n], r_out[:n]
     g_out, g_q = _decode(tf, R, st, seeds)
     eq = colerr(g_q, r_q, rms_q)
     eo = colerr(wrap_phi(g_out, r_out), r_out, rms_o)
     print(f"[decode] {name} head {mode}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
-    tq, to = head_tols(mode, d)
+    tq, to = head_tols(mode, d, nh)
     assert eq.max() <= tq and eo.max() <= to
     # without the quantile output the decode is the same, bit for bit
     g2, q2 = _decode(tf, R, st, seeds, quantiles=False)
@@ -231,21 +248,24 @@ def test_decode_matches_oracle_on_the_same_states(tf, name, n, mode):
 
 
 @pytest.mark.parametrize("mode", ["fp32", "bf16"])
-def test_decode_median_and_decode_rules_on_a_planted_head(tf, mode):
+def test_decode_point_estimate_and_decode_rules_on_a_planted_head(tf, mode):
     """A head whose quantiles are known in closed form: W1 = 0 and W2 = 0, so
     q = b2 for every track; the seven values of each parameter are planted
-    out of order, the decode then adds their middle value to the seed."""
-    d = 32
-    hb = np.zeros(oracle.readout_blob_size(d), np.float32)
+    out of order, and the decode adds the median quantile, output 7p + 3 (not
+    the middle of the sorted seven), to the seed.  Hidden width 64, states 64."""
+    d, nh = 32, 64
+    hb = np.zeros(oracle.readout_blob_size(d, nh), np.float32)
     hb[: 2 * d] = 1.0
     b2 = hb[-35:]
     rng = np.random.default_rng(8)
-    meds = np.array([0.25, -1.5, 3.0, 0.125, -0.75])
+    meds = np.zeros(5)
     for p in range(5):
         v = np.sort(rng.uniform(-4, 4, 7))
         b2[7 * p:7 * p + 7] = rng.permutation(v)
-        meds[p] = float(np.sort(b2[7 * p:7 * p + 7])[3])   # as stored (float32)
-    R = tf.Readout(hb, d, mode)
+        if b2[7 * p + 3] == np.sort(b2[7 * p:7 * p + 7])[3]:   # make the two readings differ
+            b2[7 * p + 3], b2[7 * p] = b2[7 * p], b2[7 * p + 3]
+        meds[p] = float(b2[7 * p + 3])   # as stored (float32)
+    R = tf.Readout(hb, d, nh, mode)
     n = 40
     states = rng.normal(size=(n, 2 * d)).astype(np.float32)
     seeds = np.stack([rng.uniform(-1, 1, n), rng.uniform(-50, 50, n), rng.uniform(-np.pi, np.pi, n),
@@ -271,16 +291,17 @@ def test_decode_nan_inputs_stay_local(tf, mode):
                       rng.uniform(0.2, 2.9, n), rng.uniform(-1, 1, n)], axis=1)
     st[7] = np.nan          # a rejected track's states
     seeds[40] = np.nan      # a track without a seed
+    nh = ts.readout_dims(w)[1]
     hb = ts.make_readout_weights(w)
-    R = tf.Readout(hb, d, mode)
+    R = tf.Readout(hb, d, nh, mode)
     out, q = _decode(tf, R, st, seeds)
     assert np.all(np.isnan(out[[7, 40]])) and np.all(np.isnan(q[7]))
     assert np.all(np.isfinite(q[40]))
     good = np.ones(n, bool)
     good[[7, 40]] = False
     assert np.all(np.isfinite(out[good]))
-    r_q, r_out = oracle.readout_tracks(st[good].astype(np.float64), seeds[good], hb, d)
-    tq, to = head_tols(mode, d)
+    r_q, r_out = oracle.readout_tracks(st[good].astype(np.float64), seeds[good], hb, d, nh)
+    tq, to = head_tols(mode, d, nh)
     assert colerr(q[good], r_q).max() <= tq
     assert colerr(wrap_phi(out[good], r_out), r_out).max() <= to
 
@@ -294,7 +315,8 @@ def test_seed_states_decode_end_to_end(tf, name):
     W, blob = _weights(tf, w)
     hb = ts.make_readout_weights(w)
     mode = tf.MODE_FOR_WEIGHTS[w.dtype]
-    R = tf.Readout(hb, w.d_model, mode)
+    d, nh = ts.readout_dims(w)
+    R = tf.Readout(hb, d, nh, mode)
     hits, offs = ts.make_tracks(w, n_tracks=1500)
     h = torch.from_numpy(hits).cuda()
     o = torch.from_numpy(offs).cuda()
@@ -303,10 +325,10 @@ def test_seed_states_decode_end_to_end(tf, name):
     out, q = tf.decode_tracks(states, seeds, R, quantiles=True)
     torch.cuda.synchronize()
     r_seeds, _, _ = oracle.seed_tracks(hits, offs, w.b_field, features=False)
-    r_q, r_out = oracle.readout_tracks(_ref_states(w, hits, offs, blob), r_seeds, hb, w.d_model)
+    r_q, r_out = oracle.readout_tracks(_ref_states(w, hits, offs, blob), r_seeds, hb, d, nh)
     eq = colerr(q.cpu().numpy(), r_q)
     eo = colerr(wrap_phi(out.cpu().numpy(), r_out), r_out)
     print(f"[chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
     # the quantiles carry the head's own rounding on top of the encoder's
-    tq, _ = head_tols(mode, w.d_model)
+    tq, _ = head_tols(mode, d, nh)
     assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]
