@@ -36,7 +36,8 @@ typedef enum {
     TF_EINVAL = -1,       /* a host-checkable argument is invalid; nothing was launched */
     TF_ENOMEM = -2,       /* device or host allocation failed (tf_weights_create only) */
     TF_EHIP = -3,         /* a HIP runtime call failed */
-    TF_EUNSUPPORTED = -4  /* valid request the library does not implement (e.g. d_model) */
+    TF_EUNSUPPORTED = -4, /* valid request the library does not implement (e.g. d_model) */
+    TF_ETOOLARGE = -5     /* the request exceeds a fixed capacity of the library (nothing was launched) */
 } tf_status;
 
 typedef enum { TF_FP32 = 0, TF_BF16 = 1, TF_BF16_F16ACT = 2 } tf_dtype;
@@ -367,6 +368,34 @@ size_t tf_mingru_workspace_size(const tf_mingru *h, int64_t n_rows);
 tf_status tf_mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                            const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
                            hipStream_t stream);
+
+/*
+ * tf_mingru_states for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid allocation):
+ * the same kernels and results, with the workspace taken from a fixed
+ * 128 MiB array that the library keeps in device memory, one copy per device,
+ * for the life of the process (looked up once per device in tf_mingru_create,
+ * on the device current there).  The call itself allocates nothing and
+ * never synchronises.
+ *
+ * Arguments as for tf_mingru_states, without the workspace.  The hit array
+ * may have at most tf_mingru_noalloc_max_rows(h) rows (n_hits): offsets then
+ * index it from row 0 up, so every row of the batch fits.
+ * All calls on one device share that device's array and leave their rows in
+ * it; nothing needs clearing between calls (every row a kernel reads was
+ * written earlier in the same call).  Calls that overlap in time on one
+ * device (other streams, other handles, other threads) race on the array and
+ * must be ordered by the caller.
+ * Errors: TF_EINVAL (as tf_mingru_states), TF_ETOOLARGE (n_hits above
+ * tf_mingru_noalloc_max_rows(h); nothing launched), TF_EHIP.
+ */
+tf_status tf_mingru_states_noalloc(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                                   const tf_mingru *h, float *states, hipStream_t stream);
+
+/* Rows of hits tf_mingru_states_noalloc accepts for this handle (0 for NULL):
+ * 128 MiB over the workspace bytes per row (1 KiB per row for d_model 128,
+ * H 192, two layers, 16-bit operands: 131071 rows). */
+int64_t tf_mingru_noalloc_max_rows(const tf_mingru *h);
 
 /* Read (and if clear != 0, reset) the handle's sticky device error word
  * (TF_DEVERR_* bits).  Synchronises stream. */

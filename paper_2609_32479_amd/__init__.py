@@ -19,7 +19,7 @@ __all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libtrackfit.so")
 
-TF_OK, TF_EINVAL, TF_ENOMEM, TF_EHIP, TF_EUNSUPPORTED = 0, -1, -2, -3, -4
+TF_OK, TF_EINVAL, TF_ENOMEM, TF_EHIP, TF_EUNSUPPORTED, TF_ETOOLARGE = 0, -1, -2, -3, -4, -5
 TF_FP32, TF_BF16, TF_BF16_F16ACT = 0, 1, 2
 DTYPES = {"fp32": TF_FP32, "bf16": TF_BF16, "bf16_f16act": TF_BF16_F16ACT}
 # Library mode used for a model whose weights are given in the named type:
@@ -32,7 +32,7 @@ EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_fouri
             "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks", "fit_tracks_states",
             "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks",
             "tf_mingru_blob_size", "tf_mingru_create", "tf_mingru_destroy", "tf_mingru_workspace_size",
-            "tf_mingru_states", "tf_mingru_device_error")
+            "tf_mingru_states", "tf_mingru_device_error", "tf_mingru_states_noalloc", "tf_mingru_noalloc_max_rows")
 
 
 class TrackfitError(RuntimeError):
@@ -100,6 +100,10 @@ def lib():
         L.tf_mingru_workspace_size.argtypes = [vp, ctypes.c_int64]
         L.tf_mingru_states.restype = ctypes.c_int
         L.tf_mingru_states.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, ctypes.c_size_t, vp, vp]
+        L.tf_mingru_states_noalloc.restype = ctypes.c_int
+        L.tf_mingru_states_noalloc.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, vp]
+        L.tf_mingru_noalloc_max_rows.restype = ctypes.c_int64
+        L.tf_mingru_noalloc_max_rows.argtypes = [vp]
         L.tf_mingru_device_error.restype = ctypes.c_int
         L.tf_mingru_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
         L.tf_decode_tracks.restype = ctypes.c_int
@@ -382,6 +386,22 @@ class MinGRU:
         _check(lib().tf_mingru_states(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, self._h,
                                       workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                       out.data_ptr(), _stream_handle(stream)), "tf_mingru_states")
+        return out
+
+    def noalloc_max_rows(self) -> int:
+        return int(lib().tf_mingru_noalloc_max_rows(self._h))
+
+    def states_noalloc(self, hits: torch.Tensor, offsets: torch.Tensor, out: torch.Tensor,
+                       n_tracks: int | None = None, stream=None) -> torch.Tensor:
+        """tf_mingru_states_noalloc: the backbone over a packed batch with the
+        library's fixed device workspace; ``out`` (float32 [N, 2H]) is the
+        caller's, so the call allocates nothing."""
+        n = _batch(hits, offsets, n_tracks, self.n_features or 3)
+        if not (out.is_cuda and out.is_contiguous() and out.dtype == torch.float32 and
+                out.numel() >= n * 2 * self.hidden):
+            raise ValueError(f"out must be a contiguous float32 GPU tensor of at least [{n}, {2 * self.hidden}]")
+        _check(lib().tf_mingru_states_noalloc(hits.data_ptr(), hits.shape[0], offsets.data_ptr(), n, self._h,
+                                              out.data_ptr(), _stream_handle(stream)), "tf_mingru_states_noalloc")
         return out
 
     def device_error(self, stream=None, clear: bool = True) -> int:

@@ -28,6 +28,7 @@
 #include <cmath>
 #include <cstdint>
 #include <cstring>
+#include <mutex>
 #include <new>
 #include <vector>
 
@@ -426,7 +427,41 @@ struct tf_mingru {
     char *dmem = nullptr;             // layer stages, error word
     std::vector<const unsigned char *> stages;  // per layer
     int *err = nullptr;
+    void *scratch = nullptr;          // this device's copy of `scratch` (tf_mingru_states_noalloc)
 };
+
+// Workspace of tf_mingru_states_noalloc: a fixed array in device memory,
+// one copy on every device the library runs on, held until the process ends.
+// In host code `scratch` only names the symbol; its device address (one per
+// device) comes from hipGetSymbolAddress, looked up once per device while
+// that device is current (in tf_mingru_create) and used for every access.
+static constexpr size_t kNoAllocScratchBytes = size_t(128) << 20;
+static __device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mutex;
+void *g_scratch_ptr[kMaxDevices];   // device address of `scratch` per device (null: not looked up yet)
+
+// The current device's address of `scratch`, looked up on first use.
+hipError_t scratch_of_current_device(void **out) {
+    *out = nullptr;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mutex);
+    if (!g_scratch_ptr[dev]) {
+        void *p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return hipSuccess;
+}
+}  // namespace
 
 static size_t front_floats(int d, int nf) {
     return nf > 0 ? 2 * (size_t)nf + (size_t)d * 32 * nf + d : 4 * (size_t)d;
@@ -543,6 +578,12 @@ extern "C" tf_status tf_mingru_create(const tf_mingru_config *cfg, const float *
     }
     for (int l = 0; l < L; ++l) h->stages.push_back(reinterpret_cast<const unsigned char *>(h->dmem + loff[l]));
     h->err = reinterpret_cast<int *>(h->dmem + err_off);
+    if (scratch_of_current_device(&h->scratch) != hipSuccess) {
+        (void)hipFree(h->dmem);
+        tf_weights_destroy(h->front);
+        delete h;
+        return TF_EHIP;
+    }
     *out = h;
     return TF_OK;
 }
@@ -567,12 +608,10 @@ extern "C" size_t tf_mingru_workspace_size(const tf_mingru *h, int64_t n_rows) {
     return row_bytes(h) * (size_t)n_rows + 256;
 }
 
-extern "C" tf_status tf_mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
-                                      const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
-                                      hipStream_t stream) {
-    if (!h || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
-    if (n_tracks == 0) return TF_OK;
-    if (!offsets || !states || !workspace || (!hits && n_hits > 0)) return TF_EINVAL;
+namespace {
+tf_status mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                        const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
+                        hipStream_t stream) {
     const int d = h->cfg.d_model, H = h->cfg.hidden, L = h->cfg.n_layers;
     const size_t eb = h->op == OP_F32 ? 4 : 2;
     // rows of the batch that fit the workspace: X0 [rows][d], then up to two [rows][2H]
@@ -619,6 +658,34 @@ extern "C" tf_status tf_mingru_states(const float *hits, int64_t n_hits, const i
         xin = yout;
     }
     return TF_OK;
+}
+}  // namespace
+
+extern "C" tf_status tf_mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
+                                      const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
+                                      hipStream_t stream) {
+    if (!h || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
+    if (n_tracks == 0) return TF_OK;
+    if (!offsets || !states || !workspace || (!hits && n_hits > 0)) return TF_EINVAL;
+    return mingru_states(hits, n_hits, offsets, n_tracks, h, workspace, workspace_bytes, states, stream);
+}
+
+extern "C" int64_t tf_mingru_noalloc_max_rows(const tf_mingru *h) {
+    if (!h) return 0;
+    return (int64_t)((kNoAllocScratchBytes - 256) / row_bytes(h));
+}
+
+extern "C" tf_status tf_mingru_states_noalloc(const float *hits, int64_t n_hits, const int32_t *offsets,
+                                              int32_t n_tracks, const tf_mingru *h, float *states,
+                                              hipStream_t stream) {
+    if (!h || n_tracks < 0 || n_hits < 0) return TF_EINVAL;
+    if (n_hits > tf_mingru_noalloc_max_rows(h)) return TF_ETOOLARGE;
+    if (n_tracks == 0) return TF_OK;
+    if (!offsets || !states || (!hits && n_hits > 0)) return TF_EINVAL;
+    if (!h->scratch) return TF_EHIP;
+    // every workspace row a kernel reads was written earlier in the same call, so
+    // nothing left in the array by an earlier call needs clearing
+    return mingru_states(hits, n_hits, offsets, n_tracks, h, h->scratch, kNoAllocScratchBytes, states, stream);
 }
 
 extern "C" tf_status tf_mingru_device_error(const tf_mingru *h, hipStream_t stream, int32_t *flags, int clear) {

@@ -1397,6 +1397,7 @@ extern "C" const char *tf_status_string(tf_status s) {
         case TF_ENOMEM: return "out of memory";
         case TF_EHIP: return "HIP runtime error";
         case TF_EUNSUPPORTED: return "unsupported configuration";
+        case TF_ETOOLARGE: return "request exceeds a fixed capacity of the library";
     }
     return "unknown status";
 }
