@@ -116,6 +116,27 @@ __device__ __forceinline__ int slot_to_hit(int s) {
     return SP * g + 16 * n + 4 * i + j;
 }
 
+// Folded slot order of the encoder: stream 0 (lanes 0-31) holds tile rows
+// 0 .. SP-1 in register order, stream 1 (lanes 32-63) holds rows 2 SP-1 down to
+// SP, i.e. register position p of stream 1 is row 2 SP - 1 - p.  An ascending
+// pass over the registers then runs stream 0 forward and stream 1 in reverse,
+// and a descending pass the other two directions; both meet at rows SP - 1 and
+// SP, so one lane swap carries a track across the streams.
+template <int SP>
+__device__ __forceinline__ int slot_to_row(int s) {
+    const int n = s >> 5, i = (s >> 3) & 3, g = (s >> 2) & 1, j = s & 3;
+    const int p = 16 * n + 4 * i + j;
+    return g ? 2 * SP - 1 - p : p;
+}
+
+// The SP row bits of stream 1 (rows SP .. 2 SP - 1 of a row mask) in register
+// order: bit p is row 2 SP - 1 - p.
+template <int SP>
+__device__ __forceinline__ unsigned stream1_bits(unsigned long long rows) {
+    const unsigned hi = unsigned(rows >> SP) & (SP >= 32 ? 0xffffffffu : ((1u << SP) - 1u));
+    return __builtin_bitreverse32(hi) >> (32 - SP);
+}
+
 // Copy of one weight stage from global memory straight into an LDS slot:
 // global_load_lds_dwordx4 moves 16 bytes per lane, 1 KiB per wave
 // instruction, into LDS at M0 + 16 * lane.  Each wave copies the pieces

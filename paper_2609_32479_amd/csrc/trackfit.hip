@@ -85,9 +85,11 @@ struct KCfg {
     // spilled) across tiles.
     static constexpr bool TIGHT = WAVES > 4;
     // wave-private LDS: [f; b] buffer, aliased by the pooling scratch
-    static constexpr int FBS = HALF ? 72 : 65;   // row stride of [f; b] (elements)
+    // [f; b] buffer: fp32 slot-major with a padded row; 16-bit channel-major
+    // (row k = channel k of the chunk's [f; b], CAP slots, swizzled by fb_off)
+    static constexpr int FBS = HALF ? CAP : 65;  // row stride of [f; b] (elements)
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
-    static constexpr int FB_BYTES = CAP * FBS * EB;
+    static constexpr int FB_BYTES = HALF ? (64 * CAP + (HT_ == 1 ? 64 : 0)) * EB : CAP * FBS * EB;
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
     static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 4 * MAXTR * 4;
     static constexpr int EMB_BYTES = D * 16;
@@ -100,6 +102,10 @@ struct KCfg {
     static constexpr int G1_BYTES = G1_FR * FRAG + 64 * 4;  // + bx[32], bg[32]
     static constexpr int G2_BYTES = G2_FR * FRAG + D * 4;   // + bout[D]
     static constexpr int MERGED_STAGE = round_up(round_up(G1_BYTES, 16) + G2_BYTES, kCopyBytes);
+    // PIPE (16-bit, d <= 128): pipelined layers, where chunk c runs its input
+    // projection and then its gate interleaved with the output projection of
+    // chunk c - 1; merged, those two share a stage.
+    static constexpr bool PIPE = HALF && D <= 128;
     static constexpr bool MERGE = RING_BYTES / MERGED_STAGE >= 2;
     static constexpr int STAGE = MERGE ? MERGED_STAGE : round_up(cmax(G1_BYTES, G2_BYTES), kCopyBytes);
     static constexpr int G2_OFF = MERGE ? round_up(G1_BYTES, 16) : 0;  // output projection in its stage
@@ -132,7 +138,7 @@ struct DevParams {
                                  // the Fourier front end: bias [D], lo [16], 1 / (hi - lo) [16]
     const unsigned char *stages; // n_stages x STAGE bytes, in the order the kernel walks them
     int n_layers;
-    int n_stages;                // n_fstages + (MERGE ? 1 : 2) * n_layers * NCH + NH1 + 1
+    int n_stages;                // n_fstages + layer stages + NH1 + 1
     int n_feat;                  // per-hit features of the Fourier front end (0: x, y, z)
     int n_fstages;               // stages of the front end's dense projection
     int kpf;                     // k-steps of that projection per stage
@@ -161,22 +167,74 @@ __device__ __forceinline__ void split_operand(const float *v, typename F::T &hi,
     }
 }
 
-// Positions p and p + 1 (p even) of one lane's scan outputs to the [f; b]
-// buffer (rows = hit slots s and s + 1 of the positions, column col0 + cc).
-template <class C, class E>
+// fp32 [f; b] buffer (slot-major): positions p and p + 1 (p even) of one
+// lane's scan outputs, rows = hit slots s and s + 1, column col0 + cc.
+template <class C>
 __device__ __forceinline__ void store_fb_pair(char *ws, int p, float v0, float v1, int col0, int hh, int cc) {
-    E *fb = reinterpret_cast<E *>(ws) + col0 + cc;
+    float *fb = reinterpret_cast<float *>(ws) + col0 + cc;
     const int s = 32 * (p >> 4) + 8 * ((p >> 2) & 3) + 4 * hh + (p & 3);
-    if constexpr (sizeof(E) == 2) {
-        typedef E e2 __attribute__((ext_vector_type(2)));
-        typedef float f2 __attribute__((ext_vector_type(2)));
-        const e2 pr = __builtin_convertvector((f2){v0, v1}, e2);
-        fb[s * C::FBS] = pr.x;
-        fb[(s + 1) * C::FBS] = pr.y;
+    fb[s * C::FBS] = v0;
+    fb[(s + 1) * C::FBS] = v1;
+}
+
+// 16-bit [f; b] buffer (channel-major): row k (channel k of the chunk's
+// [f; b]) holds the CAP hit slots in 4-slot groups.  A scan lane owns one
+// channel and stores four consecutive slots at once (8 bytes); the output
+// projection reads its operand with the transposing LDS read, which hands each
+// lane 4 channels of one slot from 4 slot-runs loaded by 4 lanes.  A store
+// writes 32 rows at one slot group, a read 4 (2 for 64 slots) consecutive rows
+// across a 32-slot tile; rows that share banks must then differ in the banks
+// of their groups.  32 slots: row k starts 4 (k / 4) elements late (a skew,
+// so a lane's rows and groups are a base plus constants); 64 slots: group g of
+// row k sits at group g ^ swz(k).
+template <class C> __device__ __forceinline__ int fb_row(int k) {
+    return C::HT == 1 ? k * C::CAP + 4 * (k >> 2) : k * C::CAP;
+}
+template <class C> __device__ __forceinline__ int fb_off(int k, int grp) {
+    if constexpr (C::HT == 1)
+        return fb_row<C>(k) + 4 * grp;
+    else
+        return fb_row<C>(k) + 4 * (grp ^ ((((k >> 1) & 1) << 3) | ((k >> 2) & 7)));
+}
+// Positions p0 .. p0 + 3 (p0 a multiple of 4) of one lane's scan outputs,
+// channel col: hit slots 4 grp .. 4 grp + 3.
+template <class C, class E>
+__device__ __forceinline__ void store_fb_quad(char *ws, int p0, float v0, float v1, float v2, float v3, int col,
+                                              int hh) {
+    typedef E e4 __attribute__((ext_vector_type(4)));
+    typedef float f4 __attribute__((ext_vector_type(4)));
+    const int grp = 8 * (p0 >> 4) + 2 * ((p0 >> 2) & 3) + hh;
+    *reinterpret_cast<e4 *>(reinterpret_cast<E *>(ws) + fb_off<C>(col, grp)) =
+        __builtin_convertvector((f4){v0, v1, v2, v3}, e4);
+}
+// The output projection's B operand for 32-slot tile nt and k-step kk: lane
+// (hh, cc) receives channels 16 kk + 8 hh .. + 7 of slot 32 nt + cc.  As a
+// loader it fetches the slot run 32 nt + 16 (cc / 16) + 4 (cc % 4) .. + 3 of
+// channel 16 kk + 8 hh + 4 h + (cc / 4) % 4 for halves h = 0, 1.
+template <class C, class T>
+__device__ __forceinline__ T fb_tr_frag(const char *ws, int nt, int kk, int hh, int cc) {
+    typedef short s4 __attribute__((ext_vector_type(4)));
+    typedef short s8 __attribute__((ext_vector_type(8)));
+    typedef __attribute__((address_space(3))) s4 lds_s4;
+    const short *fb = reinterpret_cast<const short *>(ws);
+    const int grp = 8 * nt + 4 * (cc >> 4) + (cc & 3);
+    const int jj = (cc >> 2) & 3;
+    int o0, o1;
+    if constexpr (C::HT == 1) {
+        // rows 16 kk + 8 hh + 4 h + jj all have k / 4 = 4 kk + 2 hh + h: one
+        // lane base plus constants
+        const int lb = (8 * hh + jj) * C::CAP + 8 * hh + 16 * (cc >> 4) + 4 * (cc & 3);
+        o0 = lb + 16 * kk * C::CAP + 16 * kk + 32 * nt;
+        o1 = o0 + 4 * C::CAP + 4;
     } else {
-        fb[s * C::FBS] = v0;
-        fb[(s + 1) * C::FBS] = v1;
+        const int k0 = 16 * kk + 8 * hh + jj;
+        o0 = fb_off<C>(k0, grp);
+        o1 = fb_off<C>(k0 + 4, grp);
     }
+    const s4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(fb + o0));
+    const s4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_s4 *)(fb + o1));
+    const s8 v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(T, v);
 }
 
 // STATES: instead of the pooled head, write each track's last-layer end states
@@ -244,6 +302,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     // stores may complete out of order with the loads) and leaves the next
     // load to the start of the next tile, after that tile's own loads.
     int q = 0;
+    int errbits = 0;
     auto advance = [&](bool last) {
         if (last)
             wait_vmcnt<0>();
@@ -261,7 +320,6 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     const int g_begin = group_begin(offsets, n_tracks, gw, nw, lane);
     const int g_end = group_begin(offsets, n_tracks, gw + 1, nw, lane);
 
-    int errbits = 0;
     const float qnan = __builtin_nanf("");
 
     // Tiles are packed from a window of the wave's tracks: the first track not
@@ -321,9 +379,13 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_lds(q + C::NSLOT - 1), wid, lane);
 
         // ---- tile metadata: the tile's tracks in window order, on consecutive
-        // tile rows; start/end masks per stream
-        unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0;
-        unsigned st0 = 0, st1 = 0;  // per stream: tile rows that start a track
+        // tile rows; per stream, in register order (slot_to_row), the rows whose
+        // coefficient the ascending pass zeroes (su0: track starts of stream 0,
+        // forward; su1: track ends of stream 1, reverse) and the descending pass
+        // zeroes (sd0: ends of stream 0; sd1: starts of stream 1).  The row after
+        // the last hit counts as a start, so the padding never feeds a track.
+        unsigned su0 = 0, su1 = 0, sd0 = 0, sd1 = 0;
+        unsigned st0 = 0, st1 = 0;  // per stream, in row order: tile rows that start a track
         f32x16 r[MT][HT];  // the residual stream (a wave without a tile keeps zeros)
         if constexpr (C::TIGHT) {
 #pragma unroll
@@ -360,17 +422,17 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 st0 = unsigned(smask) & spm;
                 st1 = unsigned(smask >> SP) & spm;
             }
-            sb0 = unsigned(vstart) & spm;
-            sb1 = unsigned(vstart >> SP) & spm;
-            eb0 = unsigned(emask) & spm;
-            eb1 = unsigned(emask >> SP) & spm;
+            su0 = unsigned(vstart) & spm;
+            su1 = stream1_bits<SP>(emask);
+            sd0 = unsigned(emask) & spm;
+            sd1 = stream1_bits<SP>(vstart);
             wave_lds_sync();  // the track table is written
 
             if constexpr (!FOURIER) {
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
-                const int th = slot_to_hit<SP>(32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31));  // tile row
+                const int th = slot_to_row<SP>(32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31));  // tile row
                 float hx = 0.f, hy = 0.f, hz = 0.f;
                 if (th < n) {
                     // the track holding tile row th, and the row's hit
@@ -398,7 +460,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
                 const int sl = 32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31);
-                const int th = slot_to_hit<SP>(sl);
+                const int th = slot_to_row<SP>(sl);
                 const float *hp = nullptr;
                 if (th < n) {
                     const int j = __builtin_popcountll(smask & ((2ull << th) - 1ull)) - 1;
@@ -581,90 +643,96 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             AX[nt * 16 + q] = a * (ax[nt][q] + bxv);
                             CF[nt * 16 + q] = cf;
                         }
-                    // Forward and reverse scans along this lane's stream, interleaved.  A
-                    // track start (forward) or end (reverse) drops the carried state: its
-                    // coefficient is zeroed in the lanes of that stream.  The masks are
-                    // formed where they are used (the asm hides the loop invariance that
-                    // would otherwise keep all of them in scalar registers).
-                    unsigned ms0 = sb0, ms1 = sb1, me0 = eb0, me1 = eb1;
-                    asm volatile("" : "+s"(ms0), "+s"(ms1), "+s"(me0), "+s"(me1));
-                    float Fs[HT * 16], Bs[HT * 16], CFf[HT * 16], CFb[HT * 16];
-                    {
-                        float f = 0.f, b = 0.f;
+                    // Both scans of Eq. (2) in two passes over the lane's registers, in the
+                    // folded row order (slot_to_row): the ascending pass runs stream 0
+                    // forward and stream 1 in reverse, the descending pass stream 0 in
+                    // reverse and stream 1 forward.  A track start (forward) or end
+                    // (reverse) drops the carried state: its coefficient is zeroed in that
+                    // stream's lanes.  The two passes meet at rows SP - 1 and SP: the
+                    // descending pass starts from the other stream's last ascending state
+                    // (one lane swap), so a track that straddles the streams is scanned in
+                    // one unbroken sequence, exactly as any other.  (The asm hides the
+                    // loop invariance that would otherwise keep every position's mask in
+                    // scalar registers.)
+                    unsigned mu0 = su0, mu1 = su1, md0 = sd0, md1 = sd1;
+                    asm volatile("" : "+s"(mu0), "+s"(mu1), "+s"(md0), "+s"(md1));
+                    constexpr int NP = HT * 16;  // register positions per stream
+                    wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
+                    if constexpr (!LAST) {
+                        // ascending pass: stream 0 forward states to [f], stream 1 reverse
+                        // states to [b]; descending pass the other way round.  Each pair of
+                        // positions goes to the [f; b] buffer as soon as it is final.
+                        float U[NP], Dn[NP];
+                        float u = 0.f;
 #pragma unroll
-                        for (int i = 0; i < SP; ++i) {
-                            const int pb = SP - 1 - i;
-                            CFf[i] = zero_lanes(CF[i], half_mask(ms0, ms1, i));
-                            CFb[pb] = zero_lanes(CF[pb], half_mask(me0, me1, pb));
-                            f = fmaf(CFf[i], f, AX[i]);
-                            b = fmaf(CFb[pb], b, AX[pb]);
-                            Fs[i] = f;
-                            Bs[pb] = b;
-                        }
-                    }
-                    {
-                        // A track may straddle the two streams: both scans run again from the
-                        // true boundary states, the end of stream 0 (forward, into stream 1)
-                        // and the start of stream 1 (reverse, into stream 0); the outer
-                        // boundaries keep their zero state.  With the zeroed coefficients
-                        // this reproduces every other position exactly, so the result is
-                        // that of one unsplit scan (and a tile without a straddling track
-                        // gets its first pass back).  One lane swap brings both states
-                        // across.
-                        // Each pair of positions goes to the [f; b] buffer as soon as it is
-                        // final, which keeps few scan outputs live.
-                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(Bs[0]),
-                                                                         __float_as_uint(Fs[SP - 1]), false, false);
-                        float f = hh ? __uint_as_float(xs[0]) : 0.f;  // Fs[SP - 1] of stream 0
-                        float b = hh ? 0.f : __uint_as_float(xs[1]);  // Bs[0] of stream 1
-                        wave_lds_sync();  // the previous chunk's reads of the [f; b] buffer are done
-                        if constexpr (!LAST) {
-#pragma unroll
-                            for (int i = 0; i < SP; ++i) {
-                                const int pb = SP - 1 - i;
-                                f = fmaf(CFf[i], f, AX[i]);
-                                b = fmaf(CFb[pb], b, AX[pb]);
-                                Fs[i] = f;
-                                Bs[pb] = b;
-                                if (i & 1) {
-                                    store_fb_pair<C, FE>(ws, i - 1, Fs[i - 1], Fs[i], 0, hh, cc);
-                                    store_fb_pair<C, FE>(ws, pb, Bs[pb], Bs[pb + 1], 32, hh, cc);
-                                }
+                        for (int i = 0; i < NP; ++i) {
+                            u = fmaf(zero_lanes(CF[i], half_mask(mu0, mu1, i)), u, AX[i]);
+                            U[i] = u;
+                            if constexpr (C::HALF) {
+                                if ((i & 3) == 3)
+                                    store_fb_quad<C, FE>(ws, i - 3, U[i - 3], U[i - 2], U[i - 1], U[i], 32 * hh + cc, hh);
+                            } else if (i & 1) {
+                                store_fb_pair<C>(ws, i - 1, U[i - 1], U[i], 32 * hh, hh, cc);
                             }
-                        } else {
-                            // Last layer, end states only, in fp32: the forward state at
-                            // a track's last row goes to scratch row j (its index in the
-                            // tile), the reverse state at its first row to row MAXTR + j;
-                            // every other position writes a dummy row.  The track of a
-                            // row is the number of track starts up to it, less one:
-                            // counted up along the forward scan and down along the
-                            // reverse one.
-                            // (the asm keeps the compiler from hoisting every position's
-                            // row out of the chunk loop into registers)
-                            unsigned sw = hh ? st1 : st0;  // this stream's track starts
-                            unsigned ew = hh ? eb1 : eb0;  // and ends
-                            int jf = hh ? __builtin_popcount(st0) - 1 : -1;
-                            int jr = jf + __builtin_popcount(sw);
-                            asm volatile("" : "+v"(sw), "+v"(ew), "+v"(jf), "+v"(jr));
-                            constexpr int DUMMY = CAP * C::STS;  // first pooled row, unused here
+                        }
+                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u),
+                                                                         false, false);
+                        float dn = __uint_as_float(hh ? xs[0] : xs[1]);  // the other stream's last state
 #pragma unroll
-                            for (int i = 0; i < SP; ++i) {
-                                const int pb = SP - 1 - i;
-                                f = fmaf(CFf[i], f, AX[i]);
-                                b = fmaf(CFb[pb], b, AX[pb]);
-                                const unsigned si = (sw >> i) & 1u, ei = (ew >> i) & 1u, sr = (sw >> pb) & 1u;
-                                jf += int(si);
-                                // (selects written as products, which stay branch-free)
-                                stage[DUMMY + cc + int(ei) * (jf * C::STS - DUMMY)] = f;
-                                stage[DUMMY + cc + int(sr) * ((MAXTR + jr) * C::STS - DUMMY)] = b;
-                                jr -= int(sr);
+                        for (int i = NP - 1; i >= 0; --i) {
+                            dn = fmaf(zero_lanes(CF[i], half_mask(md0, md1, i)), dn, AX[i]);
+                            Dn[i] = dn;
+                            if constexpr (C::HALF) {
+                                if ((i & 3) == 0)
+                                    store_fb_quad<C, FE>(ws, i, Dn[i], Dn[i + 1], Dn[i + 2], Dn[i + 3], 32 - 32 * hh + cc,
+                                                         hh);
+                            } else if (!(i & 1)) {
+                                store_fb_pair<C>(ws, i, Dn[i], Dn[i + 1], 32 - 32 * hh, hh, cc);
+                            }
+                        }
+                    } else {
+                        // Last layer, end states only, in fp32: the forward state at a
+                        // track's last row goes to scratch row j (its index in the tile),
+                        // the reverse state at its first row to row MAXTR + j; every other
+                        // position writes a dummy row.  The track of a row is counted
+                        // along each pass from the starts it crosses: per lane, cnt marks
+                        // the starts in register order, put the positions to keep, jc the
+                        // running track index (stepped by dj at each start before the
+                        // position is stored) and base the scratch row of track 0.
+                        // (The asm keeps the compiler from hoisting every position's row
+                        // out of the chunk loop into registers.)
+                        const unsigned s1 = stream1_bits<SP>((unsigned long long)st1 << SP);  // stream 1 starts
+                        const unsigned e0 = sd0, e1 = su1;                                    // ends, per stream
+                        constexpr int DUMMY = CAP * C::STS;  // first pooled row, unused here
+                        auto pass = [&](float st, unsigned cnt, unsigned put, int dj, int jc, int base, bool up,
+                                        unsigned m0, unsigned m1) -> float {
+                            asm volatile("" : "+v"(cnt), "+v"(put), "+v"(dj), "+v"(jc), "+v"(base));
+#pragma unroll
+                            for (int ii = 0; ii < NP; ++ii) {
+                                const int i = up ? ii : NP - 1 - ii;
+                                st = fmaf(zero_lanes(CF[i], half_mask(m0, m1, i)), st, AX[i]);
+                                jc += dj * int((cnt >> i) & 1u);
+                                // (select written as a product, which stays branch-free)
+                                stage[DUMMY + cc + int((put >> i) & 1u) * ((base + jc) * C::STS - DUMMY)] = st;
                                 __builtin_amdgcn_sched_barrier(0);  // one position at a time
                             }
-                            wave_lds_sync();
-                            // rows of the tile's tracks out, f in the low lane half, b in the high
-                            for (int j = 0; j < k; ++j)
-                                out[(size_t)t_id[j] * OUTW + hh * D + 32 * ch + cc] = stage[(hh * MAXTR + j) * C::STS + cc];
-                        }
+                            return st;
+                        };
+                        const int n0 = __builtin_popcount(st0);  // tracks that start in stream 0
+                        // ascending: stream 0 forward (ends kept, rows j), stream 1 reverse
+                        // (starts kept, rows MAXTR + j, counted down from k)
+                        const float u = pass(0.f, hh ? s1 : st0, hh ? s1 : e0, hh ? -1 : 1, hh ? k : -1,
+                                             hh ? MAXTR : 0, true, mu0, mu1);
+                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u),
+                                                                         false, false);
+                        // descending: stream 0 reverse (starts kept, counted down from n0),
+                        // stream 1 forward (ends kept, counted up from n0 - 1)
+                        (void)pass(__uint_as_float(hh ? xs[0] : xs[1]), hh ? s1 : st0, hh ? e1 : st0, hh ? 1 : -1,
+                                   hh ? n0 - 1 : n0, hh ? 0 : MAXTR, false, md0, md1);
+                        wave_lds_sync();
+                        // rows of the tile's tracks out, f in the low lane half, b in the high
+                        for (int j = 0; j < k; ++j)
+                            out[(size_t)t_id[j] * OUTW + hh * D + 32 * ch + cc] = stage[(hh * MAXTR + j) * C::STS + cc];
                     }
                 }
                 if constexpr (!C::MERGE) advance(false);
@@ -691,8 +759,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         FT bfr[HT];
 #pragma unroll
                         for (int nt = 0; nt < HT; ++nt) {
-                            const FE *fb = reinterpret_cast<const FE *>(ws);
-                            bfr[nt] = *reinterpret_cast<const FT *>(fb + (32 * nt + cc) * C::FBS + kk * K + hh * KL);
+                            if constexpr (C::HALF) {
+                                bfr[nt] = fb_tr_frag<C, FT>(ws, nt, kk, hh, cc);
+                            } else {
+                                const float *fb = reinterpret_cast<const float *>(ws);
+                                bfr[nt] = fb[(32 * nt + cc) * C::FBS + kk * K + hh * KL];
+                            }
                         }
 #pragma unroll
                         for (int m = 0; m < MT; ++m) {
@@ -728,7 +800,336 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 advance(false);
             }
         };
-        if constexpr (STATES) {
+
+        // ---- pipelined layers (PIPE).  Chunk ch runs its input projection, then its
+        // gate interleaved with the output projection of chunk ch - 1, then its
+        // scans: the output projection reads the [f; b] buffer before this chunk's
+        // scans refill it, and its products go straight into the residual
+        // registers.  A layer's last output projection runs at the start of the next
+        // layer (before its norm) or after the last layer.  Merged, the stage of
+        // IN(ch) also holds the output projection that runs with it (one barrier
+        // per chunk); unmerged, the stages are IN(0), IN(1), OUT(0), IN(2), OUT(1),
+        // ..., OUT(NCH - 1).
+        // out_proj: r += W_out [f; b] of the chunk in the wave's buffer (fragments
+        // at g2), plus b_out when the chunk is the layer's last.  The fp32 model sums
+        // a chunk in fresh accumulators and adds it once (to keep within 1e-5).
+        auto out_frag = [&](const char *g2, int m, int kk) -> FT {
+            return reinterpret_cast<const FT *>(g2)[(m * KS2 + kk) * 64 + lane];
+        };
+        auto fb_frag = [&](int nt, int kk) -> FT {
+            if constexpr (C::HALF) {
+                return fb_tr_frag<C, FT>(ws, nt, kk, hh, cc);
+            } else {
+                const float *fb = reinterpret_cast<const float *>(ws);
+                return fb[(32 * nt + cc) * C::FBS + kk * K + hh * KL];
+            }
+        };
+        auto out_bias = [&](const char *g2) {
+            const float *bo = reinterpret_cast<const float *>(g2 + C::G2_FR * C::FRAG);
+#pragma unroll
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int q = 0; q < 16; ++q) {
+                    const float bv = bo[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) r[m][nt][q] += bv;
+                }
+        };
+        auto out_proj = [&](const char *g2) {
+            f32x16 part[C::HALF ? 1 : MT][HT];
+            if constexpr (!C::HALF) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
+            }
+#pragma unroll
+            for (int kk = 0; kk < KS2; ++kk) {
+                FT bfr[HT];
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt) bfr[nt] = fb_frag(nt, kk);
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    const FT a = out_frag(g2, m, kk);
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) {
+                        if constexpr (C::HALF)
+                            r[m][nt] = F::mma(a, bfr[nt], r[m][nt]);
+                        else
+                            part[m][nt] = F::mma(a, bfr[nt], part[m][nt]);
+                    }
+                }
+            }
+            if constexpr (!C::HALF) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int nt = 0; nt < HT; ++nt) r[m][nt] += part[m][nt];
+            }
+        };
+        auto layer_p = [&](auto last_c, bool prev_out) {
+            constexpr bool LAST = decltype(last_c)::value;
+            if (prev_out) {
+                // the previous layer's last output projection (merged: in the stage
+                // of this layer's first input projection)
+                if (work) {
+                    wave_lds_sync();  // this wave's [f; b] stores are visible
+                    __builtin_amdgcn_s_setprio(1);
+                    out_proj(slot() + C::G2_OFF);
+                    __builtin_amdgcn_s_setprio(0);
+                    out_bias(slot() + C::G2_OFF);
+                }
+                if constexpr (!C::MERGE) advance(false);
+            }
+            FT yf[HT][KS1];
+            if constexpr (C::TIGHT) {
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) yf[nt][ks] = FT{};
+            }
+            if (work) {
+                // RMSNorm: each lane holds half the channels of hit slot 32 nt + cc
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt) {
+                    float ss = 0.f;
+#pragma unroll
+                    for (int m = 0; m < MT; ++m)
+#pragma unroll
+                        for (int q = 0; q < 16; ++q) ss = fmaf(r[m][nt][q], r[m][nt][q], ss);
+                    ss += __shfl_xor(ss, 32);
+                    float rs;
+                    if constexpr (C::HALF)
+                        rs = rsqrtf(ss * (1.0f / D) + kRmsEps);
+                    else
+                        rs = 1.0f / sqrtf(ss * (1.0f / D) + kRmsEps);
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        float v[8];
+#pragma unroll
+                        for (int u = 0; u < KL; ++u) v[u] = r[ks / RPK][nt][(ks % RPK) * KL + u] * rs;
+                        yf[nt][ks] = F::pack(v);
+                    }
+                }
+            }
+            auto chunk = [&](auto with_out_c, int ch) {
+                // chunk ch >= 1 also takes the stage of the output projection of chunk
+                // ch - 1 (computed unless this is the end-states layer)
+                constexpr bool HAS_OUT = decltype(with_out_c)::value;
+                constexpr bool WO = HAS_OUT && !LAST;
+                // candidate and gate pre-activation (zero accumulators cost no moves;
+                // a wave without a tile keeps them)
+                f32x16 ax[HT], gx[HT];
+                float bxv = 0.f, bgv = 0.f;
+#pragma unroll
+                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        ax[nt][q] = 0.f;
+                        gx[nt][q] = 0.f;
+                    }
+                if (work) {
+                    const char *sl = slot();
+                    const FT *wf = reinterpret_cast<const FT *>(sl);
+                    const float *bias = reinterpret_cast<const float *>(sl + C::G1_FR * C::FRAG);
+                    bxv = bias[cc];
+                    bgv = bias[32 + cc];  // -log2(e) b in the 16-bit modes
+                    // input projection: the gate's products first, so that the gate
+                    // arithmetic can start while the candidate's are still running
+                    __builtin_amdgcn_s_setprio(1);
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        const FT bg = wf[(KS1 + ks) * 64 + lane];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) gx[nt] = F::mma(yf[nt][ks], bg, gx[nt]);
+                    }
+#pragma unroll
+                    for (int ks = 0; ks < KS1; ++ks) {
+                        const FT bx = wf[ks * 64 + lane];
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) ax[nt] = F::mma(yf[nt][ks], bx, ax[nt]);
+                    }
+                    __builtin_amdgcn_s_setprio(0);
+                }
+                if constexpr (!C::MERGE) advance(false);  // the input projection's stage is read
+                // gate a = sigmoid(g): the update adds a x and keeps cf = 1 - a of the state
+                float AX[HT * 16], CF[HT * 16];
+                if constexpr (C::TIGHT) {
+#pragma unroll
+                    for (int e = 0; e < HT * 16; ++e) AX[e] = CF[e] = 0.f;
+                }
+                if (work) {
+                    auto gate = [&](int e) {
+                        const float g = gx[e / 16][e % 16];
+                        float a, cf;
+                        if constexpr (C::HALF) {
+                            // hardware exp2 and reciprocal; exp2 of a large argument is inf
+                            // (a = 0, cf = 1) or 0 (a = 1, cf = 0)
+                            const float ex = __builtin_amdgcn_exp2f(fmaf(g, -kLog2e, bgv));
+                            a = __builtin_amdgcn_rcpf(1.0f + ex);
+                            cf = 1.0f - a;
+                        } else {
+                            // library exp and correctly rounded division for the fp32 model
+                            const float ex = expf(-__builtin_amdgcn_fmed3f(g + bgv, -80.0f, 80.0f));
+                            a = 1.0f / (1.0f + ex);
+                            cf = ex * a;
+                        }
+                        AX[e] = a * (ax[e / 16][e % 16] + bxv);
+                        CF[e] = cf;
+                    };
+                    constexpr int NE = HT * 16;  // gate elements per lane
+                    if constexpr (WO) {
+                        // Interleaved with the previous chunk's output projection: step i
+                        // issues product i (kk outer, then m, then nt) and a share of the
+                        // gate elements; each step's operands are read one step ahead.  The
+                        // fence after each step keeps this order (the wave issues in order,
+                        // so a run of products would hold its vector work back).
+                        constexpr int NMF = MT * KS2 * HT;
+                        const char *g2 = slot() + C::G2_OFF;  // the output projection's fragments
+                        f32x16 part[C::HALF ? 1 : MT][HT];
+                        if constexpr (!C::HALF) {
+#pragma unroll
+                            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                                for (int nt = 0; nt < HT; ++nt)
+#pragma unroll
+                                    for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
+                        }
+                        FT bcur[HT], bnxt[HT], acur, anxt;
+                        if constexpr (C::MERGE) wave_lds_sync();  // this wave's [f; b] stores are visible
+#pragma unroll
+                        for (int nt = 0; nt < HT; ++nt) bcur[nt] = fb_frag(nt, 0);
+                        acur = out_frag(g2, 0, 0);
+#pragma unroll
+                        for (int i = 0; i < NMF; ++i) {
+                            const int kk = i / (MT * HT), m = (i / HT) % MT, nt = i % HT;
+                            if (i + 1 < NMF) {
+                                const int kk1 = (i + 1) / (MT * HT), m1 = ((i + 1) / HT) % MT;
+                                anxt = out_frag(g2, m1, kk1);
+                                if (kk1 != kk) {
+#pragma unroll
+                                    for (int t = 0; t < HT; ++t) bnxt[t] = fb_frag(t, kk1);
+                                }
+                            }
+#pragma unroll
+                            for (int e = i * NE / NMF; e < (i + 1) * NE / NMF; ++e) gate(e);
+                            if constexpr (C::HALF)
+                                r[m][nt] = F::mma(acur, bcur[nt], r[m][nt]);
+                            else
+                                part[m][nt] = F::mma(acur, bcur[nt], part[m][nt]);
+                            __builtin_amdgcn_sched_barrier(0);
+                            acur = anxt;
+                            if (i + 1 < NMF && (i + 1) / (MT * HT) != kk) {
+#pragma unroll
+                                for (int t = 0; t < HT; ++t) bcur[t] = bnxt[t];
+                            }
+                        }
+                        if constexpr (!C::HALF) {
+#pragma unroll
+                            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                                for (int nt = 0; nt < HT; ++nt) r[m][nt] += part[m][nt];
+                        }
+                    } else {
+#pragma unroll
+                        for (int e = 0; e < NE; ++e) gate(e);
+                    }
+                }
+                if constexpr (HAS_OUT || C::MERGE) advance(false);  // the stage is read
+                if (work) {
+                    wave_lds_sync();  // the output projection's reads of the [f; b] buffer are done
+                    unsigned mu0 = su0, mu1 = su1, md0 = sd0, md1 = sd1;
+                    asm volatile("" : "+s"(mu0), "+s"(mu1), "+s"(md0), "+s"(md1));
+                    constexpr int NP = HT * 16;  // register positions per stream
+                    if constexpr (!LAST) {
+                        // ascending pass: stream 0 forward states to [f], stream 1 reverse
+                        // states to [b]; descending pass the other way round.  Each pair of
+                        // positions goes to the [f; b] buffer as soon as it is final.
+                        float U[NP], Dn[NP];
+                        float u = 0.f;
+#pragma unroll
+                        for (int i = 0; i < NP; ++i) {
+                            u = fmaf(zero_lanes(CF[i], half_mask(mu0, mu1, i)), u, AX[i]);
+                            U[i] = u;
+                            if constexpr (C::HALF) {
+                                if ((i & 3) == 3)
+                                    store_fb_quad<C, FE>(ws, i - 3, U[i - 3], U[i - 2], U[i - 1], U[i], 32 * hh + cc, hh);
+                            } else if (i & 1) {
+                                store_fb_pair<C>(ws, i - 1, U[i - 1], U[i], 32 * hh, hh, cc);
+                            }
+                        }
+                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u),
+                                                                         false, false);
+                        float dn = __uint_as_float(hh ? xs[0] : xs[1]);  // the other stream's last state
+#pragma unroll
+                        for (int i = NP - 1; i >= 0; --i) {
+                            dn = fmaf(zero_lanes(CF[i], half_mask(md0, md1, i)), dn, AX[i]);
+                            Dn[i] = dn;
+                            if constexpr (C::HALF) {
+                                if ((i & 3) == 0)
+                                    store_fb_quad<C, FE>(ws, i, Dn[i], Dn[i + 1], Dn[i + 2], Dn[i + 3], 32 - 32 * hh + cc,
+                                                         hh);
+                            } else if (!(i & 1)) {
+                                store_fb_pair<C>(ws, i, Dn[i], Dn[i + 1], 32 - 32 * hh, hh, cc);
+                            }
+                        }
+                    } else {
+                        // Last layer, end states only, in fp32: the forward state at a
+                        // track's last row goes to scratch row j (its index in the tile),
+                        // the reverse state at its first row to row MAXTR + j; every other
+                        // position writes a dummy row.  The track of a row is counted
+                        // along each pass from the starts it crosses: per lane, cnt marks
+                        // the starts in register order, put the positions to keep, jc the
+                        // running track index (stepped by dj at each start before the
+                        // position is stored) and base the scratch row of track 0.
+                        // (The asm keeps the compiler from hoisting every position's row
+                        // out of the chunk loop into registers.)
+                        const unsigned s1 = stream1_bits<SP>((unsigned long long)st1 << SP);  // stream 1 starts
+                        const unsigned e0 = sd0, e1 = su1;                                    // ends, per stream
+                        constexpr int DUMMY = CAP * C::STS;  // first pooled row, unused here
+                        auto pass = [&](float st, unsigned cnt, unsigned put, int dj, int jc, int base, bool up,
+                                        unsigned m0, unsigned m1) -> float {
+                            asm volatile("" : "+v"(cnt), "+v"(put), "+v"(dj), "+v"(jc), "+v"(base));
+#pragma unroll
+                            for (int ii = 0; ii < NP; ++ii) {
+                                const int i = up ? ii : NP - 1 - ii;
+                                st = fmaf(zero_lanes(CF[i], half_mask(m0, m1, i)), st, AX[i]);
+                                jc += dj * int((cnt >> i) & 1u);
+                                // (select written as a product, which stays branch-free)
+                                stage[DUMMY + cc + int((put >> i) & 1u) * ((base + jc) * C::STS - DUMMY)] = st;
+                                __builtin_amdgcn_sched_barrier(0);  // one position at a time
+                            }
+                            return st;
+                        };
+                        const int n0 = __builtin_popcount(st0);  // tracks that start in stream 0
+                        // ascending: stream 0 forward (ends kept, rows j), stream 1 reverse
+                        // (starts kept, rows MAXTR + j, counted down from k)
+                        const float u = pass(0.f, hh ? s1 : st0, hh ? s1 : e0, hh ? -1 : 1, hh ? k : -1,
+                                             hh ? MAXTR : 0, true, mu0, mu1);
+                        const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u),
+                                                                         false, false);
+                        // descending: stream 0 reverse (starts kept, counted down from n0),
+                        // stream 1 forward (ends kept, counted up from n0 - 1)
+                        (void)pass(__uint_as_float(hh ? xs[0] : xs[1]), hh ? s1 : st0, hh ? e1 : st0, hh ? 1 : -1,
+                                   hh ? n0 - 1 : n0, hh ? 0 : MAXTR, false, md0, md1);
+                        wave_lds_sync();
+                        // rows of the tile's tracks out, f in the low lane half, b in the high
+                        for (int j = 0; j < k; ++j)
+                            out[(size_t)t_id[j] * OUTW + hh * D + 32 * ch + cc] = stage[(hh * MAXTR + j) * C::STS + cc];
+                    }
+                }
+            };
+            chunk(std::false_type{}, 0);
+            for (int ch = 1; ch < NCH; ++ch) chunk(std::true_type{}, ch);
+        };
+
+        if constexpr (STATES && C::PIPE) {
+            for (int l = 0; l + 1 < P.n_layers; ++l) layer_p(std::false_type{}, l > 0);
+            layer_p(std::true_type{}, P.n_layers > 1);
+            advance(false);  // the last layer's last output projection, which the end states do not need
+        } else if constexpr (STATES) {
             for (int l = 0; l + 1 < P.n_layers; ++l) layer(std::false_type{});
             layer(std::true_type{});
         } else if constexpr (FRONT) {
@@ -740,7 +1141,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 FE *xo = reinterpret_cast<FE *>(out);
 #pragma unroll
                 for (int nt = 0; nt < HT; ++nt) {
-                    const int th = slot_to_hit<SP>(32 * nt + cc);
+                    const int th = slot_to_row<SP>(32 * nt + cc);
                     if (th < n) {
                         // the track of tile row th: the number of track starts up to it, less one
                         const int j = (th < SP ? __builtin_popcount(st0 & ((2u << th) - 1u))
@@ -762,6 +1163,19 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         }
                     }
                 }
+            }
+        } else if constexpr (C::PIPE) {
+            for (int l = 0; l < P.n_layers; ++l) layer_p(std::false_type{}, l > 0);
+            if (P.n_layers > 0) {
+                // the last layer's last output projection
+                if (work) {
+                    wave_lds_sync();  // this wave's [f; b] stores are visible
+                    __builtin_amdgcn_s_setprio(1);
+                    out_proj(slot() + C::G2_OFF);
+                    __builtin_amdgcn_s_setprio(0);
+                    out_bias(slot() + C::G2_OFF);
+                }
+                advance(false);
             }
         } else {
             for (int l = 0; l < P.n_layers; ++l) layer(std::false_type{});
@@ -798,7 +1212,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         wave_lds_sync();
 #pragma unroll
                         for (int nt = 0; nt < HT; ++nt) {
-                            const int th = slot_to_hit<SP>(32 * nt + cc);
+                            const int th = slot_to_row<SP>(32 * nt + cc);
 #pragma unroll
                             for (int q = 0; q < 16; ++q)
                                 stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
@@ -994,12 +1408,12 @@ struct StageWriter {
 
 // Stage geometry of one instance, for the host.
 struct Geom {
-    int stage, ksps, nh1, merge, g2_off, head16;
+    int stage, ksps, nh1, merge, g2_off, head16, pipe;
 };
 template <int D, int OP, int HT>
 Geom geom() {
     using C = KCfg<D, OP, HT>;
-    return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF, C::HEAD16 ? 1 : 0};
+    return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF, C::HEAD16 ? 1 : 0, C::PIPE ? 1 : 0};
 }
 template <int D, int OP>
 Geom geom_ht(int ht) {
@@ -1089,7 +1503,23 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
     const int KF = NFEAT ? (int)(KF32 / K) : 0;
     const int KPF = NFEAT ? std::min(KF, G.stage / (MT * frag_bytes)) : 1;
     const int NFS = NFEAT ? (KF + KPF - 1) / KPF : 0;
-    const int n_stages = NFS + (G.merge ? 1 : 2) * L * NCH + G.nh1 + 1;
+    // Layer stages.  Merged: a chunk's input and output projections share a
+    // stage; otherwise each has a stage of its own, in chunk order.  Pipelined
+    // kernels take them in the order they need them: merged, stage (l, c) holds
+    // the input projection of chunk c of layer l and the output projection of the
+    // chunk before it in walk order (chunk c - 1, or the previous layer's last
+    // chunk), and one stage after the last layer holds that layer's last output
+    // projection; unmerged, per layer IN(0), IN(1), OUT(0), IN(2), OUT(1), ...,
+    // OUT(NCH - 1), the last taken at the start of the next layer.
+    const int n_layer_stages =
+        G.pipe ? (G.merge ? (L > 0 ? L * NCH + 1 : 0) : 2 * L * NCH) : (G.merge ? L * NCH : 2 * L * NCH);
+    auto pipe_in = [&](int l, int c) {
+        return G.merge ? NFS + NCH * l + c : NFS + 2 * NCH * l + (c == 0 ? 0 : 2 * c - 1);
+    };
+    auto pipe_out = [&](int l, int c) {
+        return G.merge ? pipe_in(l, c) + 1 : NFS + 2 * NCH * l + (c < NCH - 1 ? 2 * c + 2 : 2 * NCH - 1);
+    };
+    const int n_stages = NFS + n_layer_stages + G.nh1 + 1;
     const size_t emb_bytes = (size_t)D * 16;
     const size_t emb_off = 0, st_off = (emb_bytes + 255) & ~size_t(255);
     const size_t err_off = st_off + (size_t)n_stages * G.stage;
@@ -1139,7 +1569,8 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
             // input projection B fragments: lane (g, c) value u of k-step ks holds
             // W[out 32 ch + c][in 32 m + 8 i + 4 g + j] * gain[in], with
             // (m, 4 i + j) = (ks / RPK, (ks % RPK) * KL + u); then bx[32], bg[32]
-            StageWriter w{op, hb.data() + st_off + (size_t)s++ * G.stage};
+            const int s_in = G.pipe ? pipe_in(l, ch) : s++;
+            StageWriter w{op, hb.data() + st_off + (size_t)s_in * G.stage};
             for (int part = 0; part < 2; ++part)
                 for (int ks = 0; ks < KS1; ++ks)
                     for (int lane = 0; lane < 64; ++lane)
@@ -1155,9 +1586,9 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
             // output projection A fragments: lane (g, c) value u of k-step kk of
             // block m holds W[out 32 m + c][column of [f; b] channel
             // q = kk K + g KL + u of the chunk]; then bout[D]
-            // (in the stage of the input projection, at g2_off, when stages are merged)
-            StageWriter w2{op, G.merge ? hb.data() + st_off + (size_t)(s - 1) * G.stage + G.g2_off
-                                       : hb.data() + st_off + (size_t)s++ * G.stage};
+            // (merged: at g2_off in the stage of the input projection)
+            const int s_out = G.pipe ? pipe_out(l, ch) : G.merge ? s_in : s++;
+            StageWriter w2{op, hb.data() + st_off + (size_t)s_out * G.stage + G.g2_off};
             for (int m = 0; m < MT; ++m)
                 for (int kk = 0; kk < KS2; ++kk)
                     for (int lane = 0; lane < 64; ++lane)
@@ -1170,6 +1601,7 @@ extern "C" tf_status tf_weights_create(const tf_config *cfg, const float *blob, 
             for (int c = 0; c < D; ++c) w2.f32(bo[c]);
         }
     }
+    if (G.pipe) s = NFS + n_layer_stages;
     if (G.head16) {
         // 16x16x32 head.  Layer 1 A fragments, KSPS / 2 32-channel blocks per
         // stage: lane value u of block bl, unit block ub holds
