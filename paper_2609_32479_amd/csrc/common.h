@@ -145,13 +145,14 @@ __device__ __forceinline__ unsigned stream1_bits(unsigned long long rows) {
 // wait for an older stage with a constant vmcnt.  The instruction is written
 // out because the compiler, which cannot tell the ring slots apart, would
 // otherwise wait for every such load before each LDS access; the kernel keeps
-// the count itself (wait_vmcnt).  The kernel has no other use of M0.
+// the count itself (wait_vmcnt).  The LDS address is an operand bound to M0,
+// so the compiler writes M0 itself and knows it is read here; the s_nop is
+// the one wait state the hardware needs between that write and the load.
 __device__ __forceinline__ void lds_dma16(const void *gsrc, unsigned lds_addr) {
-    // one wait state between the M0 write and its use by the load
-    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+    asm volatile("s_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                  :
-                 : "s"(__builtin_amdgcn_readfirstlane(lds_addr)), "v"(gsrc)
-                 : "memory", "m0");
+                 : "v"(gsrc), "{m0}"(__builtin_amdgcn_readfirstlane(lds_addr))
+                 : "memory");
 }
 
 // slot_lds: LDS byte address of the slot.

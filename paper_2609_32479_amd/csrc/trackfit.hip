@@ -93,7 +93,7 @@ struct KCfg {
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
     static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 4 * MAXTR * 4;
     static constexpr int EMB_BYTES = D * 16;
-    static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES;  // for the stage ring
+    static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES - 16;  // for the stage ring
     // Weight stages, all padded to STAGE bytes.  A chunk's input and output
     // projections share one stage (one barrier per chunk) when two such stages
     // fit in the ring; otherwise each has its own.
@@ -126,7 +126,8 @@ struct KCfg {
     static constexpr int NSLOT = NSLOT_FIT > 4 ? 4 : NSLOT_FIT;
     static_assert(NSLOT >= 2, "stage ring");
     static constexpr int WAVE0 = SLOT0 + NSLOT * STAGE;
-    static constexpr int LDS_BYTES = WAVE0 + WAVES * WAVE_BYTES;
+    static constexpr int FLAG_OFF = WAVE0 + WAVES * WAVE_BYTES;  // the tile flag (see the kernel)
+    static constexpr int LDS_BYTES = FLAG_OFF + 16;
     static_assert(LDS_BYTES <= kLdsBytesMax, "LDS budget");
     static_assert(D % 32 == 0, "d must be a multiple of 32");
     static_assert(KSPS >= KPB && KS1 % KSPS == 0, "head stage split");
@@ -148,6 +149,9 @@ constexpr int kMaxFeat = 16;     // per-hit features of the Fourier front end, a
 // What the encoder kernel writes: the pooled head's five outputs, the last
 // layer's end states, or (with no layers) the front end's output per hit.
 enum { OUT_HEAD = 0, OUT_STATES = 1, OUT_FRONT = 2 };
+// Pipelined layers: bit g set = waves 4 g .. 4 g + 3 take each chunk's stage
+// barrier after the chunk's scans instead of before them.
+constexpr unsigned kLateWaveGroups = 1u;
 constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
 
 // The head multiplies fp32 vectors (pooled stream, hidden layer) by the
@@ -292,6 +296,14 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     auto slot_lds = [&](int q) -> unsigned { return smem_lds + C::SLOT0 + (q % C::NSLOT) * C::STAGE; };
 #pragma unroll
     for (int q = 0; q < C::NSLOT - 1; ++q) copy_stage<C>(P.stages, q % S, slot_lds(q), wid, lane);
+    // The tile flag: at the start of its t-th tile every wave that has a tile
+    // writes t, so the workgroup stops when after the barrier it does not read
+    // t.  (No wave writes t + 1 before every wave has read it: each tile has
+    // barriers of its own.)
+    int *tile_flag = reinterpret_cast<int *>(smem + C::FLAG_OFF);
+    if (threadIdx.x == 0) *tile_flag = 0;
+    lds_barrier();  // the flag and the embedding table are in place
+    int tile_count = 0;
 
     // Stage q (counted across tiles; a tile iteration takes S stages) lives in
     // slot q % NSLOT.  At the end of stage q every wave waits for its share of
@@ -320,7 +332,6 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     const int g_begin = group_begin(offsets, n_tracks, gw, nw, lane);
     const int g_end = group_begin(offsets, n_tracks, gw + 1, nw, lane);
 
-    const float qnan = __builtin_nanf("");
 
     // Tiles are packed from a window of the wave's tracks: the first track not
     // yet fitted (t) and the WIN - 1 after it, in track order; bit i of `taken`
@@ -358,6 +369,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 errbits |= (bad_m ? TF_DEVERR_BAD_OFFSETS : 0) | (empty_m ? TF_DEVERR_EMPTY_TRACK : 0) |
                            (long_m ? TF_DEVERR_TOO_LONG : 0);
                 if (!FRONT && fresh && (bad || empty || too_long)) {
+                    // (a NaN made here, so that the compiler does not keep one across tiles)
+                    float qnan;
+                    asm volatile("v_mov_b32 %0, 0x7fc00000" : "=v"(qnan));
 #pragma unroll
                     for (int e = 0; e < OUTW; ++e) out[(size_t)idx * OUTW + e] = qnan;
                 }
@@ -375,7 +389,10 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         }
         const bool work = k > 0;
         wait_vmcnt<0>();                     // stages q .. q + NSLOT - 2 are in LDS
-        if (!__syncthreads_or(work)) break;  // every wave of the workgroup is done
+        ++tile_count;
+        if (work && lane == 0) *tile_flag = tile_count;
+        lds_barrier();
+        if (uniform(*tile_flag) != tile_count) break;  // every wave of the workgroup is done
         copy_stage<C>(P.stages, (q + C::NSLOT - 1) % S, slot_lds(q + C::NSLOT - 1), wid, lane);
 
         // ---- tile metadata: the tile's tracks in window order, on consecutive
@@ -459,7 +476,8 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             const int nf = P.n_feat;
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
-                const int sl = 32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31);
+                const int ln = C::TIGHT ? fresh_lane() : lane;
+                const int sl = 32 * nt + (ln & 31), h2 = ln >> 5;
                 const int th = slot_to_row<SP>(sl);
                 const float *hp = nullptr;
                 if (th < n) {
@@ -468,13 +486,13 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 }
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const int f = 8 * hh + e;
+                    const int f = 8 * h2 + e;
                     if (f < nf) us[sl * kUStride + f] = hp ? (hp[f] - fe[D + f]) * fe[D + kMaxFeat + f] : 0.f;
                 }
 #pragma unroll
                 for (int m = 0; m < MT; ++m)
 #pragma unroll
-                    for (int q = 0; q < 16; ++q) r[m][nt][q] = fe[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                    for (int q = 0; q < 16; ++q) r[m][nt][q] = fe[32 * m + 8 * (q >> 2) + 4 * h2 + (q & 3)];
             }
             wave_lds_sync();  // the features are in the scratch
             }
@@ -813,24 +831,27 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         // out_proj: r += W_out [f; b] of the chunk in the wave's buffer (fragments
         // at g2), plus b_out when the chunk is the layer's last.  The fp32 model sums
         // a chunk in fresh accumulators and adds it once (to keep within 1e-5).
-        auto out_frag = [&](const char *g2, int m, int kk) -> FT {
-            return reinterpret_cast<const FT *>(g2)[(m * KS2 + kk) * 64 + lane];
+        // (the lane argument: out_proj and out_bias, which run once per layer,
+        // re-derive it (see KCfg::TIGHT))
+        auto out_frag = [&](const char *g2, int m, int kk, int ln) -> FT {
+            return reinterpret_cast<const FT *>(g2)[(m * KS2 + kk) * 64 + ln];
         };
-        auto fb_frag = [&](int nt, int kk) -> FT {
+        auto fb_frag = [&](int nt, int kk, int ln) -> FT {
             if constexpr (C::HALF) {
-                return fb_tr_frag<C, FT>(ws, nt, kk, hh, cc);
+                return fb_tr_frag<C, FT>(ws, nt, kk, ln >> 5, ln & 31);
             } else {
                 const float *fb = reinterpret_cast<const float *>(ws);
-                return fb[(32 * nt + cc) * C::FBS + kk * K + hh * KL];
+                return fb[(32 * nt + (ln & 31)) * C::FBS + kk * K + (ln >> 5) * KL];
             }
         };
         auto out_bias = [&](const char *g2) {
             const float *bo = reinterpret_cast<const float *>(g2 + C::G2_FR * C::FRAG);
+            const int h2 = (C::TIGHT ? fresh_lane() : lane) >> 5;
 #pragma unroll
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int q = 0; q < 16; ++q) {
-                    const float bv = bo[32 * m + 8 * (q >> 2) + 4 * hh + (q & 3)];
+                    const float bv = bo[32 * m + 8 * (q >> 2) + 4 * h2 + (q & 3)];
 #pragma unroll
                     for (int nt = 0; nt < HT; ++nt) r[m][nt][q] += bv;
                 }
@@ -845,14 +866,15 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 #pragma unroll
                         for (int q = 0; q < 16; ++q) part[m][nt][q] = 0.f;
             }
+            const int ln = C::TIGHT ? fresh_lane() : lane;
 #pragma unroll
             for (int kk = 0; kk < KS2; ++kk) {
                 FT bfr[HT];
 #pragma unroll
-                for (int nt = 0; nt < HT; ++nt) bfr[nt] = fb_frag(nt, kk);
+                for (int nt = 0; nt < HT; ++nt) bfr[nt] = fb_frag(nt, kk, ln);
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
-                    const FT a = out_frag(g2, m, kk);
+                    const FT a = out_frag(g2, m, kk, ln);
 #pragma unroll
                     for (int nt = 0; nt < HT; ++nt) {
                         if constexpr (C::HALF)
@@ -1000,17 +1022,17 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         FT bcur[HT], bnxt[HT], acur, anxt;
                         if constexpr (C::MERGE) wave_lds_sync();  // this wave's [f; b] stores are visible
 #pragma unroll
-                        for (int nt = 0; nt < HT; ++nt) bcur[nt] = fb_frag(nt, 0);
-                        acur = out_frag(g2, 0, 0);
+                        for (int nt = 0; nt < HT; ++nt) bcur[nt] = fb_frag(nt, 0, lane);
+                        acur = out_frag(g2, 0, 0, lane);
 #pragma unroll
                         for (int i = 0; i < NMF; ++i) {
                             const int kk = i / (MT * HT), m = (i / HT) % MT, nt = i % HT;
                             if (i + 1 < NMF) {
                                 const int kk1 = (i + 1) / (MT * HT), m1 = ((i + 1) / HT) % MT;
-                                anxt = out_frag(g2, m1, kk1);
+                                anxt = out_frag(g2, m1, kk1, lane);
                                 if (kk1 != kk) {
 #pragma unroll
-                                    for (int t = 0; t < HT; ++t) bnxt[t] = fb_frag(t, kk1);
+                                    for (int t = 0; t < HT; ++t) bnxt[t] = fb_frag(t, kk1, lane);
                                 }
                             }
 #pragma unroll
@@ -1037,7 +1059,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         for (int e = 0; e < NE; ++e) gate(e);
                     }
                 }
-                if constexpr (HAS_OUT || C::MERGE) advance(false);  // the stage is read
+                // the stage is read: the barrier comes before this chunk's scans, or
+                // (late waves) after them
+                const bool late = (kLateWaveGroups >> (wid >> 2)) & 1;
+                if constexpr (HAS_OUT || C::MERGE) {
+                    if (!late) advance(false);
+                }
                 if (work) {
                     wave_lds_sync();  // the output projection's reads of the [f; b] buffer are done
                     unsigned mu0 = su0, mu1 = su1, md0 = sd0, md1 = sd1;
@@ -1120,6 +1147,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             out[(size_t)t_id[j] * OUTW + hh * D + 32 * ch + cc] = stage[(hh * MAXTR + j) * C::STS + cc];
                     }
                 }
+                if constexpr (HAS_OUT || C::MERGE) {
+                    if (late) advance(false);
+                }
             };
             chunk(std::false_type{}, 0);
             for (int ch = 1; ch < NCH; ++ch) chunk(std::true_type{}, ch);
@@ -1190,10 +1220,13 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             f32x4 hq[C::HEAD16 ? C::UB : 1];  // 16x16 head: units 16 ub + 4 hg + i of track hcol
             const int hcol = lane & 15, hg = lane >> 4;
             if constexpr (C::HEAD16) {
+                // a zero made here, so that the compiler does not keep one across tiles
+                float z;
+                asm volatile("v_mov_b32 %0, 0" : "=v"(z));
 #pragma unroll
                 for (int ub = 0; ub < C::UB; ++ub)
 #pragma unroll
-                    for (int i = 0; i < 4; ++i) hq[ub][i] = 0.f;
+                    for (int i = 0; i < 4; ++i) hq[ub][i] = z;
             } else {
 #pragma unroll
                 for (int m = 0; m < MT; ++m)
