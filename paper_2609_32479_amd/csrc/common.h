@@ -238,16 +238,19 @@ __device__ __forceinline__ unsigned pack_tile(unsigned cand, int len, int lane, 
             n += single;
         }
     }
-    // first-fit over the rest
+    // first-fit over the rest, in window order.  A lane passed over once never
+    // fits later (the rows only fill up), so each step takes the lowest remaining
+    // lane whose track fits the rows left: one ballot per track taken.
     int k = __builtin_popcount(sel);
-    for (unsigned c = rest & ~sel; c && k < MAXTR && n < CAP; c &= c - 1u) {
-        const int i = __builtin_ctz(c);
-        const int li = __builtin_amdgcn_readlane(len, i);
-        if (n + li <= CAP) {
-            sel |= 1u << i;
-            n += li;
-            ++k;
-        }
+    unsigned left = rest & ~sel;
+    while (left && k < MAXTR && n < CAP) {
+        const unsigned fit = left & unsigned(__ballot(lane < 32 && len <= CAP - n));
+        if (!fit) break;
+        const int i = __builtin_ctz(fit);
+        n += __builtin_amdgcn_readlane(len, i);
+        sel |= 1u << i;
+        left &= ~(1u << i);
+        ++k;
     }
     rows = n;
     return sel;
