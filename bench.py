@@ -48,23 +48,42 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # only while the SHA-256 of the listed kernel sources, concatenated, is the one
 # recorded and the launch shape is the recorded one; otherwise traffic is null.
 ENCODER_SRCS = ("trackfit.hip", "common.h")
+_ENC_SHA = "d677da28f5a99800ed84b448c38af592bfdadc7807118072e819be93fb0dd131"
 TRAFFIC = {
+    # "profile": the summary in profiles/ that these figures come from (its
+    # trace, counter runs and bench line were taken on one box in one session)
     ("encoder", "deploy_d128x4_bf16_8m"): {
-        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 52855939, "write_bytes": 5546560,
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
+        "fetch_bytes": 53197234, "write_bytes": 5540608,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.326, "valu_busy": 0.545},
-    ("readout", "deploy_d128x4_bf16_8m"): {
-        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 57532379, "write_bytes": 269221888},
+        "mfma_util": 0.374, "valu_busy": 0.592,
+        "profile": "profiles/tf_encoder_kernel_deploy_d128x4_bf16_8m.md"},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
-        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32,
-        "sha256": "67922d7a1419f105cfe050bae617f9bc2459053b617b30bde7e73ba191600bd5", "fetch_bytes": 236664040, "write_bytes": 21588592},
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
+        "fetch_bytes": 233148886, "write_bytes": 9526928, "mfma_util": 0.389, "valu_busy": 0.573,
+        "profile": "profiles/tf_encoder_kernel_fourier15_deploy_d128x4_bf16_8m.md"},
+    ("encoder", "d128x4_fp32_65k"): {
+        "srcs": ENCODER_SRCS, "batch": 65536, "calls_per_step": 1, "sha256": _ENC_SHA,
+        "fetch_bytes": 22523299, "write_bytes": 1386912, "mfma_util": 0.605, "valu_busy": 0.178,
+        "profile": "profiles/tf_encoder_kernel_d128x4_fp32_65k.md"},
+    ("encoder", "d256x6_bf16_1m"): {
+        "srcs": ENCODER_SRCS, "batch": 1048576, "calls_per_step": 1, "sha256": _ENC_SHA,
+        "fetch_bytes": 319348003, "write_bytes": 99491168, "mfma_util": 0.279, "valu_busy": 0.294,
+        "profile": "profiles/tf_encoder_kernel_d256x6_bf16_1m.md"},
+    ("encoder", "long64_d128x4_bf16_200k"): {
+        "srcs": ENCODER_SRCS, "batch": 200000, "calls_per_step": 1, "sha256": _ENC_SHA,
+        "fetch_bytes": 162861812, "write_bytes": 4030080, "mfma_util": 0.235, "valu_busy": 0.441,
+        "profile": "profiles/tf_encoder_kernel_long64_d128x4_bf16_200k.md"},
+    ("readout", "deploy_d128x4_bf16_8m"): {
+        "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
+        "fetch_bytes": 59033168, "write_bytes": 270794752, "mfma_util": 0.327, "valu_busy": 0.606,
+        "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "8ce150acd7e4ca76414fea62ac26e03373d56c05736fdb3d88291b72f1ceb2fb",
-        "fetch_bytes": 264824499 + 996095115 + 3002571931, "write_bytes": 939887920 + 3411865312 + 402653184},
+        "sha256": "b82523572adc3b9c9212a35a4c576833cb94698b7f28e1215c0a456b4b4c405e",
+        "fetch_bytes": 270193641 + 1004644963 + 3010084583, "write_bytes": 940292368 + 3448130272 + 402653184,
+        "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
 
@@ -92,6 +111,26 @@ def traffic_bytes(path, w, batch, calls):
     """Counter-derived HBM bytes per launch, or None."""
     rec = counter_record(path, w, batch, calls)
     return None if rec is None else rec["fetch_bytes"] + rec["write_bytes"]
+
+
+def counter_profile(path, w, batch, calls):
+    """The profiles/ summary the counter figures come from, or None."""
+    rec = counter_record(path, w, batch, calls)
+    return None if rec is None else rec["profile"]
+
+
+def host_cpu():
+    """The host CPU model (as lscpu and /proc/cpuinfo name it) and the threads this process may use."""
+    model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus": os.cpu_count(), "usable_cpus": len(os.sched_getaffinity(0))}
 
 
 def busy_counter(path, w, batch, calls, key):
@@ -286,12 +325,14 @@ def bench_seed(args, w, hits, offs):
                    "b_tesla": w.b_field, "features": True},
         "roofline": {"bound": "hbm", "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s",
                      "frac": gbs / PEAK_HBM_GBS, "traffic": seed_traffic_bytes(w, n_tracks), "kernel": "tf_seed_kernel",
+                     "counters_profile": "profiles/tf_seed_kernel_deploy_8m.md" if seed_traffic_bytes(w, n_tracks) else None,
                      "kernel_avg_ms": ms_per_step, "bytes_per_launch": byts},
         "host_wall_s": wall,
         "device_error_flags": int(flags.item()),
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = seed_cpu_baseline(w, hits, offs, args.cpu_seconds, seeds.cpu().numpy())
+        res["cpu_baseline"]["host_cpu"] = host_cpu()
     if args.copy_calibration:
         copy_calibration(dev)
     print(json.dumps(res), flush=True)
@@ -445,6 +486,9 @@ def bench_readout(args, w, hits, offs, mode, batch):
                    "max_hits": W.max_hits, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": traffic_bytes("readout", w, batch, len(starts)),
+                     "mfma_util_counter": busy_counter("readout", w, batch, len(starts), "mfma_util"),
+                     "valu_busy_counter": busy_counter("readout", w, batch, len(starts), "valu_busy"),
+                     "counters_profile": counter_profile("readout", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel (end states)", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "readout_flops_per_step": readout_algorithmic_flops(*ts.readout_dims(w), n_tracks),
@@ -455,6 +499,7 @@ def bench_readout(args, w, hits, offs, mode, batch):
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = readout_cpu_baseline(w, blob, hb, hits, offs, args.cpu_seconds, args.cpu_threads,
                                                    gpu_out)
+        res["cpu_baseline"]["host_cpu"] = host_cpu()
     if args.copy_calibration:
         copy_calibration(dev)
     print(json.dumps(res), flush=True)
@@ -603,7 +648,9 @@ def bench_paper(args, w, hits, offs, mode, batch):
                    "launches_per_call": 5, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model,
                    "hidden": H, "n_features": w.n_features, "mode": mode, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
-                     "traffic": traffic_bytes("paper", w, batch, len(starts)), "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
+                     "traffic": traffic_bytes("paper", w, batch, len(starts)),
+                     "counters_profile": counter_profile("paper", w, batch, len(starts)),
+                     "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
                      "kernel_avg_ms": call_avg, "flops_per_launch": per_call},
         "context": {"paper_h100_nvl_tracks_per_s": PAPER_H100_TRACKS_PER_S,
                     "ratio_to_paper_h100": value / PAPER_H100_TRACKS_PER_S,
@@ -614,6 +661,7 @@ def bench_paper(args, w, hits, offs, mode, batch):
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = paper_cpu_baseline(w, blob, hb, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
+        res["cpu_baseline"]["host_cpu"] = host_cpu()
     if args.copy_calibration:
         copy_calibration(dev)
     print(json.dumps(res), flush=True)
@@ -770,6 +818,7 @@ def main():
                      "frac": achieved_tflops / peak, "traffic": traffic_bytes("encoder", w, batch, len(starts)),
                      "mfma_util_counter": busy_counter("encoder", w, batch, len(starts), "mfma_util"),
                      "valu_busy_counter": busy_counter("encoder", w, batch, len(starts), "valu_busy"),
+                     "counters_profile": counter_profile("encoder", w, batch, len(starts)),
                      "kernel": "tf_encoder_kernel", "kernel_avg_ms": kernel_ms,
                      "flops_per_launch": per_launch_flops},
         "hbm": {"algorithmic_GBps": bytes_step / (ms_per_step / 1e3) / 1e9, "peak_GBps": PEAK_HBM_GBS,
@@ -779,6 +828,7 @@ def main():
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(w, blob, hits, offs, args.cpu_seconds, args.cpu_threads, gpu_out)
+        res["cpu_baseline"]["host_cpu"] = host_cpu()
     if args.copy_calibration:
         copy_calibration(dev)
     print(json.dumps(res), flush=True)
