@@ -179,6 +179,8 @@ tf_status fit_tracks_states(const float *hits, int64_t n_hits, const int32_t *of
 #define TF_DEVERR_EMPTY_TRACK 1   /* a track with zero hits */
 #define TF_DEVERR_TOO_LONG 2      /* a track longer than tf_max_hits */
 #define TF_DEVERR_BAD_OFFSETS 4   /* decreasing offsets or rows outside [0, n_hits) */
+#define TF_DEVERR_PAIR 8          /* internal: in a 64-hit launch, a wave gave up waiting for the
+                                     other wave of its tile (the launch's outputs are not valid) */
 
 /* Read (and if clear != 0, reset) the sticky device error word after the work
  * already enqueued on stream.  Synchronises stream.  *flags receives the OR of

@@ -13,7 +13,7 @@ import os
 import torch  # noqa: F401  -- load torch's HIP runtime before the library (one runtime per process)
 
 __all__ = ["LIB_PATH", "Config", "Weights", "fit_tracks", "device_error", "blob_size",
-           "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS",
+           "TF_FP32", "TF_BF16", "TF_BF16_F16ACT", "DTYPES", "MODE_FOR_WEIGHTS", "DEVERR_EMPTY_TRACK", "DEVERR_TOO_LONG", "DEVERR_BAD_OFFSETS", "DEVERR_PAIR",
            "TrackfitError", "lib", "seed_tracks", "fit_tracks_states", "Readout", "decode_tracks",
            "readout_blob_size", "MinGRU", "MinGRUConfig", "SEED_TOO_SHORT", "SEED_NO_CIRCLE", "SEED_BAD_OFFSETS"]
 
@@ -25,7 +25,7 @@ DTYPES = {"fp32": TF_FP32, "bf16": TF_BF16, "bf16_f16act": TF_BF16_F16ACT}
 # Library mode used for a model whose weights are given in the named type:
 # bf16 weights run with fp16 activation operands (see include/trackfit.h).
 MODE_FOR_WEIGHTS = {"fp32": "fp32", "bf16": "bf16_f16act"}
-DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS = 1, 2, 4
+DEVERR_EMPTY_TRACK, DEVERR_TOO_LONG, DEVERR_BAD_OFFSETS, DEVERR_PAIR = 1, 2, 4, 8
 SEED_TOO_SHORT, SEED_NO_CIRCLE, SEED_BAD_OFFSETS = 1, 2, 4
 
 EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_fourier_blob_size", "tf_max_hits",

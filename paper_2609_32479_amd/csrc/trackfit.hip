@@ -60,13 +60,18 @@ namespace {
 // ---------------------------------------------------------------------------
 // Compile-time shape of one kernel instance.
 // ---------------------------------------------------------------------------
-template <int D, int OP, int HT_>
+template <int D, int OP, int HT_, bool PAIR_ = false>
 struct KCfg {
     static constexpr bool HALF = OP != OP_F32;
     static constexpr int HT = HT_;               // 32-hit tiles per wave tile
     static constexpr int CAP = 32 * HT;          // hit slots per wave tile
     static constexpr int SP = 16 * HT;           // positions per stream (2 streams)
-    static constexpr int MAXTR = 16 * HT;        // tracks per wave tile
+    static constexpr int MAXTR = 16 * HT;        // tracks per wave tile (of its head)
+    // PAIR: two waves hold one 64-row tile of up to 32 tracks between them (see
+    // tile_row); each runs the head of 16 of its tracks
+    static constexpr bool PAIR = PAIR_;
+    static constexpr int TCAP = PAIR ? 64 : CAP;      // rows of a tile
+    static constexpr int TMAXTR = PAIR ? 32 : MAXTR;  // tracks of a tile
     static constexpr int MT = D / 32;            // 32-channel blocks
     static constexpr int NCH = D / 32;           // chunks of the scan / output projection
     static constexpr int K = HALF ? 16 : 2;      // MFMA reduction depth
@@ -91,9 +96,11 @@ struct KCfg {
     static constexpr int STS = 33;               // row stride of the pooling scratch (floats)
     static constexpr int FB_BYTES = HALF ? (64 * CAP + (HT_ == 1 ? 64 : 0)) * EB : CAP * FBS * EB;
     static constexpr int POOL_BYTES = CAP * STS * 4 + MAXTR * STS * 4;
-    static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 4 * MAXTR * 4;
+    static constexpr int WAVE_BYTES = round_up(cmax(FB_BYTES, POOL_BYTES), 16) + 4 * TMAXTR * 4;
     static constexpr int EMB_BYTES = D * 16;
-    static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES - 16;  // for the stage ring
+    // PAIR: per wave pair, the two scan hand-over rows (64 floats each) and their flags
+    static constexpr int PX_BYTES = PAIR ? (WAVES / 2) * (2 * 64 * 4 + 16) : 0;
+    static constexpr int RING_BYTES = kLdsBytesMax - EMB_BYTES - WAVES * WAVE_BYTES - 16 - PX_BYTES;  // for the stage ring
     // Weight stages, all padded to STAGE bytes.  A chunk's input and output
     // projections share one stage (one barrier per chunk) when two such stages
     // fit in the ring; otherwise each has its own.
@@ -127,7 +134,9 @@ struct KCfg {
     static_assert(NSLOT >= 2, "stage ring");
     static constexpr int WAVE0 = SLOT0 + NSLOT * STAGE;
     static constexpr int FLAG_OFF = WAVE0 + WAVES * WAVE_BYTES;  // the tile flag (see the kernel)
-    static constexpr int LDS_BYTES = FLAG_OFF + 16;
+    static constexpr int PX_OFF = FLAG_OFF + 16;
+    static constexpr int LDS_BYTES = PX_OFF + PX_BYTES;
+    static_assert(!PAIR || (HT == 1 && PIPE && MERGE && HEAD16 && WAVES % 2 == 0), "paired tiles");
     static_assert(LDS_BYTES <= kLdsBytesMax, "LDS budget");
     static_assert(D % 32 == 0, "d must be a multiple of 32");
     static_assert(KSPS >= KPB && KS1 % KSPS == 0, "head stage split");
@@ -152,6 +161,9 @@ enum { OUT_HEAD = 0, OUT_STATES = 1, OUT_FRONT = 2 };
 // Pipelined layers: bit g set = waves 4 g .. 4 g + 3 take each chunk's stage
 // barrier after the chunk's scans instead of before them.
 constexpr unsigned kLateWaveGroups = 1u;
+// Polls of a paired wave's flag before it gives up (far beyond any real wait:
+// each poll is an LDS read and a short sleep).
+constexpr int kPairSpinLimit = 1 << 20;
 constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
 
 // The head multiplies fp32 vectors (pooled stream, hidden layer) by the
@@ -241,6 +253,30 @@ __device__ __forceinline__ T fb_tr_frag(const char *ws, int nt, int kk, int hh, 
     return __builtin_bit_cast(T, v);
 }
 
+// Tile row of hit slot s (the wave's MFMA column order).  A wave tile holds
+// its 32 rows in the folded order of slot_to_row.  A paired tile (64 rows)
+// folds over both waves: wave 0 of the pair holds rows 0..15 (stream 0) and
+// 63..48 (stream 1), wave 1 rows 16..31 and 47..32, so that each scan runs
+// along a stream of wave 0, then one of wave 1, then the other stream of
+// each in turn (the hand-over states pass through LDS).
+template <class C> __device__ __forceinline__ int tile_row(int s, int pb) {
+    if constexpr (C::PAIR) {
+        const int p = 4 * ((s >> 3) & 3) + (s & 3);
+        return ((s >> 2) & 1) ? (pb ? 47 : 63) - p : (pb ? 16 : 0) + p;
+    } else {
+        (void)pb;
+        return slot_to_row<C::SP>(s);
+    }
+}
+// A 64-bit tile-row mask as two 16-bit stream masks of wave pb of a pair, in
+// register order: stream 0 rows base0 + p, stream 1 rows base1 - p.
+__device__ __forceinline__ unsigned pair_s0(unsigned long long rows, int pb) {
+    return unsigned(rows >> (pb ? 16 : 0)) & 0xffffu;
+}
+__device__ __forceinline__ unsigned pair_s1(unsigned long long rows, int pb) {
+    return __builtin_bitreverse32(unsigned(rows >> (pb ? 32 : 48)) & 0xffffu) >> 16;
+}
+
 // STATES: instead of the pooled head, write each track's last-layer end states
 // (the paper's own readout input): out is then [n_tracks][2d], the forward
 // state at the track's last hit in columns 0..d-1 and the reverse state at its
@@ -255,20 +291,22 @@ __device__ __forceinline__ T fb_tr_frag(const char *ws, int nt, int kk, int hh, 
 // to d on the matrix cores (the projection's weights stream through the stage
 // ring ahead of the first layer's).  Column k of that projection is feature
 // k / 32, cosine if bit 4 of k is set, scale k % 16.
-template <int D, int OP, int HT_, int OUTM, bool FOURIER>
-__global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_>::WAVES, 64 * KCfg<D, OP, HT_>::WAVES),
-                          amdgpu_waves_per_eu(KCfg<D, OP, HT_>::WAVES / 4, KCfg<D, OP, HT_>::WAVES / 4)))
+template <int D, int OP, int HT_, int OUTM, bool FOURIER, bool PAIR = false>
+__global__ __attribute__((amdgpu_flat_work_group_size(64 * KCfg<D, OP, HT_, PAIR>::WAVES,
+                                                      64 * KCfg<D, OP, HT_, PAIR>::WAVES),
+                          amdgpu_waves_per_eu(KCfg<D, OP, HT_, PAIR>::WAVES / 4, KCfg<D, OP, HT_, PAIR>::WAVES / 4)))
 void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, const int *__restrict__ offsets,
                        int n_tracks, DevParams P, float *__restrict__ out, long long out_rows, int *__restrict__ err) {
     constexpr bool STATES = OUTM == OUT_STATES;
     constexpr bool FRONT = OUTM == OUT_FRONT;
-    using C = KCfg<D, OP, HT_>;
+    using C = KCfg<D, OP, HT_, PAIR>;
+    static_assert(!PAIR || OUTM == OUT_HEAD, "paired tiles: pooled head only");
     using F = Frag<OP>;
     using FT = typename F::T;
     using FE = typename F::E;
     constexpr int HT = C::HT, CAP = C::CAP, SP = C::SP, MT = C::MT, K = C::K, KL = C::KL;
     constexpr int KS1 = C::KS1, KS2 = C::KS2, RPK = C::RPK, KPB = C::KPB, NCH = C::NCH;
-    constexpr int MAXTR = C::MAXTR;
+    constexpr int MAXTR = C::MAXTR, TMAXTR = C::TMAXTR;
     constexpr int OUTW = STATES ? 2 * D : 5;  // floats per output row (head, states)
 
     __shared__ __attribute__((aligned(16))) char smem[C::LDS_BYTES];
@@ -279,10 +317,25 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     float *stage = reinterpret_cast<float *>(ws);                           // [CAP][STS]
     float *pblk = stage + CAP * C::STS;                                     // [MAXTR][STS]
     // the tile's tracks: first tile row, length, first hit row, track index
-    int *t_start = reinterpret_cast<int *>(ws + C::WAVE_BYTES - 4 * MAXTR * 4);
-    int *t_len = t_start + MAXTR;
-    int *t_off = t_len + MAXTR;
-    int *t_id = t_off + MAXTR;
+    int *t_start = reinterpret_cast<int *>(ws + C::WAVE_BYTES - 4 * TMAXTR * 4);
+    int *t_len = t_start + TMAXTR;
+    int *t_off = t_len + TMAXTR;
+    int *t_id = t_off + TMAXTR;
+    // PAIR: the pairs are waves (w, w + 4) for w < 4, then (8, 9) and (10, 11):
+    // the waves of a workgroup take the SIMDs in turn, so every SIMD holds both
+    // places (a wave that waits for its partner leaves its SIMD to the partner
+    // or to a wave of the other place).  pi: the pair; pb: this wave's place
+    // (0 or 1); pw0: the wave in place 0.  The pair's hand-over rows (xab: place
+    // 0 to 1, xba: back), their flags, and the chunk count the flags carry.
+    static_assert(!C::PAIR || C::WAVES == 12, "pair layout");
+    const int pi = C::PAIR ? (wid < 8 ? (wid & 3) : 4 + ((wid - 8) >> 1)) : 0;
+    const int pb = C::PAIR ? (wid < 8 ? (wid >> 2) : (wid & 1)) : 0;
+    const int pw0 = C::PAIR ? (wid < 8 ? (wid & 3) : (wid & ~1)) : wid;
+    const int pw1 = C::PAIR ? (wid < 8 ? (wid & 3) + 4 : (wid | 1)) : wid;
+    float *xab = reinterpret_cast<float *>(smem + C::PX_OFF + pi * (2 * 64 * 4 + 16));
+    float *xba = xab + 64;
+    int *fab = reinterpret_cast<int *>(xba + 64), *fba = fab + 1;
+    int pseq = 0;
 
     const int hh = lane >> 5;  // lane half
     const int cc = lane & 31;  // lane column
@@ -302,6 +355,13 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
     // barriers of its own.)
     int *tile_flag = reinterpret_cast<int *>(smem + C::FLAG_OFF);
     if (threadIdx.x == 0) *tile_flag = 0;
+    if constexpr (C::PAIR) {
+        if (threadIdx.x < C::WAVES / 2) {
+            int *f = reinterpret_cast<int *>(smem + C::PX_OFF + threadIdx.x * (2 * 64 * 4 + 16) + 2 * 64 * 4);
+            f[0] = 0;
+            f[1] = 0;
+        }
+    }
     lds_barrier();  // the flag and the embedding table are in place
     int tile_count = 0;
 
@@ -325,10 +385,35 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
         ++q;
     };
     auto slot = [&]() -> const char * { return slot_ptr(q); };
+    // PAIR hand-over of scan states: a flag holds the number (pseq) of the chunk
+    // whose row is in place.  A wait gives up after kPairSpinLimit polls
+    // (TF_DEVERR_PAIR), and later waits are skipped, so that a fault here
+    // cannot hang the GPU.
+    bool pair_broken = false;
+    auto pair_give = [&](float *buf, int *flag, float v) {
+        buf[lane] = v;
+        if (lane == 0) __hip_atomic_store(flag, pseq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    };
+    auto pair_take = [&](const float *buf, int *flag) -> float {
+        if (!pair_broken) {
+            for (int spins = 0;; ++spins) {
+                if (uniform(__hip_atomic_load(flag, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP)) == pseq) break;
+                if (spins >= kPairSpinLimit) {
+                    errbits |= TF_DEVERR_PAIR;
+                    pair_broken = true;
+                    break;
+                }
+                __builtin_amdgcn_s_sleep(1);
+            }
+        }
+        return buf[lane];
+    };
 
     // Contiguous group of tracks for this wave, balanced by hit rows.
-    const long long gw = (long long)blockIdx.x * C::WAVES + wid;
-    const long long nw = (long long)gridDim.x * C::WAVES;
+    // (a pair shares one group)
+    constexpr int GPB = C::PAIR ? C::WAVES / 2 : C::WAVES;  // groups per workgroup
+    const long long gw = (long long)blockIdx.x * GPB + (C::PAIR ? pi : wid);
+    const long long nw = (long long)gridDim.x * GPB;
     const int g_begin = group_begin(offsets, n_tracks, gw, nw, lane);
     const int g_end = group_begin(offsets, n_tracks, gw + 1, nw, lane);
 
@@ -361,7 +446,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // before the start, no hits, or more hits than a tile holds
             const bool bad = off < 0 || nxt < off || (long long)nxt > n_hits_total;
             const bool empty = !bad && len == 0;
-            const bool too_long = !bad && len > CAP;
+            const bool too_long = !bad && len > C::TCAP;
             const unsigned long long bad_m = __ballot(fresh && bad);
             const unsigned long long empty_m = __ballot(fresh && empty);
             const unsigned long long long_m = __ballot(fresh && too_long);
@@ -381,7 +466,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // tile than it saves)
             const unsigned cand = unsigned(__ballot(fresh && !bad && !empty && !too_long));
             if (cand) {
-                sel = pack_tile<CAP, MAXTR, false>(cand, len, lane, n);
+                sel = pack_tile<C::TCAP, TMAXTR, false>(cand, len, lane, n);
                 k = __builtin_popcount(sel);
                 taken |= sel;
                 break;
@@ -439,17 +524,24 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 st0 = unsigned(smask) & spm;
                 st1 = unsigned(smask >> SP) & spm;
             }
-            su0 = unsigned(vstart) & spm;
-            su1 = stream1_bits<SP>(emask);
-            sd0 = unsigned(emask) & spm;
-            sd1 = stream1_bits<SP>(vstart);
+            if constexpr (C::PAIR) {
+                su0 = pair_s0(vstart, pb);
+                su1 = pair_s1(emask, pb);
+                sd0 = pair_s0(emask, pb);
+                sd1 = pair_s1(vstart, pb);
+            } else {
+                su0 = unsigned(vstart) & spm;
+                su1 = stream1_bits<SP>(emask);
+                sd0 = unsigned(emask) & spm;
+                sd1 = stream1_bits<SP>(vstart);
+            }
             wave_lds_sync();  // the track table is written
 
             if constexpr (!FOURIER) {
             // embedding: r[m][nt][q] = channel 32 m + 8 (q/4) + 4 hh + (q%4) of hit slot 32 nt + cc
 #pragma unroll
             for (int nt = 0; nt < HT; ++nt) {
-                const int th = slot_to_row<SP>(32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31));  // tile row
+                const int th = tile_row<C>(32 * nt + ((C::TIGHT ? fresh_lane() : lane) & 31), pb);  // tile row
                 float hx = 0.f, hy = 0.f, hz = 0.f;
                 if (th < n) {
                     // the track holding tile row th, and the row's hit
@@ -478,7 +570,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             for (int nt = 0; nt < HT; ++nt) {
                 const int ln = C::TIGHT ? fresh_lane() : lane;
                 const int sl = 32 * nt + (ln & 31), h2 = ln >> 5;
-                const int th = slot_to_row<SP>(sl);
+                const int th = tile_row<C>(sl, pb);
                 const float *hp = nullptr;
                 if (th < n) {
                     const int j = __builtin_popcountll(smask & ((2ull << th) - 1ull)) - 1;
@@ -1061,7 +1153,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 }
                 // the stage is read: the barrier comes before this chunk's scans, or
                 // (late waves) after them
-                const bool late = (kLateWaveGroups >> (wid >> 2)) & 1;
+                const bool late = !C::PAIR && ((kLateWaveGroups >> (wid >> 2)) & 1);
                 if constexpr (HAS_OUT || C::MERGE) {
                     if (!late) advance(false);
                 }
@@ -1074,8 +1166,15 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         // ascending pass: stream 0 forward states to [f], stream 1 reverse
                         // states to [b]; descending pass the other way round.  Each pair of
                         // positions goes to the [f; b] buffer as soon as it is final.
+                        // PAIR: wave 1 starts from wave 0's ascending end states (the states
+                        // at rows 15 and 48), and wave 0's descending pass from wave 1's
+                        // descending end states (rows 16 and 47); each gives its row on.
                         float U[NP], Dn[NP];
                         float u = 0.f;
+                        if constexpr (C::PAIR) {
+                            ++pseq;
+                            if (pb) u = pair_take(xab, fab);
+                        }
 #pragma unroll
                         for (int i = 0; i < NP; ++i) {
                             u = fmaf(zero_lanes(CF[i], half_mask(mu0, mu1, i)), u, AX[i]);
@@ -1090,6 +1189,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         const auto xs = __builtin_amdgcn_permlane32_swap(__float_as_uint(u), __float_as_uint(u),
                                                                          false, false);
                         float dn = __uint_as_float(hh ? xs[0] : xs[1]);  // the other stream's last state
+                        if constexpr (C::PAIR) {
+                            if (!pb) {
+                                pair_give(xab, fab, u);
+                                dn = pair_take(xba, fba);
+                            }
+                        }
 #pragma unroll
                         for (int i = NP - 1; i >= 0; --i) {
                             dn = fmaf(zero_lanes(CF[i], half_mask(md0, md1, i)), dn, AX[i]);
@@ -1101,6 +1206,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             } else if (!(i & 1)) {
                                 store_fb_pair<C>(ws, i, Dn[i], Dn[i + 1], 32 - 32 * hh, hh, cc);
                             }
+                        }
+                        if constexpr (C::PAIR) {
+                            if (pb) pair_give(xba, fba, dn);
                         }
                     } else {
                         // Last layer, end states only, in fp32: the forward state at a
@@ -1237,21 +1345,44 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // unrolled, so that the residual block pooled at each step is a fixed register block
 #pragma unroll
             for (int j = 0; j < C::NH1; ++j) {
-                if (work && OUTM == OUT_HEAD) {
+                // (PAIR: a pair pools the rows of both its waves, so every wave takes
+                // the workgroup barriers between writing and reading them)
+                const bool hw = work && OUTM == OUT_HEAD;
+                if (C::PAIR || hw) {
                     const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
                     for (int bl = 0; bl < C::KSPS / KPB; ++bl) {
                         const int m = j * (C::KSPS / KPB) + bl;  // channel block being pooled
-                        wave_lds_sync();
+                        // tile row th of the block goes to row th % 32 of the pooling
+                        // scratch of wave th / 32 of the pair (PAIR), else of this wave
+                        auto prow_of = [&](int th) -> float * {
+                            if constexpr (C::PAIR)
+                                return reinterpret_cast<float *>(smem + C::WAVE0 + (th < 32 ? pw0 : pw1) * C::WAVE_BYTES) +
+                                       (th & 31) * C::STS;
+                            else
+                                return stage + th * C::STS;
+                        };
+                        if constexpr (C::PAIR)
+                            lds_barrier();
+                        else
+                            wave_lds_sync();
+                        if (hw) {
 #pragma unroll
-                        for (int nt = 0; nt < HT; ++nt) {
-                            const int th = slot_to_row<SP>(32 * nt + cc);
+                            for (int nt = 0; nt < HT; ++nt) {
+                                float *row = prow_of(tile_row<C>(32 * nt + cc, pb));
 #pragma unroll
-                            for (int q = 0; q < 16; ++q)
-                                stage[th * C::STS + 8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
+                                for (int q = 0; q < 16; ++q) row[8 * (q >> 2) + 4 * hh + (q & 3)] = r[m][nt][q];
+                            }
                         }
-                        wave_lds_sync();
-                        for (int tr = hh; tr < k; tr += 2) {
+                        if constexpr (C::PAIR)
+                            lds_barrier();
+                        else
+                            wave_lds_sync();
+                        if (!hw) continue;
+                        // this wave's head tracks: all of the tile's, or (PAIR) 16 pb .. 16 pb + 15
+                        const int tr0 = C::PAIR ? 16 * pb : 0;
+                        const int tr1 = C::PAIR ? (k < tr0 + 16 ? k : tr0 + 16) : k;
+                        for (int tr = tr0 + hh; tr < tr1; tr += 2) {
                             const int s0 = t_start[tr], len = t_len[tr];
                             // in order of u, eight independent reads at a time (rows past the
                             // track's end are read in bounds and not added)
@@ -1259,12 +1390,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             for (int u0 = 0; u0 < len; u0 += 8) {
                                 float v[8];
 #pragma unroll
-                                for (int i = 0; i < 8; ++i) v[i] = stage[(s0 + (u0 + i < len ? u0 + i : len - 1)) * C::STS + cc];
+                                for (int i = 0; i < 8; ++i) v[i] = prow_of(s0 + (u0 + i < len ? u0 + i : len - 1))[cc];
 #pragma unroll
                                 for (int i = 0; i < 8; ++i)
                                     if (u0 + i < len) sum += v[i];
                             }
-                            pblk[tr * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
+                            pblk[(tr - tr0) * C::STS + cc] = sum / (float)len;  // 0 / 0 = NaN for an empty track
                         }
                         wave_lds_sync();
                         if constexpr (C::HEAD16) {
@@ -1298,7 +1429,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         }
                     }
                     if constexpr (C::HEAD16) {
-                      if (j == C::NH1 - 1) {
+                      if (hw && j == C::NH1 - 1) {
                         // bias and SiLU: lane (hg, hcol) holds units 16 ub + 4 hg + i of track hcol
                         const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
@@ -1310,7 +1441,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                                                                       __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
                             }
                       }
-                    } else if (j == C::NH1 - 1) {
+                    } else if (hw && j == C::NH1 - 1) {
                         // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
                         const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
@@ -1353,8 +1484,9 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     o = F::mma16(a, b_hi, o);
                     o = F::mma16(a, b_lo, o);
                 }
-                if (hcol < k) {
-                    float *op = out + (size_t)t_id[hcol] * 5;
+                const int ht = (C::PAIR ? 16 * pb : 0) + hcol;  // the track of column hcol
+                if (ht < k) {
+                    float *op = out + (size_t)t_id[ht] * 5;
                     if (hg == 0) {
                         op[0] = o[0] + b2[0];
                         op[1] = o[1] + b2[1];
@@ -1443,15 +1575,32 @@ struct StageWriter {
 struct Geom {
     int stage, ksps, nh1, merge, g2_off, head16, pipe;
 };
-template <int D, int OP, int HT>
+template <int D, int OP, int HT, bool PAIR = false>
 Geom geom() {
-    using C = KCfg<D, OP, HT>;
+    using C = KCfg<D, OP, HT, PAIR>;
     return {C::STAGE, C::KSPS, C::NH1, C::MERGE ? 1 : 0, C::G2_OFF, C::HEAD16 ? 1 : 0, C::PIPE ? 1 : 0};
+}
+// 64-hit tracks: the 16-bit modes run the pooled head on paired tiles, and the
+// end-states and front-end passes (which have no head) on 64-row wave tiles
+// that walk the same stages.
+template <int D, int OP>
+constexpr bool same_stages() {
+    using A = KCfg<D, OP, 2>;
+    using B = KCfg<D, OP, 1, true>;
+    return A::STAGE == B::STAGE && A::KSPS == B::KSPS && A::NH1 == B::NH1 && A::MERGE == B::MERGE &&
+           A::G2_OFF == B::G2_OFF && A::PIPE == B::PIPE;
 }
 template <int D, int OP>
 Geom geom_ht(int ht) {
     if constexpr (D <= 128) {
-        if (ht == 2) return geom<D, OP, 2>();
+        if (ht == 2) {
+            if constexpr (OP != OP_F32) {
+                static_assert(same_stages<D, OP>(), "64-row and paired tiles walk the same stages");
+                return geom<D, OP, 1, true>();
+            } else {
+                return geom<D, OP, 2>();
+            }
+        }
     }
     return geom<D, OP, 1>();
 }
@@ -1740,10 +1889,10 @@ extern "C" void tf_weights_destroy(tf_weights *w) {
 extern "C" int32_t tf_max_hits(const tf_weights *w) { return w ? w->max_hits : 0; }
 
 namespace {
-template <int D, int OP, int HT, int OUTM, bool FOURIER>
+template <int D, int OP, int HT, int OUTM, bool FOURIER, bool PAIR = false>
 hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                   const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
-    using C = KCfg<D, OP, HT>;
+    using C = KCfg<D, OP, HT, PAIR>;
     // one workgroup per compute unit (the LDS ring and the register file are
     // sized for it), at least 8 tracks per wave
     long long waves = (n_tracks + 7) / 8;
@@ -1751,7 +1900,7 @@ hipError_t launch(const float *hits, int64_t n_hits, const int32_t *offsets, int
     const long long cap = (long long)w->cu_count;
     if (blocks > cap) blocks = cap;
     if (blocks < 1) blocks = 1;
-    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, OUTM, FOURIER>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
+    hipLaunchKernelGGL((tf_encoder_kernel<D, OP, HT, OUTM, FOURIER, PAIR>), dim3((unsigned)blocks), dim3(64 * C::WAVES), 0, stream,
                        hits, (long long)n_hits, offsets, (int)n_tracks, w->params, out, out_rows, w->err);
     return hipGetLastError();
 }
@@ -1760,8 +1909,11 @@ template <int D, int OP, int OUTM, bool FOURIER>
 hipError_t launch_ht(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                      const tf_weights *w, float *out, long long out_rows, hipStream_t stream) {
     if constexpr (D <= 128) {
-        if (w->max_hits == 64)
+        if (w->max_hits == 64) {
+            if constexpr (OP != OP_F32 && OUTM == OUT_HEAD)
+                return launch<D, OP, 1, OUTM, FOURIER, true>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
             return launch<D, OP, 2, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
+        }
     }
     return launch<D, OP, 1, OUTM, FOURIER>(hits, n_hits, offsets, n_tracks, w, out, out_rows, stream);
 }

@@ -190,6 +190,29 @@ def test_determinism_and_neighbour_independence(tf, name, mode):
     assert np.array_equal(c, a[perm])
 
 
+def test_paired_tiles_mixed_lengths(tf):
+    """64-hit mode (two waves share a 64-row tile, the scan states passing
+    between them): lengths 1..64 mixed, parity with the oracle, and a track's
+    result unchanged, bitwise, when the tracks are permuted into other tiles
+    and other positions in them."""
+    w0 = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    W, blob = _weights(tf, w0, max_hits=64)
+    assert W.max_hits == 64
+    w = dataclasses.replace(w0, len_min=1, len_max=64, n_det_layers=64)
+    hits, offs = ts.make_tracks(w, n_tracks=3000)
+    print("[paired] deploy d128x4 lengths 1..64", flush=True)
+    a = _gpu(tf, W, hits, offs)
+    r = _ref(w, hits, offs, blob)
+    assert_parity(a, r, TOL[w.dtype], "paired tiles")
+    perm = np.random.default_rng(1).permutation(offs.size - 1)
+    L = np.diff(offs)
+    hp = np.concatenate([hits[offs[i]:offs[i + 1]] for i in perm])
+    op = np.concatenate([[0], np.cumsum(L[perm])]).astype(np.int32)
+    c = _gpu(tf, W, hp, op)
+    assert np.array_equal(c, a[perm])
+    assert tf.device_error(W) == 0
+
+
 def test_graph_replay_matches_direct(tf):
     w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
     W, blob = _weights(tf, w)
