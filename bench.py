@@ -238,8 +238,8 @@ SEED_SRC = os.path.join(ROOT, "paper_2609_32479_amd", "csrc", "seed.hip")
 # FETCH_SIZE / WRITE_SIZE runs of this script's seed path with --copy-calibration
 # (scaled as for the encoder); valid only for the recorded source.
 SEED_TRAFFIC = {"workload": "deploy_d128x4_bf16_8m", "n_tracks": 8388608,
-                "kernel_sha256": "95e15c248fe9e118aec25f0451b9ee525b1ebbdb58a9f7125625fab4e8e6629f",
-                "fetch_bytes": 2672606279, "write_bytes": 1778368704}
+                "kernel_sha256": "e1a3819882b73f490ea59aa680513cee1e3ad35b038193b373f2bfb5c83660a4",
+                "fetch_bytes": 1460226274, "write_bytes": 1756872480}
 
 
 def seed_algorithmic_bytes(n_hits, n_tracks):
