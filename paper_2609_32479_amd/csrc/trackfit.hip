@@ -167,9 +167,23 @@ constexpr int kPairSpinLimit = 1 << 20;
 constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
 
 // The head multiplies fp32 vectors (pooled stream, hidden layer) by the
-// weights: with 16-bit operands each vector is split into a rounded high part
+// weights: with bf16 operands each vector is split into a rounded high part
 // and the rounded remainder, and both are multiplied (the weights are exact in
-// the operand type), so the head keeps about 16 significant bits.
+// the operand type), so the head keeps about 16 significant bits.  With fp16
+// operands (11 significant bits, as the layers' activations) the 16x16 head
+// takes each vector as one operand.
+template <class F>
+__device__ __forceinline__ void split_operand(const float *v, typename F::T &hi, typename F::T &lo);
+// The 16x16 head's operand: fp16 alone (lo unused), else split.
+template <int OP, class F>
+__device__ __forceinline__ void head_operand(const float *v, typename F::T &hi, typename F::T &lo) {
+    if constexpr (OP == OP_F16) {
+        hi = F::pack(v);
+        lo = hi;
+    } else {
+        split_operand<F>(v, hi, lo);
+    }
+}
 template <class F>
 __device__ __forceinline__ void split_operand(const float *v, typename F::T &hi, typename F::T &lo) {
     hi = F::pack(v);
@@ -1404,12 +1418,12 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
 #pragma unroll
                             for (int u = 0; u < 8; ++u) v[u] = pblk[hcol * C::STS + 8 * hg + u];
                             FT b_hi, b_lo;
-                            split_operand<F>(v, b_hi, b_lo);
+                            head_operand<OP, F>(v, b_hi, b_lo);
 #pragma unroll
                             for (int ub = 0; ub < C::UB; ++ub) {
                                 const FT a = w1[(bl * C::UB + ub) * 64 + lane];
                                 hq[ub] = F::mma16(a, b_hi, hq[ub]);
-                                hq[ub] = F::mma16(a, b_lo, hq[ub]);
+                                if constexpr (OP != OP_F16) hq[ub] = F::mma16(a, b_lo, hq[ub]);
                             }
                         } else {
 #pragma unroll
@@ -1479,10 +1493,10 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         v[4 + i] = hq[2 * kb + 1][i];
                     }
                     FT b_hi, b_lo;
-                    split_operand<F>(v, b_hi, b_lo);
+                    head_operand<OP, F>(v, b_hi, b_lo);
                     const FT a = w2[kb * 64 + lane];
                     o = F::mma16(a, b_hi, o);
-                    o = F::mma16(a, b_lo, o);
+                    if constexpr (OP != OP_F16) o = F::mma16(a, b_lo, o);
                 }
                 const int ht = (C::PAIR ? 16 * pb : 0) + hcol;  // the track of column hcol
                 if (ht < k) {
