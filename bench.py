@@ -48,41 +48,41 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # only while the SHA-256 of the listed kernel sources, concatenated, is the one
 # recorded and the launch shape is the recorded one; otherwise traffic is null.
 ENCODER_SRCS = ("trackfit.hip", "common.h")
-_ENC_SHA = "d677da28f5a99800ed84b448c38af592bfdadc7807118072e819be93fb0dd131"
+_ENC_SHA = "7f692f31995d1214dba91b089b6b0a785afb6a37ab309938858662dd02e7b6b5"
 TRAFFIC = {
     # "profile": the summary in profiles/ that these figures come from (its
     # trace, counter runs and bench line were taken on one box in one session)
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 53197234, "write_bytes": 5540608,
+        "fetch_bytes": 53177587, "write_bytes": 5548224,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.374, "valu_busy": 0.592,
+        "mfma_util": 0.369, "valu_busy": 0.583,
         "profile": "profiles/tf_encoder_kernel_deploy_d128x4_bf16_8m.md"},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 233148886, "write_bytes": 9526928, "mfma_util": 0.389, "valu_busy": 0.573,
+        "fetch_bytes": 233129047, "write_bytes": 9439984, "mfma_util": 0.381, "valu_busy": 0.558,
         "profile": "profiles/tf_encoder_kernel_fourier15_deploy_d128x4_bf16_8m.md"},
     ("encoder", "d128x4_fp32_65k"): {
         "srcs": ENCODER_SRCS, "batch": 65536, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 22523299, "write_bytes": 1386912, "mfma_util": 0.605, "valu_busy": 0.178,
+        "fetch_bytes": 22524835, "write_bytes": 1386592, "mfma_util": 0.603, "valu_busy": 0.177,
         "profile": "profiles/tf_encoder_kernel_d128x4_fp32_65k.md"},
     ("encoder", "d256x6_bf16_1m"): {
         "srcs": ENCODER_SRCS, "batch": 1048576, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 319348003, "write_bytes": 99491168, "mfma_util": 0.279, "valu_busy": 0.294,
+        "fetch_bytes": 320208377, "write_bytes": 99553504, "mfma_util": 0.275, "valu_busy": 0.292,
         "profile": "profiles/tf_encoder_kernel_d256x6_bf16_1m.md"},
     ("encoder", "long64_d128x4_bf16_200k"): {
         "srcs": ENCODER_SRCS, "batch": 200000, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 162861812, "write_bytes": 4030080, "mfma_util": 0.235, "valu_busy": 0.441,
+        "fetch_bytes": 162475143, "write_bytes": 4051552, "mfma_util": 0.293, "valu_busy": 0.547,
         "profile": "profiles/tf_encoder_kernel_long64_d128x4_bf16_200k.md"},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 59033168, "write_bytes": 270794752, "mfma_util": 0.327, "valu_busy": 0.606,
+        "fetch_bytes": 59022801, "write_bytes": 270794752, "mfma_util": 0.327, "valu_busy": 0.603,
         "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "b82523572adc3b9c9212a35a4c576833cb94698b7f28e1215c0a456b4b4c405e",
-        "fetch_bytes": 270193641 + 1004644963 + 3010084583, "write_bytes": 940292368 + 3448130272 + 402653184,
+        "sha256": "b7027a4e3f1f5987567df6a6d20a021c115edc78b2be15ffd5c23f534123a72d",
+        "fetch_bytes": 4281905928, "write_bytes": 4792703472,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
