@@ -254,6 +254,36 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
             }
         }
 
+        // Each block's outputs leave through the wave's LDS tile as 16-byte pieces
+        // (one value per lane and row would be 2- or 4-byte stores), and are
+        // stored only after the barrier that ends the block: the barrier first
+        // waits for this wave's memory operations (the stage copies), and stores
+        // still in flight would hold it up.  Layer outputs: tile row -> input row
+        // (32 rows of 32 channels); end states: the tile's tracks (up to kMgMaxTr
+        // rows of 32 fp32 channels).
+        constexpr int VPP = LAST ? 4 : 16 / (int)sizeof(FE);  // values per 16-byte piece
+        constexpr int PPR = 32 / VPP;                          // pieces per row of 32 channels
+        constexpr int NPEND = (LAST ? kMgMaxTr : 32) * PPR / 64;  // pieces per lane
+        static_assert(NPEND * 64 == (LAST ? kMgMaxTr : 32) * PPR, "pieces");
+        u32x4 pv[NPEND];
+        int prow[NPEND];  // destination row of each piece (-1: none)
+        int pcol = 0;     // first channel of the pieces (uniform)
+#pragma unroll
+        for (int p = 0; p < NPEND; ++p) prow[p] = -1;
+        auto flush = [&]() {
+#pragma unroll
+            for (int p = 0; p < NPEND; ++p) {
+                const int g = (lane + 64 * p) % PPR;
+                if (prow[p] >= 0) {
+                    if constexpr (LAST)
+                        *reinterpret_cast<u32x4 *>(states + (size_t)prow[p] * 2 * H + pcol + g * VPP) = pv[p];
+                    else
+                        *reinterpret_cast<u32x4 *>(Y + (size_t)prow[p] * 2 * H + pcol + g * VPP) = pv[p];
+                }
+                prow[p] = -1;
+            }
+        };
+
         // ---- chunks of 32 hidden channels, forward then reverse direction
         for (int ch = 0; ch < NCHK; ++ch) {
 #pragma unroll
@@ -271,6 +301,7 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                     ax += reinterpret_cast<const float *>(slot() + KIN * C::FRAG)[cc];
                 }
                 if constexpr (!C::MERGE) advance(false);
+                flush();  // the previous block's outputs
                 // the gate block: the next stage, or the second block of this one
                 const char *gsl = slot() + (C::MERGE ? C::BLOCK : 0);
                 if (work) {
@@ -306,10 +337,16 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                         scan_dir<true>(AX, CF, sb0, sb1, hh);
                     else
                         scan_dir<false>(AX, CF, eb0, eb1, hh);
-                    const int col = dir * H + 32 * ch + cc;
+                    pcol = dir * H + 32 * ch;
+                    char *tile = smem + C::WAVE0 + wid * C::WAVE_BYTES + C::TB_OFF;
+                    wave_lds_sync();  // the previous block's reads of the tile are done
                     if constexpr (LAST) {
-                        // forward state at a track's last row, reverse state at its first row;
-                        // the track of a row is the number of track starts up to it, less one
+                        // forward state at a track's last row, reverse state at its first row,
+                        // to row j of the tile (the track's index in it: the number of track
+                        // starts up to the row, less one)
+                        constexpr int ROWF = 32 + 4;  // row stride (floats)
+                        static_assert(kMgMaxTr * ROWF * 4 <= kMgCap * C::ROWB, "end-state rows in the tile");
+                        float *tf = reinterpret_cast<float *>(tile);
                         const unsigned sw = hh ? st1 : st0;
                         const unsigned mw = dir == 0 ? (hh ? eb1 : eb0) : sw;
                         const int jb = hh ? __builtin_popcount(st0) - 1 : -1;
@@ -317,16 +354,18 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                         for (int i = 0; i < SP; ++i)
                             if ((mw >> i) & 1u) {
                                 const int j = jb + __builtin_popcount(sw & ((2u << i) - 1u));
-                                states[(size_t)t_id[j] * 2 * H + col] = AX[i];
+                                tf[j * ROWF + cc] = AX[i];
                             }
+                        wave_lds_sync();
+#pragma unroll
+                        for (int p = 0; p < NPEND; ++p) {
+                            const int it = lane + 64 * p, j = it / PPR, g = it % PPR;
+                            prow[p] = j < k ? t_id[j] : -1;
+                            pv[p] = *reinterpret_cast<const u32x4 *>(tf + j * ROWF + g * VPP);
+                        }
                     } else {
-                        // through the wave's LDS tile, so that each lane stores 16 bytes
-                        // of one row at a time instead of one value per row
                         constexpr int ROWE = C::ROWB / (int)sizeof(FE);  // tile row stride (elements)
-                        constexpr int VPP = 16 / (int)sizeof(FE);        // values per 16-byte piece
-                        constexpr int PPR = 32 / VPP;                    // pieces per row
-                        FE *tb = reinterpret_cast<FE *>(smem + C::WAVE0 + wid * C::WAVE_BYTES + C::TB_OFF);
-                        wave_lds_sync();  // the previous block's reads of the tile are done
+                        FE *tb = reinterpret_cast<FE *>(tile);
 #pragma unroll
                         for (int i = 0; i < SP; ++i) {
                             // the asm keeps the state's last update (rounded to fp32) and its
@@ -340,18 +379,17 @@ void tf_mingru_kernel(const typename Frag<OP>::E *__restrict__ X, long long x_ro
                         }
                         wave_lds_sync();
 #pragma unroll
-                        for (int it = lane; it < 32 * PPR; it += 64) {
-                            const int row = it / PPR, g = it % PPR;
-                            const int yr = rowmap[row];
-                            if (yr >= 0)
-                                *reinterpret_cast<u32x4 *>(Y + (size_t)yr * 2 * H + dir * H + 32 * ch + g * VPP) =
-                                    *reinterpret_cast<const u32x4 *>(tb + row * ROWE + g * VPP);
+                        for (int p = 0; p < NPEND; ++p) {
+                            const int it = lane + 64 * p, row = it / PPR, g = it % PPR;
+                            prow[p] = rowmap[row];
+                            pv[p] = *reinterpret_cast<const u32x4 *>(tb + row * ROWE + g * VPP);
                         }
                     }
                 }
                 advance(ch == NCHK - 1 && dir == 1);
             }
         }
+        flush();  // the tile's last block
     }
     if (errbits && lane == 0) atomicOr(err, errbits);
 }
