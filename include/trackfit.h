@@ -364,12 +364,28 @@ size_t tf_mingru_workspace_size(const tf_mingru *h, int64_t n_rows);
  *           written; tracks with no hits, more than 32 hits or rows outside
  *           [0, n_hits) get NaN rows and set the device error word.
  * Asynchronous, allocates nothing.  One launch for the front end, one per
- * layer, all on stream.  Errors: TF_EINVAL (null pointers with n_tracks > 0,
- * negative sizes), TF_EHIP (launch failure).
+ * layer, all on stream; or, for the paper's deployed configuration (16-bit
+ * modes, Fourier front end, d_model 128, hidden 192, two layers) and unless
+ * tf_mingru_set_fused turned it off, one fused launch that keeps the front
+ * end's output and the first layer's states on chip (same results, bit for
+ * bit; the workspace is then left untouched but still bounds the rows).
+ * Errors: TF_EINVAL (null pointers with n_tracks > 0, negative sizes),
+ * TF_EHIP (launch failure).
  */
 tf_status tf_mingru_states(const float *hits, int64_t n_hits, const int32_t *offsets, int32_t n_tracks,
                            const tf_mingru *h, void *workspace, size_t workspace_bytes, float *states,
                            hipStream_t stream);
+
+/*
+ * Choose how tf_mingru_states and tf_mingru_states_noalloc run the paper's
+ * deployed configuration (Sec. Kernel adaptation: the front end and the token
+ * mixing of the layers fused on chip): fused != 0 one launch (the default
+ * where it applies), 0 the layered launches.  Not to be called while calls
+ * on the handle are in flight.  Errors: TF_EINVAL (NULL handle),
+ * TF_EUNSUPPORTED (fused asked for another configuration; the handle keeps
+ * the layered path).
+ */
+tf_status tf_mingru_set_fused(tf_mingru *h, int fused);
 
 /*
  * tf_mingru_states for callers that cannot allocate device memory (code under

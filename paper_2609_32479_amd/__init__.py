@@ -32,7 +32,8 @@ EXPORTED = ("tf_weights_create", "tf_weights_destroy", "tf_blob_size", "tf_fouri
             "fit_tracks", "tf_get_device_error", "tf_status_string", "tf_seed_tracks", "fit_tracks_states",
             "tf_readout_blob_size", "tf_readout_create", "tf_readout_destroy", "tf_decode_tracks",
             "tf_mingru_blob_size", "tf_mingru_create", "tf_mingru_destroy", "tf_mingru_workspace_size",
-            "tf_mingru_states", "tf_mingru_device_error", "tf_mingru_states_noalloc", "tf_mingru_noalloc_max_rows")
+            "tf_mingru_states", "tf_mingru_device_error", "tf_mingru_states_noalloc", "tf_mingru_noalloc_max_rows",
+            "tf_mingru_set_fused")
 
 
 class TrackfitError(RuntimeError):
@@ -104,6 +105,8 @@ def lib():
         L.tf_mingru_states_noalloc.argtypes = [vp, ctypes.c_int64, vp, ctypes.c_int32, vp, vp, vp]
         L.tf_mingru_noalloc_max_rows.restype = ctypes.c_int64
         L.tf_mingru_noalloc_max_rows.argtypes = [vp]
+        L.tf_mingru_set_fused.restype = ctypes.c_int
+        L.tf_mingru_set_fused.argtypes = [vp, ctypes.c_int]
         L.tf_mingru_device_error.restype = ctypes.c_int
         L.tf_mingru_device_error.argtypes = [vp, vp, ctypes.POINTER(ctypes.c_int32), ctypes.c_int]
         L.tf_decode_tracks.restype = ctypes.c_int
@@ -387,6 +390,11 @@ class MinGRU:
                                       workspace.data_ptr(), workspace.numel() * workspace.element_size(),
                                       out.data_ptr(), _stream_handle(stream)), "tf_mingru_states")
         return out
+
+    def set_fused(self, fused: bool) -> None:
+        """tf_mingru_set_fused: one fused launch (the default for the paper's
+        deployed configuration) or the layered launches."""
+        _check(lib().tf_mingru_set_fused(self._h, int(bool(fused))), "tf_mingru_set_fused")
 
     def noalloc_max_rows(self) -> int:
         return int(lib().tf_mingru_noalloc_max_rows(self._h))

@@ -130,6 +130,53 @@ def test_mingru_tile_independence_and_absolute_offsets(tf):
     assert np.array_equal(g, a[1000:2000])
 
 
+@pytest.mark.parametrize("mode", ["bf16_f16act", "bf16"])
+def test_fused_backbone_matches_layered_launches_bitwise(tf, mode):
+    """The paper's deployed configuration (16-bit, Fourier front end, d = 128,
+    H = 192, two layers) runs as one fused launch by default: its end states
+    and error bits are those of the layered launches, bit for bit, on ragged
+    lengths 1..32, empty and too-long tracks, absolute offsets and a
+    workspace too short for the batch."""
+    w0 = ts.workload("mingru2_h192_fourier15_deploy_bf16_8m")
+    w = dataclasses.replace(w0, len_min=1, len_max=32, n_det_layers=32)
+    blob = ts.make_mingru_weights(w0)
+    M = tf.MinGRU(blob, w.n_layers, w.d_model, w.hidden, mode, w.n_features)
+    inp, offs = _inputs(w, 3000)
+    print(f"[fused] {mode}", flush=True)
+
+    def both(inp, offs, **kw):
+        out = []
+        for fused in (True, False):
+            M.set_fused(fused)
+            out += [_gpu(M, inp, offs, **kw), M.device_error()]
+        M.set_fused(True)
+        return out
+
+    a, ea, b, eb = both(inp, offs)
+    assert np.array_equal(a, b) and ea == eb == 0
+    assert np.isfinite(a).all()
+    a1, ea, b1, eb = both(inp, offs[1000:], n_tracks=1000)
+    assert np.array_equal(a1, b1) and np.array_equal(a1, a[1000:2000]) and ea == eb == 0
+    Lk = np.diff(offs)
+    Lk[3], Lk[7] = 0, 33
+    rows = [np.resize(np.arange(offs[i], offs[i + 1]), Lk[i]) if Lk[i] else np.arange(0) for i in range(3000)]
+    o2 = np.concatenate([[0], np.cumsum(Lk)]).astype(np.int32)
+    a2, ea, b2, eb = both(inp[np.concatenate(rows)], o2)
+    assert np.array_equal(a2, b2, equal_nan=True) and ea == eb == (tf.DEVERR_EMPTY_TRACK | tf.DEVERR_TOO_LONG)
+    assert np.all(np.isnan(a2[[3, 7]]))
+    a3, ea, b3, eb = both(inp, offs, ws_rows=int(offs[200] - offs[0]))
+    assert np.array_equal(a3, b3, equal_nan=True) and ea == eb and ea & tf.DEVERR_BAD_OFFSETS
+    assert np.array_equal(a3[:200], a[:200]) and np.all(np.isnan(a3[200:]))
+
+
+def test_fused_backbone_only_for_its_configuration(tf):
+    w = ts.workload("mingru2_h192_fourier15_d128_fp32_65k")
+    M, _ = _model(tf, w)
+    with pytest.raises(tf.TrackfitError):
+        M.set_fused(True)
+    M.set_fused(False)
+
+
 @pytest.mark.parametrize("name", ["mingru2_h192_fourier15_deploy_bf16_8m", "mingru2_h192_fourier15_d128_fp32_65k"])
 def test_mingru_chain_into_readout_and_decode(tf, name):
     """hits -> seed (features, seeds), backbone end states, the paper's
