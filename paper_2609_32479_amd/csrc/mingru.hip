@@ -574,8 +574,10 @@ void tf_backbone_kernel(const float *__restrict__ feats, int nf, long long n_hit
     unsigned taken = 0;
     for (;;) {
         int n = 0, off = 0, len = 0;
+        // (lane values read afresh per tile: held across the tile's layers they
+        // would take registers the last layer's operands need)
         const unsigned sel =
-            mg_select(offsets, g_end, row0, x_rows, n_hits, lane, t, taken, errbits, states, H, n, off, len);
+            mg_select(offsets, g_end, row0, x_rows, n_hits, fresh_lane(), t, taken, errbits, states, H, n, off, len);
         const int k = __builtin_popcount(sel);
         const bool work = k > 0;
         wait_vmcnt<0>();
@@ -587,8 +589,8 @@ void tf_backbone_kernel(const float *__restrict__ feats, int nf, long long n_hit
 
         unsigned sb0 = 0, sb1 = 0, eb0 = 0, eb1 = 0, st0 = 0, st1 = 0;
         if (work)
-            mg_tile_meta(sel, n, off, len, t, row0, lane, t_start, t_len, t_off, t_id, rowmap, sb0, sb1, eb0, eb1,
-                         st0, st1);
+            mg_tile_meta(sel, n, off, len, t, row0, fresh_lane(), t_start, t_len, t_off, t_id, rowmap, sb0, sb1, eb0,
+                         eb1, st0, st1);
 
         // ---- front end: r = b + W f(u) for the hit of column cc (tile row
         // slot_to_hit(cc), the first layer's operand row cc); lane half hh forms
@@ -597,18 +599,19 @@ void tf_backbone_kernel(const float *__restrict__ feats, int nf, long long n_hit
             f32x16 r[4];
             float *us = reinterpret_cast<float *>(xa1);  // [32][kBbUStride]
             if (work) {
+                const int ln = fresh_lane(), h2 = ln >> 5, c2 = ln & 31;
                 const float *fp = reinterpret_cast<const float *>(slot() + C::PARAM_OFF);  // bias, lo, 1 / span
-                const int xr = rowmap[slot_to_hit<SP>(cc)];
+                const int xr = rowmap[slot_to_hit<SP>(c2)];
                 const float *hp = xr >= 0 ? feats + (size_t)(xr + row0) * nf : nullptr;
 #pragma unroll
                 for (int e = 0; e < 8; ++e) {
-                    const int f = 8 * hh + e;
-                    if (f < nf) us[cc * kBbUStride + f] = hp ? (hp[f] - fp[D + f]) * fp[D + kBbMaxFeat + f] : 0.f;
+                    const int f = 8 * h2 + e;
+                    if (f < nf) us[c2 * kBbUStride + f] = hp ? (hp[f] - fp[D + f]) * fp[D + kBbMaxFeat + f] : 0.f;
                 }
 #pragma unroll
                 for (int m = 0; m < 4; ++m)
 #pragma unroll
-                    for (int qq = 0; qq < 16; ++qq) r[m][qq] = fp[32 * m + 16 * (qq >> 3) + 8 * hh + (qq & 7)];
+                    for (int qq = 0; qq < 16; ++qq) r[m][qq] = fp[32 * m + 16 * (qq >> 3) + 8 * h2 + (qq & 7)];
                 wave_lds_sync();  // the features are in the tile
             }
             // k-step ks takes, for this lane's column, the features k = 16 ks + 8 hh + e
