@@ -80,9 +80,10 @@ TRAFFIC = {
         "fetch_bytes": 59022801, "write_bytes": 270794752, "mfma_util": 0.327, "valu_busy": 0.603,
         "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
+        # the backbone call: one tf_backbone_kernel launch (front end and both layers)
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "b7027a4e3f1f5987567df6a6d20a021c115edc78b2be15ffd5c23f534123a72d",
-        "fetch_bytes": 4281905928, "write_bytes": 4792703472,
+        "sha256": "7f1dc1bb4018eb5f8b3e7f861d847a8827537337578c71b868e862afa621bf80",
+        "fetch_bytes": 254038346, "write_bytes": 402653184, "mfma_util": 0.330, "valu_busy": 0.356,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
@@ -568,6 +569,11 @@ def bench_paper(args, w, hits, offs, mode, batch):
     blob = ts.make_mingru_weights(w)
     hb = ts.make_readout_weights(w)
     M = tf.MinGRU(blob, w.n_layers, w.d_model, H, mode, w.n_features)
+    try:
+        M.set_fused(True)  # the paper's deployed configuration: one fused backbone launch
+        fused = True
+    except tf.TrackfitError:
+        fused = False
     R = tf.Readout(hb, *ts.readout_dims(w), mode)
     feats = device_features(tf, w, hits, offs, h, o, dev)
     seeds = torch.empty((n_tracks, 5), dtype=torch.float64, device=dev)
@@ -645,12 +651,17 @@ def bench_paper(args, w, hits, offs, mode, batch):
                  + "; seed and decode f64",
         "data": "synthetic helix tracks (2 T solenoid, seeded), synthetic per-hit features, random-init weights",
         "config": {"workload": w.name, "n_tracks": n_tracks, "batch": batch, "calls_per_step": len(starts),
-                   "launches_per_call": 5, "n_hits": n_hits, "n_layers": w.n_layers, "d_model": w.d_model,
-                   "hidden": H, "n_features": w.n_features, "mode": mode, "hip_graph": graph is not None},
+                   "launches_per_call": 3 if fused else 3 + w.n_layers, "n_hits": n_hits, "n_layers": w.n_layers,
+                   "d_model": w.d_model, "hidden": H, "n_features": w.n_features, "mode": mode,
+                   "fused_backbone": fused, "hip_graph": graph is not None},
         "roofline": {"bound": "mfma", "achieved": achieved, "peak": peak, "unit": "TFLOP/s", "frac": achieved / peak,
                      "traffic": traffic_bytes("paper", w, batch, len(starts)),
+                     "mfma_util_counter": busy_counter("paper", w, batch, len(starts), "mfma_util"),
+                     "valu_busy_counter": busy_counter("paper", w, batch, len(starts), "valu_busy"),
                      "counters_profile": counter_profile("paper", w, batch, len(starts)),
-                     "kernel": "tf_mingru_states (front end + minGRU layers, 3 launches)",
+                     "kernel": "tf_mingru_states (" + ("tf_backbone_kernel: front end and both layers fused, 1 launch"
+                                                       if fused else f"front end + minGRU layers, {1 + w.n_layers} launches")
+                               + ")",
                      "kernel_avg_ms": call_avg, "flops_per_launch": per_call},
         "context": {"paper_h100_nvl_tracks_per_s": PAPER_H100_TRACKS_PER_S,
                     "ratio_to_paper_h100": value / PAPER_H100_TRACKS_PER_S,
