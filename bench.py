@@ -760,12 +760,15 @@ def main():
             n = min(batch, n_tracks - s0)
             tf.fit_tracks(h, o[s0:], W, out=out[s0:], n_tracks=n, stream=stream)
 
-    # per-launch kernel time, eager, with events on the launch stream
+    # per-launch kernel time, eager, with events on the launch stream: the
+    # batches in turn, at least 8 launches (a one-batch workload would
+    # otherwise time a single launch, the first after idle)
     torch.cuda.synchronize()
     step()
     torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in starts]
-    for (a, b), s0 in zip(ev, starts):
+    timed = [starts[i % len(starts)] for i in range(max(len(starts), 8))]
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in timed]
+    for (a, b), s0 in zip(ev, timed):
         a.record()
         tf.fit_tracks(h, o[s0:], W, out=out[s0:], n_tracks=min(batch, n_tracks - s0))
         b.record()
