@@ -460,7 +460,8 @@ hipError_t launch_last(bool last, const void *X, long long x_rows, const int32_t
 // Stage sequence of a tile: the front end's projection (KPF k-steps of all
 // four channel blocks per stage; the first stage also holds the bias and the
 // features' lo and 1 / (hi - lo)), the first layer's candidate and gate blocks
-// two to a stage, then the last layer's one to a stage.
+// of both directions of a chunk in one stage, then the last layer's blocks one
+// to a stage.
 // ---------------------------------------------------------------------------
 constexpr int kBbMaxFeat = 16;  // per-hit features, at most
 constexpr int kBbUStride = 17;  // LDS row stride of a hit's normalised features (floats)
@@ -474,7 +475,7 @@ struct BCfg {
     static constexpr int BLOCK1 = round_up(KIN1 * FRAG + 32 * 4, 16);
     static constexpr int BLOCK2 = round_up(KIN2 * FRAG + 32 * 4, 16);
     static constexpr int PARAM_BYTES = (D + 2 * kBbMaxFeat) * 4;
-    static constexpr int STAGE = round_up(cmax(BLOCK2, 2 * BLOCK1), kCopyBytes);
+    static constexpr int STAGE = round_up(cmax(BLOCK2, 4 * BLOCK1), kCopyBytes);
     static constexpr int KPF = (STAGE - PARAM_BYTES) / (4 * FRAG);  // front-end k-steps per stage
     static constexpr int PARAM_OFF = KPF * 4 * FRAG;
     static constexpr int COPIES = STAGE / kCopyBytes;
@@ -492,7 +493,7 @@ struct BCfg {
     static constexpr int WAVE0 = NSLOT * STAGE;
     static constexpr int FLAG_OFF = WAVE0 + WAVES * WAVE_BYTES;
     static constexpr int LDS_BYTES = FLAG_OFF + FLAG_BYTES;
-    static constexpr int L1_STAGES = 2 * NCHK, L2_STAGES = 4 * NCHK;
+    static constexpr int L1_STAGES = NCHK, L2_STAGES = 4 * NCHK;
     static_assert(NSLOT >= 2 && KPF >= 1, "stage ring");
     static_assert(kMgCap * kBbUStride * 4 <= KIN1 * FRAG, "features in the operand area");
 };
@@ -678,7 +679,7 @@ void tf_backbone_kernel(const float *__restrict__ feats, int nf, long long n_hit
         for (int b = 0; b < 2 * NCHK; ++b) {
             const int ch = b >> 1, dir = b & 1;
             if (work) {
-                const char *sl = slot();
+                const char *sl = slot() + 2 * dir * C::BLOCK1;  // both directions of a chunk per stage
                 const FT *wc = reinterpret_cast<const FT *>(sl);
                 const FT *wg = reinterpret_cast<const FT *>(sl + C::BLOCK1);
                 f32x16 ax, gx;
@@ -720,7 +721,7 @@ void tf_backbone_kernel(const float *__restrict__ feats, int nf, long long n_hit
                 xa2[12 * dir + 2 * ch] = *reinterpret_cast<const FT *>(row);
                 xa2[12 * dir + 2 * ch + 1] = *reinterpret_cast<const FT *>(row + 16);
             }
-            advance(false);
+            if (dir == 1) advance(false);
             __builtin_amdgcn_sched_barrier(0);  // blocks one after the other (registers)
         }
 
@@ -1028,8 +1029,8 @@ extern "C" tf_status tf_mingru_create(const tf_mingru_config *cfg, const float *
                     put_block(dst, W, b, din, rbase, part == 1);
                     dst += (g.merge && part == 0) ? g.block : (g.merge ? g.stage - g.block : g.stage);
                     if (fusable) {
-                        put_block(fdst + (l == 0 && part == 1 ? BC::BLOCK1 : 0), W, b, din, rbase, part == 1);
-                        fdst += l == 0 ? (part == 1 ? BC::STAGE : 0) : BC::STAGE;
+                        put_block(fdst + (l == 0 ? (2 * dir + part) * BC::BLOCK1 : 0), W, b, din, rbase, part == 1);
+                        fdst += l == 0 ? (dir == 1 && part == 1 ? BC::STAGE : 0) : BC::STAGE;
                     }
                 }
         lw += (size_t)4 * H * din + (size_t)4 * H;
