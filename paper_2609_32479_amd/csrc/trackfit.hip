@@ -162,7 +162,8 @@ enum { OUT_HEAD = 0, OUT_STATES = 1, OUT_FRONT = 2 };
 // barrier after the chunk's scans instead of before them.
 constexpr unsigned kLateWaveGroups = 1u;
 // Polls of a paired wave's flag before it gives up (far beyond any real wait:
-// each poll is an LDS read and a short sleep).
+// each poll is an LDS read and the shortest sleep, which measured 0.6 %
+// faster on 64-hit tracks than 64-cycle sleeps).
 constexpr int kPairSpinLimit = 1 << 20;
 constexpr int kUStride = 17;     // LDS row stride of a hit slot's normalised features (floats)
 
@@ -417,7 +418,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     pair_broken = true;
                     break;
                 }
-                __builtin_amdgcn_s_sleep(1);
+                __builtin_amdgcn_s_sleep(0);
             }
         }
         return buf[lane];
