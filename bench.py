@@ -48,42 +48,42 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # only while the SHA-256 of the listed kernel sources, concatenated, is the one
 # recorded and the launch shape is the recorded one; otherwise traffic is null.
 ENCODER_SRCS = ("trackfit.hip", "common.h")
-_ENC_SHA = "7f692f31995d1214dba91b089b6b0a785afb6a37ab309938858662dd02e7b6b5"
+_ENC_SHA = "298d89b73f14ee9ac8b8544676854a5c849743820c262ff37990eb2b314d2239"
 TRAFFIC = {
     # "profile": the summary in profiles/ that these figures come from (its
     # trace, counter runs and bench line were taken on one box in one session)
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 53177587, "write_bytes": 5548224,
+        "fetch_bytes": 53175731, "write_bytes": 5549648,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.369, "valu_busy": 0.583,
+        "mfma_util": 0.367, "valu_busy": 0.582,
         "profile": "profiles/tf_encoder_kernel_deploy_d128x4_bf16_8m.md"},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 233129047, "write_bytes": 9439984, "mfma_util": 0.381, "valu_busy": 0.558,
+        "fetch_bytes": 233132631, "write_bytes": 9412592, "mfma_util": 0.380, "valu_busy": 0.549,
         "profile": "profiles/tf_encoder_kernel_fourier15_deploy_d128x4_bf16_8m.md"},
     ("encoder", "d128x4_fp32_65k"): {
         "srcs": ENCODER_SRCS, "batch": 65536, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 22524835, "write_bytes": 1386592, "mfma_util": 0.603, "valu_busy": 0.177,
+        "fetch_bytes": 22526627, "write_bytes": 1389440, "mfma_util": 0.600, "valu_busy": 0.176,
         "profile": "profiles/tf_encoder_kernel_d128x4_fp32_65k.md"},
     ("encoder", "d256x6_bf16_1m"): {
         "srcs": ENCODER_SRCS, "batch": 1048576, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 320208377, "write_bytes": 99553504, "mfma_util": 0.275, "valu_busy": 0.292,
+        "fetch_bytes": 320451308, "write_bytes": 99602592, "mfma_util": 0.276, "valu_busy": 0.293,
         "profile": "profiles/tf_encoder_kernel_d256x6_bf16_1m.md"},
     ("encoder", "long64_d128x4_bf16_200k"): {
         "srcs": ENCODER_SRCS, "batch": 200000, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 162475143, "write_bytes": 4051552, "mfma_util": 0.293, "valu_busy": 0.547,
+        "fetch_bytes": 162480390, "write_bytes": 4053520, "mfma_util": 0.297, "valu_busy": 0.552,
         "profile": "profiles/tf_encoder_kernel_long64_d128x4_bf16_200k.md"},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 59022801, "write_bytes": 270794752, "mfma_util": 0.327, "valu_busy": 0.603,
+        "fetch_bytes": 59025297, "write_bytes": 270794752, "mfma_util": 0.326, "valu_busy": 0.601,
         "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         # the backbone call: one tf_backbone_kernel launch (front end and both layers)
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "7f1dc1bb4018eb5f8b3e7f861d847a8827537337578c71b868e862afa621bf80",
-        "fetch_bytes": 254038346, "write_bytes": 402653184, "mfma_util": 0.330, "valu_busy": 0.356,
+        "sha256": "14e62999d0f84c9b1c967a608fc297b39810722d1d366570ca6dc190bb66b624",
+        "fetch_bytes": 256018984, "write_bytes": 402653184, "mfma_util": 0.329, "valu_busy": 0.356,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
