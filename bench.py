@@ -82,7 +82,7 @@ TRAFFIC = {
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         # the backbone call: one tf_backbone_kernel launch (front end and both layers)
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "14e62999d0f84c9b1c967a608fc297b39810722d1d366570ca6dc190bb66b624",
+        "sha256": "72e9fcf61bee4474bce0658af2ebd6a3db3b27943c72ee81ee6faaa41b7fb28f",
         "fetch_bytes": 256018984, "write_bytes": 402653184, "mfma_util": 0.329, "valu_busy": 0.356,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }

@@ -504,6 +504,13 @@ struct BCfg {
 __host__ __device__ constexpr int bb_front_channel(int rho) {
     return 16 * ((4 * (rho >> 3) + (rho & 3)) >> 3) + 8 * ((rho >> 2) & 1) + ((4 * (rho >> 3) + (rho & 3)) & 7);
 }
+// (a permutation of the block's 32 channels)
+constexpr bool bb_front_channel_is_permutation() {
+    unsigned seen = 0;
+    for (int rho = 0; rho < 32; ++rho) seen |= 1u << bb_front_channel(rho);
+    return seen == ~0u;
+}
+static_assert(bb_front_channel_is_permutation(), "front-end row order");
 
 template <int OP>
 __global__ __attribute__((amdgpu_flat_work_group_size(64 * BCfg<OP>::WAVES, 64 * BCfg<OP>::WAVES),
