@@ -169,6 +169,40 @@ def test_fused_backbone_matches_layered_launches_bitwise(tf, mode):
     assert np.array_equal(a3[:200], a[:200]) and np.all(np.isnan(a3[200:]))
 
 
+@pytest.mark.parametrize("nf", [5, 16])
+def test_fused_backbone_other_feature_counts(tf, nf):
+    """The fused backbone's front end with other feature counts (a partly
+    filled last front-end stage, and the most features): end states bitwise
+    those of the layered launches, in both 16-bit modes."""
+    rng = np.random.default_rng(11 + nf)
+    lo = rng.uniform(-2.0, 0.0, nf).astype(np.float32)
+    hi = (lo + rng.uniform(0.5, 3.0, nf)).astype(np.float32)
+    parts = []
+    for _, shape, fan_in, kind in ts.mingru_layout(2, 128, 192, nf):
+        n = int(np.prod(shape))
+        if kind == "lo":
+            parts.append(lo)
+        elif kind == "hi":
+            parts.append(hi)
+        elif kind == "w":
+            parts.append(rng.normal(0.0, fan_in ** -0.5, n))
+        else:
+            parts.append(rng.uniform(-fan_in ** -0.5, fan_in ** -0.5, n))
+    blob = np.concatenate(parts).astype(np.float32)
+    w = dataclasses.replace(ts.workload("mingru2_h192_fourier15_deploy_bf16_8m"), len_min=1, len_max=32,
+                            n_det_layers=32)
+    _, offs = ts.make_tracks(w, n_tracks=700)
+    feats = (lo + (hi - lo) * rng.random((int(offs[-1]), nf))).astype(np.float32)
+    for mode in ("bf16_f16act", "bf16"):
+        print(f"[fused] nf={nf} {mode}", flush=True)
+        M = tf.MinGRU(blob, 2, 128, 192, mode, nf)
+        a = _gpu(M, feats, offs)
+        M.set_fused(False)
+        b = _gpu(M, feats, offs)
+        assert np.array_equal(a, b) and np.isfinite(a).all()
+        assert M.device_error() == 0
+
+
 def test_fused_backbone_only_for_its_configuration(tf):
     w = ts.workload("mingru2_h192_fourier15_d128_fp32_65k")
     M, _ = _model(tf, w)
