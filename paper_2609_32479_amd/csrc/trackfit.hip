@@ -82,9 +82,14 @@ struct KCfg {
     static constexpr int KPB = 32 / K;           // k-steps per 32-channel block
     static constexpr int EB = HALF ? 2 : 4;      // operand element bytes
     static constexpr int FRAG = 64 * KL * EB;    // one wave-wide operand fragment
-    // waves per workgroup and per SIMD
-    static constexpr int WAVES = (HALF && HT == 1 && D <= 128) ? 12 : 4;
-    // Three waves per SIMD leave 168 registers a wave.  Under that budget the
+    // waves per workgroup (three per SIMD for the 16-bit d <= 128 kernels; two
+    // where the registers of two waves fit: d = 256 with fp16 activations
+    // (-26 % time per launch against one wave) and the fp32 d = 128 model
+    // (-10 %); one for the rest)
+    static constexpr int WAVES = (HALF && HT == 1 && D <= 128)                                   ? 12
+                                 : (HT == 1 && ((OP == OP_F16 && D == 256) || (!HALF && D == 128))) ? 8
+                                                                                                      : 4;
+    // Three waves per SIMD leave 168 registers a wave, two 256.  Under that budget the
     // kernel re-derives lane-dependent values where they are used and defines
     // its per-tile register arrays on every path, so that nothing is held (or
     // spilled) across tiles.
@@ -513,13 +518,14 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     for (int q = 0; q < 16; ++q) r[m][nt][q] = 0.f;
         }
         if (work) {
-            const bool mine = lane < WIN && ((sel >> (lane & 31)) & 1u);
+            const int ln = C::TIGHT ? fresh_lane() : lane;
+            const bool mine = ln < WIN && ((sel >> (ln & 31)) & 1u);
             const int v = mine ? len : 0;
             int incl = v;  // inclusive prefix sum of the selected lengths over lanes
 #pragma unroll
             for (int d = 1; d < WIN; d <<= 1) {
                 const int y = __shfl_up(incl, d);
-                if (lane >= d) incl += y;
+                if (ln >= d) incl += y;
             }
             const int row0 = incl - v;
             if (mine) {
@@ -527,7 +533,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                 t_start[j] = row0;
                 t_len[j] = len;
                 t_off[j] = off;
-                t_id[j] = t + lane;
+                t_id[j] = t + ln;
             }
             unsigned long long smask = 0;  // tile rows that start a track
             for (unsigned m = sel; m; m &= m - 1u) smask |= 1ull << __builtin_amdgcn_readlane(row0, __builtin_ctz(m));
