@@ -48,42 +48,42 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # only while the SHA-256 of the listed kernel sources, concatenated, is the one
 # recorded and the launch shape is the recorded one; otherwise traffic is null.
 ENCODER_SRCS = ("trackfit.hip", "common.h")
-_ENC_SHA = "298d89b73f14ee9ac8b8544676854a5c849743820c262ff37990eb2b314d2239"
+_ENC_SHA = "48e94efaf89516c8a1a5ae54687962bd97d2f6a304388643b869b8ef63a15f2f"
 TRAFFIC = {
     # "profile": the summary in profiles/ that these figures come from (its
     # trace, counter runs and bench line were taken on one box in one session)
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 53175731, "write_bytes": 5549648,
+        "fetch_bytes": 53176755, "write_bytes": 5578096,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.367, "valu_busy": 0.582,
+        "mfma_util": 0.370, "valu_busy": 0.587,
         "profile": "profiles/tf_encoder_kernel_deploy_d128x4_bf16_8m.md"},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 233132631, "write_bytes": 9412592, "mfma_util": 0.380, "valu_busy": 0.549,
+        "fetch_bytes": 233132695, "write_bytes": 9522704, "mfma_util": 0.386, "valu_busy": 0.565,
         "profile": "profiles/tf_encoder_kernel_fourier15_deploy_d128x4_bf16_8m.md"},
     ("encoder", "d128x4_fp32_65k"): {
         "srcs": ENCODER_SRCS, "batch": 65536, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 22526627, "write_bytes": 1389440, "mfma_util": 0.600, "valu_busy": 0.176,
+        "fetch_bytes": 22473957, "write_bytes": 1519888, "mfma_util": 0.655, "valu_busy": 0.175,
         "profile": "profiles/tf_encoder_kernel_d128x4_fp32_65k.md"},
     ("encoder", "d256x6_bf16_1m"): {
         "srcs": ENCODER_SRCS, "batch": 1048576, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 320451308, "write_bytes": 99602592, "mfma_util": 0.276, "valu_busy": 0.293,
+        "fetch_bytes": 479580761, "write_bytes": 88990384, "mfma_util": 0.432, "valu_busy": 0.351,
         "profile": "profiles/tf_encoder_kernel_d256x6_bf16_1m.md"},
     ("encoder", "long64_d128x4_bf16_200k"): {
         "srcs": ENCODER_SRCS, "batch": 200000, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 162480390, "write_bytes": 4053520, "mfma_util": 0.297, "valu_busy": 0.552,
+        "fetch_bytes": 162486022, "write_bytes": 4057136, "mfma_util": 0.297, "valu_busy": 0.552,
         "profile": "profiles/tf_encoder_kernel_long64_d128x4_bf16_200k.md"},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 59025297, "write_bytes": 270794752, "mfma_util": 0.326, "valu_busy": 0.601,
+        "fetch_bytes": 59044496, "write_bytes": 270794752, "mfma_util": 0.329, "valu_busy": 0.610,
         "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         # the backbone call: one tf_backbone_kernel launch (front end and both layers)
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "72e9fcf61bee4474bce0658af2ebd6a3db3b27943c72ee81ee6faaa41b7fb28f",
-        "fetch_bytes": 256018984, "write_bytes": 402653184, "mfma_util": 0.329, "valu_busy": 0.356,
+        "sha256": "5f808f5b77be3e93ded685aab4760d4b61d67805d15910d6cf6f381165a6973f",
+        "fetch_bytes": 255968874, "write_bytes": 402653184, "mfma_util": 0.329, "valu_busy": 0.361,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
