@@ -1363,12 +1363,18 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     for (int q = 0; q < 16; ++q) hid[m][q] = 0.f;
             }
             const int prow = cc < MAXTR ? cc : MAXTR - 1;  // columns past the tile's tracks repeat the last
+            const bool hw = work && OUTM == OUT_HEAD;  // rows to pool
+            // this wave's head tracks: all of the tile's, or (PAIR) 16 pb .. 16 pb + 15;
+            // a wave with none (the second of a pair whose tile holds at most 16
+            // tracks) still stores its rows for its partner, then skips the head
+            const int tr0 = C::PAIR ? 16 * pb : 0;
+            const int tr1 = C::PAIR ? (k < tr0 + 16 ? k : tr0 + 16) : k;
+            const bool hc = hw && tr1 > tr0;
             // unrolled, so that the residual block pooled at each step is a fixed register block
 #pragma unroll
             for (int j = 0; j < C::NH1; ++j) {
                 // (PAIR: a pair pools the rows of both its waves, so every wave takes
                 // the workgroup barriers between writing and reading them)
-                const bool hw = work && OUTM == OUT_HEAD;
                 if (C::PAIR || hw) {
                     const FT *w1 = reinterpret_cast<const FT *>(slot());
 #pragma unroll
@@ -1399,10 +1405,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                             lds_barrier();
                         else
                             wave_lds_sync();
-                        if (!hw) continue;
-                        // this wave's head tracks: all of the tile's, or (PAIR) 16 pb .. 16 pb + 15
-                        const int tr0 = C::PAIR ? 16 * pb : 0;
-                        const int tr1 = C::PAIR ? (k < tr0 + 16 ? k : tr0 + 16) : k;
+                        if (!hc) continue;
                         for (int tr = tr0 + hh; tr < tr1; tr += 2) {
                             const int s0 = t_start[tr], len = t_len[tr];
                             // in order of u, eight independent reads at a time (rows past the
@@ -1450,7 +1453,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                         }
                     }
                     if constexpr (C::HEAD16) {
-                      if (hw && j == C::NH1 - 1) {
+                      if (hc && j == C::NH1 - 1) {
                         // bias and SiLU: lane (hg, hcol) holds units 16 ub + 4 hg + i of track hcol
                         const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
@@ -1462,7 +1465,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                                                                       __builtin_amdgcn_fmed3f(-v * kLog2e, -kGateClamp, kGateClamp)));
                             }
                       }
-                    } else if (hw && j == C::NH1 - 1) {
+                    } else if (hc && j == C::NH1 - 1) {
                         // bias and SiLU: lane (hh, cc) holds units 32 mu + 8 (q/4) + 4 hh + (q%4) of track cc
                         const float *b1 = reinterpret_cast<const float *>(slot() + C::KSPS * MT * C::FRAG);
 #pragma unroll
@@ -1485,7 +1488,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
             // ---- head layer 2: out^T = W2 hid^T; the accumulators of hid^T are its B
             // operand, output row q of column cc is output q of track cc
             if constexpr (C::HEAD16) {
-              if (work && OUTM == OUT_HEAD) {
+              if (hc) {
                 // k-step kb takes the lane's units of blocks 2 kb and 2 kb + 1 (the
                 // stored W2 fragments follow that order); output rows 4 hg + i
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
@@ -1518,7 +1521,7 @@ void tf_encoder_kernel(const float *__restrict__ hits, long long n_hits_total, c
                     }
                 }
               }
-            } else if (work && OUTM == OUT_HEAD) {
+            } else if (hc) {
                 const FT *w2 = reinterpret_cast<const FT *>(slot());
                 const float *b2 = reinterpret_cast<const float *>(slot() + KS1 * C::FRAG);
                 f32x16 o;
