@@ -7,11 +7,15 @@
 // The last layer's forward state at a track's last hit and reverse state at
 // its first hit are the readout's input.
 //
-// One launch per layer.  The front end (x, y, z embedding or the Fourier
-// front end) runs first as the encoder kernel's front-end pass; each layer
-// reads its input rows X [rows][DIN] and writes Y [rows][2H] (rows relative to
-// offsets[0], in the matrix operand type), the last one the end states
-// [n_tracks][2H] in fp32.
+// Two ways to run it.  The paper's deployed configuration (16-bit modes,
+// Fourier front end, d = 128, H = 192, two layers) runs as one launch of
+// tf_backbone_kernel, which keeps the front end's output and the first
+// layer's states on chip (below).  Otherwise, and when asked for, one launch
+// per layer: the front end (x, y, z embedding or the Fourier front end) runs
+// first as the encoder kernel's front-end pass; each layer reads its input
+// rows X [rows][DIN] and writes Y [rows][2H] (rows relative to offsets[0], in
+// the matrix operand type), the last one the end states [n_tracks][2H] in
+// fp32.  Both compute the same bits.
 //
 // A wave takes a tile of whole tracks (at most 32 hits, 16 tracks), holds the
 // tile's input rows as matrix operands in registers (hits on the rows of
