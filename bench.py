@@ -48,42 +48,42 @@ COPY_MIB = 256  # plain copy kernel used to calibrate the HBM byte counters
 # only while the SHA-256 of the listed kernel sources, concatenated, is the one
 # recorded and the launch shape is the recorded one; otherwise traffic is null.
 ENCODER_SRCS = ("trackfit.hip", "common.h")
-_ENC_SHA = "48e94efaf89516c8a1a5ae54687962bd97d2f6a304388643b869b8ef63a15f2f"
+_ENC_SHA = "03e1d19e9cfae1e6cc4e58be2f7d10039fa15c30ceb82f4b6f7b52c4b856a3d3"
 TRAFFIC = {
     # "profile": the summary in profiles/ that these figures come from (its
     # trace, counter runs and bench line were taken on one box in one session)
     ("encoder", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 53176755, "write_bytes": 5578096,
+        "fetch_bytes": 53177331, "write_bytes": 5578880,
         # rocprofv3's derived MfmaUtil (matrix-unit busy cycles over SIMD cycles) and
         # VALUBusy (cycles issuing vector instructions), medians over launches
-        "mfma_util": 0.370, "valu_busy": 0.587,
+        "mfma_util": 0.367, "valu_busy": 0.582,
         "profile": "profiles/tf_encoder_kernel_deploy_d128x4_bf16_8m.md"},
     ("encoder", "fourier15_deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 233132695, "write_bytes": 9522704, "mfma_util": 0.386, "valu_busy": 0.565,
+        "fetch_bytes": 233133847, "write_bytes": 9522144, "mfma_util": 0.383, "valu_busy": 0.559,
         "profile": "profiles/tf_encoder_kernel_fourier15_deploy_d128x4_bf16_8m.md"},
     ("encoder", "d128x4_fp32_65k"): {
         "srcs": ENCODER_SRCS, "batch": 65536, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 22473957, "write_bytes": 1519888, "mfma_util": 0.655, "valu_busy": 0.175,
+        "fetch_bytes": 22474213, "write_bytes": 1520192, "mfma_util": 0.656, "valu_busy": 0.175,
         "profile": "profiles/tf_encoder_kernel_d128x4_fp32_65k.md"},
     ("encoder", "d256x6_bf16_1m"): {
         "srcs": ENCODER_SRCS, "batch": 1048576, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 479580761, "write_bytes": 88990384, "mfma_util": 0.432, "valu_busy": 0.351,
+        "fetch_bytes": 478426450, "write_bytes": 88989104, "mfma_util": 0.434, "valu_busy": 0.351,
         "profile": "profiles/tf_encoder_kernel_d256x6_bf16_1m.md"},
     ("encoder", "long64_d128x4_bf16_200k"): {
         "srcs": ENCODER_SRCS, "batch": 200000, "calls_per_step": 1, "sha256": _ENC_SHA,
-        "fetch_bytes": 162486022, "write_bytes": 4057136, "mfma_util": 0.297, "valu_busy": 0.552,
+        "fetch_bytes": 162485638, "write_bytes": 4057664, "mfma_util": 0.295, "valu_busy": 0.545,
         "profile": "profiles/tf_encoder_kernel_long64_d128x4_bf16_200k.md"},
     ("readout", "deploy_d128x4_bf16_8m"): {
         "srcs": ENCODER_SRCS, "batch": 262144, "calls_per_step": 32, "sha256": _ENC_SHA,
-        "fetch_bytes": 59044496, "write_bytes": 270794752, "mfma_util": 0.329, "valu_busy": 0.610,
+        "fetch_bytes": 59044752, "write_bytes": 270794752, "mfma_util": 0.326, "valu_busy": 0.602,
         "profile": "profiles/readout_path_deploy_d128x4_bf16_8m.md"},
     ("paper", "mingru2_h192_fourier15_deploy_bf16_8m"): {
         # the backbone call: one tf_backbone_kernel launch (front end and both layers)
         "srcs": ENCODER_SRCS + ("mingru.hip",), "batch": 262144, "calls_per_step": 32,
-        "sha256": "5f808f5b77be3e93ded685aab4760d4b61d67805d15910d6cf6f381165a6973f",
-        "fetch_bytes": 255968874, "write_bytes": 402653184, "mfma_util": 0.329, "valu_busy": 0.361,
+        "sha256": "e4a021b3ba6e36bab6b1991c81e2f8484491bd1bef565a312373c60ec51d6e10",
+        "fetch_bytes": 255927980, "write_bytes": 402653184, "mfma_util": 0.332, "valu_busy": 0.360,
         "profile": "profiles/paper_model_mingru2_h192_fourier15_deploy_bf16_8m.md"},
 }
 
