@@ -18,8 +18,8 @@ three launches per batch, the step again captured in one HIP graph.
 ``--path paper`` times the paper's own deployed model per batch (workload
 mingru2_h192_fourier15_deploy_bf16_8m): the seed writing the three seed
 features into the 15-feature rows, the Fourier front end and the two
-bidirectional minGRU layers (tf_mingru_states), and the 35-quantile readout
-with its decode, in one HIP graph.
+bidirectional minGRU layers (tf_mingru_states: one fused launch), and the
+35-quantile readout with its decode, in one HIP graph.
 """
 import argparse
 import json
