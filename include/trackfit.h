@@ -84,7 +84,8 @@ typedef struct {
 typedef struct tf_weights tf_weights;
 
 /*
- * Copy a canonical float32 weight blob to the current device.
+ * Copy a canonical float32 weight blob to the current device: the parameters
+ * of the encoder that fit_tracks evaluates (Sec. Encoder, Eq. (2) per layer).
  *
  * Blob order (matrices row-major [out][in]):
  *   embed.W[d][3], embed.b[d],
@@ -184,7 +185,8 @@ tf_status fit_tracks_states(const float *hits, int64_t n_hits, const int32_t *of
 
 /* Read (and if clear != 0, reset) the sticky device error word after the work
  * already enqueued on stream.  Synchronises stream.  *flags receives the OR of
- * TF_DEVERR_* bits seen since the last clear. */
+ * TF_DEVERR_* bits seen since the last clear.  (Library plumbing: no passage of
+ * the paper defines it; it reports the tracks the kernels refused.) */
 tf_status tf_get_device_error(const tf_weights *w, hipStream_t stream, int32_t *flags, int clear);
 
 /*
@@ -419,7 +421,8 @@ int64_t tf_mingru_noalloc_max_rows(const tf_mingru *h);
  * (TF_DEVERR_* bits).  Synchronises stream. */
 tf_status tf_mingru_device_error(const tf_mingru *h, hipStream_t stream, int32_t *flags, int clear);
 
-/* Static description of a status code. */
+/* Static description of a status code (library plumbing: no passage of the
+ * paper defines it). */
 const char *tf_status_string(tf_status s);
 
 #ifdef __cplusplus
