@@ -2,8 +2,8 @@
 against the fp64 oracle, element by element: end states on three workloads
 (the (x, y, z) front end at d = 32, H = 64 and the Fourier front end at the
 paper's d = 128, H = 192), ragged batches, rejected tracks, a workspace too
-small for the batch, tile independence, and the chain into the 35-quantile
-readout and decode.
+small for the batch, tile independence, the chain into the 35-quantile
+readout and decode, and that chain replayed from a HIP graph.
 """
 import dataclasses
 import os
@@ -236,3 +236,67 @@ def test_mingru_chain_into_readout_and_decode(tf, name):
     print(f"[mingru-chain] {name}: quantile err {eq.max():.3g} decoded err {eo.max():.3g}", flush=True)
     tq, _ = head_tols(mode, d, nh)
     assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]
+
+
+def test_paper_chain_graph_replays_match_eager(tf):
+    """The paper's chain per batch (seed with its hit features, the fused
+    backbone, readout and decode), captured in one HIP graph over three
+    batches (the last one ragged) as the benchmark runs it: every replay,
+    with eager work and synchronisations between the replays, gives the eager
+    chain's seeds, features and decoded outputs bit for bit."""
+    w = ts.MINGRU_WORKLOADS["mingru2_h192_fourier15_deploy_bf16_8m"]
+    hits, offs = ts.make_tracks(w, n_tracks=5000)
+    n, batch, H = offs.size - 1, 2048, w.hidden
+    mode = tf.MODE_FOR_WEIGHTS[w.dtype]
+    M, _ = _model(tf, w)
+    M.set_fused(True)
+    R = tf.Readout(ts.make_readout_weights(w), *ts.readout_dims(w), mode)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    feats = torch.zeros((int(offs[-1] - offs[0]), w.n_features), dtype=torch.float32, device="cuda")
+    feats[:, :ts.N_MEASURED] = torch.from_numpy(ts.measured_features(w, hits, offs)).cuda()
+    starts = list(range(0, n, batch))
+    rows = max(int(offs[min(s0 + batch, n)] - offs[s0]) for s0 in starts)
+    ws = torch.empty(M.workspace_bytes(rows), dtype=torch.uint8, device="cuda")
+    seeds = torch.empty((n, 5), dtype=torch.float64, device="cuda")
+    out = torch.empty((n, 5), dtype=torch.float64, device="cuda")
+    states = torch.empty((batch, 2 * H), dtype=torch.float32, device="cuda")
+
+    def step(stream=None):
+        for s0 in starts:
+            k = min(batch, n - s0)
+            r0 = int(offs[s0] - offs[0])
+            tf.seed_tracks(h, o[s0:], w.b_field, seeds=seeds[s0:], n_tracks=k, stream=stream,
+                           feats=feats[r0:, ts.N_MEASURED:ts.N_MEASURED + 3])
+            M.states(feats, o[s0:], out=states, workspace=ws, n_tracks=k, stream=stream)
+            tf.decode_tracks(states[:k], seeds[s0:s0 + k], R, out=out[s0:], stream=stream)
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.cpu().numpy().copy() for t in (seeds, feats, out)]
+    assert np.isfinite(ref[2]).mean() > 0.99
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        step(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            step(side)
+    torch.cuda.synchronize()
+
+    def clear():
+        for t in (seeds, out, states):
+            t.fill_(float("nan"))
+        feats[:, ts.N_MEASURED:].fill_(float("nan"))
+
+    for rep in range(3):
+        clear()
+        step()  # eager work between the replays
+        torch.cuda.synchronize()
+        clear()  # everything the replay must write again
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [t.cpu().numpy() for t in (seeds, feats, out)]
+        for name, a, b in zip(("seeds", "features", "decoded"), got, ref):
+            assert np.array_equal(a, b, equal_nan=True), f"replay {rep}: {name}"
