@@ -332,3 +332,58 @@ def test_seed_states_decode_end_to_end(tf, name):
     # the quantiles carry the head's own rounding on top of the encoder's
     tq, _ = head_tols(mode, d, nh)
     assert eq.max() <= max(TOL[w.dtype], tq) and eo.max() <= TOL[w.dtype]
+
+
+def test_readout_chain_graph_replays_match_eager(tf):
+    """The readout path per batch (seed, the encoder's end states, readout and
+    decode), captured in one HIP graph over three batches (the last one
+    ragged) as the readout benchmark runs it: every replay, with eager work
+    and cleared outputs between the replays, gives the eager chain's seeds,
+    end states of the last batch and decoded outputs bit for bit."""
+    w = ts.WORKLOADS["deploy_d128x4_bf16_8m"]
+    hits, offs = ts.make_tracks(w, n_tracks=5000)
+    n, batch, d = offs.size - 1, 2048, w.d_model
+    mode = tf.MODE_FOR_WEIGHTS[w.dtype]
+    W = tf.Weights(ts.make_weights(w), w.n_layers, d, mode, max_hits=w.len_max)
+    R = tf.Readout(ts.make_readout_weights(w), *ts.readout_dims(w), mode)
+    h = torch.from_numpy(hits).cuda()
+    o = torch.from_numpy(offs).cuda()
+    seeds = torch.empty((n, 5), dtype=torch.float64, device="cuda")
+    out = torch.empty((n, 5), dtype=torch.float64, device="cuda")
+    states = torch.empty((batch, 2 * d), dtype=torch.float32, device="cuda")
+    starts = list(range(0, n, batch))
+
+    def step(stream=None):
+        for s0 in starts:
+            k = min(batch, n - s0)
+            tf.seed_tracks(h, o[s0:], w.b_field, features=False, seeds=seeds[s0:], n_tracks=k, stream=stream)
+            tf.fit_tracks_states(h, o[s0:], W, out=states, n_tracks=k, stream=stream)
+            tf.decode_tracks(states[:k], seeds[s0:s0 + k], R, out=out[s0:], stream=stream)
+
+    def clear():
+        for t in (seeds, out, states):
+            t.fill_(float("nan"))
+
+    step()
+    torch.cuda.synchronize()
+    ref = [t.cpu().numpy().copy() for t in (seeds, states, out)]
+    assert np.isfinite(ref[2]).mean() > 0.99
+    side = torch.cuda.Stream()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.stream(side):
+        step(side)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(g, stream=side):
+            step(side)
+    torch.cuda.synchronize()
+    for rep in range(3):
+        clear()
+        step()  # eager work between the replays
+        torch.cuda.synchronize()
+        clear()  # everything the replay must write again
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        got = [t.cpu().numpy() for t in (seeds, states, out)]
+        for name, a, b in zip(("seeds", "end states", "decoded"), got, ref):
+            assert np.array_equal(a, b, equal_nan=True), f"replay {rep}: {name}"
